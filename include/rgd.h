@@ -1,0 +1,243 @@
+/*
+ * rgd.h - C ABI of the MI355X (gfx950) refusal-gated decoding library.
+ *
+ * Refusal-gated decoding (Section 3, Algorithm 1): a prompt's KV cache is
+ * computed once and shared; a short greedy probe decodes against it and is
+ * checked after every token for compatibility with a table of refusal
+ * prefixes; a probe that stays compatible to a stop token or the length cap is
+ * returned as the greedy response, otherwise the probe's own positions are
+ * dropped and N high-temperature continuations are sampled from the prompt.
+ *
+ * Conventions (all entry points):
+ *  - Every function returns an rgd_status (int32).  On failure the reason is
+ *    available from rgd_last_error() (thread-local, valid until the next call
+ *    on the same thread).  Arguments are validated before any HIP call; an
+ *    invalid argument leaves all state untouched.
+ *  - "dev" pointers are device memory (e.g. PyTorch tensors on the GPU) and
+ *    "host" pointers ordinary host memory.  The caller owns every buffer it
+ *    passes; the library never frees them.  The library owns its handles and
+ *    the workspace it allocates in the *_create calls; no entry point on the
+ *    decode path allocates device memory.
+ *  - stream is a hipStream_t (NULL = the null stream).  Work is enqueued on it;
+ *    calls documented as synchronous wait for that stream.
+ *  - Layouts are row-major with the last index fastest.  bf16 values are IEEE
+ *    bfloat16 bit patterns, fp32 values IEEE binary32.
+ *  - Results are deterministic: reductions use a fixed order and no floating
+ *    point atomics, so equal inputs and seeds give bit-identical outputs.
+ */
+#ifndef RGD_H
+#define RGD_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct rgd_model rgd_model;
+typedef struct rgd_kv rgd_kv;
+typedef struct rgd_table rgd_table;
+typedef void* rgd_stream; /* hipStream_t */
+
+enum rgd_status {
+  RGD_OK = 0,
+  RGD_E_INVALID_ARG = 1, /* null pointer, size out of range, bad enum */
+  RGD_E_OOM = 2,         /* page pool or workspace exhausted */
+  RGD_E_HIP = 3,         /* a HIP runtime call failed */
+  RGD_E_UNSUPPORTED = 4, /* dtype or shape this build does not handle */
+  RGD_E_NONFINITE = 5,   /* a logit row had a non-finite maximum */
+  RGD_E_STATE = 6        /* entry points called out of order */
+};
+
+enum rgd_dtype { RGD_DTYPE_F32 = 0, RGD_DTYPE_BF16 = 1 };
+
+/* Decisive probe events (Algorithm 1: incompatibility, stop, length cap). */
+enum rgd_event { RGD_EVENT_INCOMPAT = 0, RGD_EVENT_STOP = 1, RGD_EVENT_MAXLEN = 2 };
+
+/* Target model M: a pre-norm decoder (RMSNorm, grouped-query attention with
+ * rotate-half RoPE, SwiGLU feed-forward, untied LM head).  The paper runs
+ * pretrained models of this family (Section 4).  d_model = n_heads * head_dim
+ * is not required; n_heads must be a multiple of n_kv_heads. */
+typedef struct rgd_model_config {
+  int32_t n_layers;
+  int32_t d_model;
+  int32_t n_heads;    /* query heads Hq */
+  int32_t n_kv_heads; /* key/value heads Hkv */
+  int32_t head_dim;   /* D */
+  int32_t ffn_dim;
+  int32_t vocab;
+  int32_t dtype;      /* rgd_dtype of weights, KV cache and activations */
+  float rms_eps;
+  float rope_theta;
+  int32_t max_pos;    /* largest position any call may use, exclusive */
+} rgd_model_config;
+
+/* Per-layer weights, device pointers in the model dtype, W[out][in] row-major
+ * (y = W x).  wq [Hq*D][d_model], wk/wv [Hkv*D][d_model], wo [d_model][Hq*D],
+ * w_gate/w_up [ffn][d_model], w_down [d_model][ffn].  Norm gains are fp32
+ * [d_model]. */
+typedef struct rgd_layer_weights {
+  const void* attn_norm;
+  const void* wq;
+  const void* wk;
+  const void* wv;
+  const void* wo;
+  const void* ffn_norm;
+  const void* w_gate;
+  const void* w_up;
+  const void* w_down;
+} rgd_layer_weights;
+
+/* embed [vocab][d_model] and lm_head [vocab][d_model] in the model dtype,
+ * final_norm fp32 [d_model]; layers is a host array of n_layers entries. */
+typedef struct rgd_weights {
+  const void* embed;
+  const void* final_norm;
+  const void* lm_head;
+  const rgd_layer_weights* layers;
+} rgd_weights;
+
+/* Library version string (static storage). */
+const char* rgd_version(void);
+
+/* Message for the last failing call on this thread ("" if none). */
+const char* rgd_last_error(void);
+
+/* Creates a model over caller-owned weights (not copied; they must outlive the
+ * handle).  max_rows bounds the rows of any decode step (probe prompts, or
+ * prompts x branches) and the tokens processed per prefill chunk; the
+ * workspace for that many rows is allocated here.  bf16 models require
+ * head_dim == 128 and d_model, Hq*D, ffn multiples of 128. */
+int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int32_t max_rows,
+                         rgd_model** out);
+void rgd_model_destroy(rgd_model* m);
+
+/* KV state for up to max_prompts prompts of up to max_prefix positions each.
+ *  prefix_k/prefix_v: dev [n_layers][max_prompts][max_prefix][Hkv][D] - the
+ *    shared prompt KV (rotated keys), written only by rgd_prefill_kv or by the
+ *    caller, read in place by every probe and branch, never copied.
+ *  pool_k/pool_v: dev [n_layers][n_pages][page_size][Hkv][D] - pages of the
+ *    per-row tails (probe positions, branch positions).
+ * The handle keeps per-prompt prefix lengths, page tables and the page free
+ * list.  All four buffers are caller owned. */
+int32_t rgd_kv_create(const rgd_model* m, int32_t max_prompts, int32_t max_prefix, int32_t n_pages,
+                      int32_t page_size, void* prefix_k, void* prefix_v, void* pool_k, void* pool_v,
+                      rgd_kv** out);
+void rgd_kv_destroy(rgd_kv* kv);
+
+/* Declares that positions [0, len) of prompt `prompt` hold valid KV written by
+ * the caller (e.g. a synthetic prefix).  Host-side bookkeeping only. */
+int32_t rgd_kv_set_prefix_len(rgd_kv* kv, int32_t prompt, int32_t len);
+
+/* Refusal-prefix table P (Section 3; token-level matching with a minimum match
+ * length, Appendix D), copied to the device.  CSR on the host: entry e is
+ * tokens[offsets[e] .. offsets[e+1]).  owner (host [n_entries] or NULL):
+ * owner[e] = -1 makes the entry apply to every prompt, p >= 0 to prompt p only.
+ * Entries shorter than min_match tokens never match.  n_entries may be 0 (every
+ * probe is then incompatible at its first token). */
+int32_t rgd_table_create(const int32_t* offsets, const int32_t* tokens, int32_t n_entries,
+                         const int32_t* owner, int32_t min_match, rgd_table** out);
+void rgd_table_destroy(rgd_table* t);
+
+/* Prefill (Algorithm 1, first line; the prompt KV reused by both stages):
+ * tokens dev int32 [B][n] for prompts 0..B-1 at positions
+ * [start_pos, start_pos + n); each prompt must already hold start_pos valid
+ * positions.  Writes their K/V into the prefix, sets each prefix length to
+ * start_pos + n and writes the logits of each prompt's last position to
+ * last_logits dev fp32 [B][vocab].  Asynchronous. */
+int32_t rgd_prefill_kv(rgd_model* m, rgd_kv* kv, const int32_t* tokens, int32_t B, int32_t n,
+                       int32_t start_pos, float* last_logits, rgd_stream stream);
+
+/* Greedy probe (Algorithm 1: the c-token gate G_M and the post-cap probe B_M)
+ * for prompts 0..B-1.  Token 1 is the argmax of last_logits (dev fp32
+ * [B][vocab]); each further token is the argmax after feeding the probe, whose
+ * K/V goes to pages of the prompt's probe tail.  After every token the probe
+ * is checked against tbl: incompatible -> INCOMPAT, token == eos_id (eos_id <
+ * 0: none) -> STOP, k tokens -> MAXLEN.  The host polls the device state after
+ * each of the first c tokens and then every c tokens, and stops launching
+ * steps once no prompt is undecided (early exit); the decision does not depend
+ * on c.  Outputs (dev): probe_tokens int32 [B][k], probe_len int32 [B],
+ * event int32 [B] (rgd_event).  Synchronous.  tbl may not be NULL. */
+int32_t rgd_probe(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_table* tbl,
+                  int32_t B, int32_t k, int32_t c, int32_t eos_id, int32_t* probe_tokens,
+                  int32_t* probe_len, int32_t* event, rgd_stream stream);
+
+/* Gate (Algorithm 1, the return branches): prompt b is a hit (return the
+ * greedy probe) iff event[b] is STOP or MAXLEN, otherwise a miss (sample from
+ * the prompt).  Releases every probe-tail page (the probe's K/V is dropped,
+ * never copied; the shared prefix is untouched).  event dev int32 [B].
+ * decision_host int32 [B] (1 = hit, 0 = miss), *n_miss_host, miss_idx_host
+ * int32 [B] (first *n_miss_host entries: missed prompts in increasing order).
+ * Synchronous. */
+int32_t rgd_gate(rgd_kv* kv, const int32_t* event, int32_t B, int32_t* decision_host,
+                 int32_t* n_miss_host, int32_t* miss_idx_host, rgd_stream stream);
+
+/* S_{T,theta}(M, p) (Section 3) with temperature-scaled min-p truncation for
+ * the n prompts listed in prompt_idx (host int32 [n]), N branches each, `steps`
+ * tokens per branch.  Branch j of listed prompt i is row r = i*N + j; it uses
+ * Philox key seeds[r] (dev uint64 [n*N]) and counter (s, 0) for token s.
+ * Token 0 is drawn from last_logits (dev fp32 [B][vocab], row prompt_idx[i]);
+ * token s >= 1 from the logits after feeding token s-1 at position
+ * prefix_len + s - 1 (the branch restarts from the prompt; probe positions are
+ * not visible).  T == 0 is greedy argmax.  A token i is kept iff
+ * exp((z_i - max z)/T) >= min_p; the draw is the smallest kept id whose running
+ * kept weight exceeds u * (total kept weight).
+ *  forced (dev int32 [n*N][steps] or NULL): if given, token forced[r][s-1] is
+ *    fed at step s instead of the drawn one (teacher forcing for tests).
+ *  logits_tap (dev fp32 [steps][n*N][vocab] or NULL): receives every step's
+ *    logits (tests).
+ *  out: dev int32 [n][N][steps].
+ * Asynchronous.  Requires every probe tail to have been released (rgd_gate). */
+int32_t rgd_sample_continuations(rgd_model* m, rgd_kv* kv, const float* last_logits,
+                                 const int32_t* prompt_idx, int32_t n, int32_t N, int32_t steps,
+                                 float T, float min_p, const uint64_t* seeds, const int32_t* forced,
+                                 float* logits_tap, int32_t* out, rgd_stream stream);
+
+/* Checks the device status flag raised by the sampler (non-finite row
+ * maximum) and clears it.  Synchronous. */
+int32_t rgd_check_status(rgd_model* m, rgd_stream stream);
+
+/* ---- kernel-level entry points (used by the tests and the benchmark) ---- */
+
+/* Decode attention for R rows of one layer: q dev [R][Hq][D] (model dtype)
+ * over prompt row_prompt[r]'s first plen[r] prefix positions followed by
+ * tail_len positions of the row's own tail.  row_prompt and plen are HOST int32
+ * [R]; rows of one prompt must be contiguous.  prefix_k/v dev
+ * [max_prompts][max_prefix][Hkv][D]; pool_k/v dev [n_pages][page_size][Hkv][D];
+ * pages dev int32 [R][max_pages] (may be NULL when tail_len == 0).  out dev
+ * [R][Hq*D] (model dtype).  splits = 0 picks the prefix split count.
+ * Asynchronous. */
+int32_t rgd_kernel_attention(rgd_model* m, const void* q, int32_t R, const int32_t* row_prompt,
+                             const int32_t* plen, const void* prefix_k, const void* prefix_v,
+                             int32_t max_prompts, int32_t max_prefix, const void* pool_k,
+                             const void* pool_v, int32_t page_size, const int32_t* pages,
+                             int32_t max_pages, int32_t tail_len, int32_t splits, void* out,
+                             rgd_stream stream);
+
+/* LM head: logits dev fp32 [R][vocab] = h W_lm^T with h dev [R][d_model]
+ * (model dtype, the already normalised final hidden state).  Asynchronous. */
+int32_t rgd_kernel_lm_head(rgd_model* m, const void* h, int32_t R, float* logits, rgd_stream stream);
+
+/* Bytes of caller-provided device workspace the two sampler entry points
+ * below need for R rows of V logits. */
+uint64_t rgd_sampler_workspace_bytes(int32_t R, int32_t V);
+
+/* Greedy token of each row of z dev fp32 [R][V] (first index of the maximum)
+ * -> out dev int32 [R].  workspace: dev, rgd_sampler_workspace_bytes(R, V)
+ * bytes, 256-byte aligned.  Asynchronous. */
+int32_t rgd_kernel_argmax(const float* z, int32_t R, int32_t V, void* workspace, int32_t* out,
+                          rgd_stream stream);
+
+/* min-p draws on z dev fp32 [R][V] (V a multiple of 4, V <= 1048576, T > 0,
+ * 0 <= min_p <= 1): draw d of row r uses Philox key seeds[r] (dev uint64 [R])
+ * and counter (ctr, stream0 + d); out dev int32 [R][draws].  workspace as for
+ * rgd_kernel_argmax.  Asynchronous. */
+int32_t rgd_kernel_sample(const float* z, int32_t R, int32_t V, float T, float min_p,
+                          const uint64_t* seeds, uint32_t ctr, uint32_t stream0, int32_t draws,
+                          void* workspace, int32_t* out, rgd_stream stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RGD_H */

@@ -76,3 +76,26 @@ def kept_probabilities(z, T: float, p_min: float) -> np.ndarray:
     w, kept = minp_weights(z, T, p_min)
     wk = np.where(kept, w, 0.0)
     return wk / wk.sum()
+
+
+def sample_minp_many(z, T: float, p_min: float, us) -> list:
+    """sample_minp for many uniforms on one row (same definition; the kept
+    weights and running sums are formed once)."""
+    z = np.asarray(z, dtype=np.float64)
+    w, kept = minp_weights(z, T, p_min)
+    wk = np.where(kept, w, 0.0)
+    total = wk.sum()
+    cdf = np.cumsum(wk)
+    kept_idx = np.flatnonzero(kept)
+    ck = cdf[kept_idx]
+    edges = np.concatenate(([0.0], ck))
+    lmarg = float(np.min(np.abs((z - z.max()) / T - math.log(p_min)))) if p_min > 0 else math.inf
+    out = []
+    for u in np.asarray(us, dtype=np.float64):
+        t = u * total
+        j = int(np.searchsorted(ck, t, side="right"))      # first kept running sum > t
+        tok = int(kept_idx[min(j, kept_idx.size - 1)])
+        k = int(np.searchsorted(edges, t))
+        near = edges[max(k - 1, 0):k + 1]
+        out.append(Draw(tok, lmarg, float(np.min(np.abs(near - t)) / total)))
+    return out

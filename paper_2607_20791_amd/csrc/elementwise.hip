@@ -1,0 +1,139 @@
+// Per-row kernels of the decode step: embedding gather, split-K reduction with
+// residual add and RMSNorm, and the Q/K/V epilogue (split-K reduction, rotary
+// embedding, store of q and append of k/v to the shared prefix or the row's
+// paged tail).
+#include "kernels.hpp"
+
+namespace rgd {
+
+namespace {
+
+template <typename T>
+__global__ __launch_bounds__(256) void embed_kernel(const int* tok, int tok_stride, const T* E, int d,
+                                                    int V, float* x) {
+  const int r = blockIdx.x;
+  // ids come from the sampler or the caller; clamp so that a bad id cannot read
+  // outside the embedding table
+  const long long t = min(max(tok[(long long)r * tok_stride], 0), V - 1);
+  for (int i = threadIdx.x; i < d; i += 256) x[(long long)r * d + i] = load_f(E + t * d + i);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void residual_rmsnorm_kernel(float* x, const float* parts, int nparts,
+                                                               long long part_stride, const float* g,
+                                                               float eps, int d, T* xn) {
+  __shared__ float red[4];
+  const int r = blockIdx.x;
+  float* xr = x + (long long)r * d;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d; i += 256) {
+    float v = xr[i];
+    for (int p = 0; p < nparts; ++p) v += parts[p * part_stride + (long long)r * d + i];
+    xr[i] = v;
+    ss += v * v;
+  }
+  ss = block_sum(ss, red);
+  const float inv = rsqrtf(ss / float(d) + eps);
+  for (int i = threadIdx.x; i < d; i += 256) store_f(xn + (long long)r * d + i, xr[i] * inv * g[i]);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void qkv_rope_kernel(const float* parts, int nparts, long long part_stride,
+                                                       Rows rows, int Hq, int Hkv, int D, float theta,
+                                                       T* q, KVLayout kv) {
+  __shared__ float cs[128], sn[128];
+  const int r = blockIdx.x;
+  const int half = D / 2;
+  const int pos = rows.prefill ? rows.base_pos[r] : rows.base_pos[r] + rows.t;
+  for (int j = threadIdx.x; j < half; j += 256) {
+    // angle in fp64: pos * theta^(-2j/D), reduced mod 2*pi before the fp32 sin/cos
+    const double ang = double(pos) * pow(double(theta), -2.0 * double(j) / double(D));
+    const double red = ang - 6.283185307179586 * floor(ang / 6.283185307179586);
+    double s, c;
+    sincos(red, &s, &c);
+    cs[j] = float(c);
+    sn[j] = float(s);
+  }
+  __syncthreads();
+  const int nqkv = (Hq + 2 * Hkv) * D;
+  const float* pr = parts + (long long)r * nqkv;
+  auto col = [&](int c) {
+    float v = 0.f;
+    for (int p = 0; p < nparts; ++p) v += pr[p * part_stride + c];
+    return v;
+  };
+  // destination of this row's new K/V
+  const int b = rows.prompt[r];
+  long long kv_off;
+  T* kd;
+  T* vd;
+  if (rows.prefill) {
+    kv_off = ((long long)b * kv.P + pos) * Hkv * D;
+    kd = (T*)kv.prefix_k;
+    vd = (T*)kv.prefix_v;
+  } else {
+    const int page = rows.pages[(long long)r * rows.max_pages + rows.t / kv.page_size];
+    kv_off = ((long long)page * kv.page_size + rows.t % kv.page_size) * Hkv * D;
+    kd = (T*)kv.pool_k;
+    vd = (T*)kv.pool_v;
+  }
+  // rotated q and k: pairs (j, j + D/2) of each head
+  const int npairs = (Hq + Hkv) * half;
+  for (int i = threadIdx.x; i < npairs; i += 256) {
+    const int h = i / half, j = i % half;
+    const int base = h * D;  // q heads then k heads are contiguous in the fused output
+    const float x1 = col(base + j), x2 = col(base + j + half);
+    const float y1 = x1 * cs[j] - x2 * sn[j];
+    const float y2 = x2 * cs[j] + x1 * sn[j];
+    if (h < Hq) {
+      T* qr = q + ((long long)r * Hq + h) * D;
+      store_f(qr + j, y1);
+      store_f(qr + j + half, y2);
+    } else {
+      T* kr = kd + kv_off + (long long)(h - Hq) * D;
+      store_f(kr + j, y1);
+      store_f(kr + j + half, y2);
+    }
+  }
+  const int vbase = (Hq + Hkv) * D;
+  for (int i = threadIdx.x; i < Hkv * D; i += 256) store_f(vd + kv_off + i, col(vbase + i));
+}
+
+}  // namespace
+
+template <typename T>
+hipError_t embed_rows(const int* tok, int tok_stride, int R, const T* E, int d, int V, float* x,
+                      hipStream_t s) {
+  hipLaunchKernelGGL(embed_kernel<T>, dim3(R), dim3(256), 0, s, tok, tok_stride, E, d, V, x);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t residual_rmsnorm(float* x, const float* parts, int nparts, long long part_stride,
+                            const float* g, float eps, int R, int d, T* xn, hipStream_t s) {
+  hipLaunchKernelGGL(residual_rmsnorm_kernel<T>, dim3(R), dim3(256), 0, s, x, parts, nparts, part_stride,
+                     g, eps, d, xn);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t qkv_rope_store(const float* parts, int nparts, long long part_stride, const Rows& rows,
+                          int Hq, int Hkv, int D, float theta, T* q, const KVLayout& kv, hipStream_t s) {
+  if (D > 256 || (D & 1)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(qkv_rope_kernel<T>, dim3(rows.R), dim3(256), 0, s, parts, nparts, part_stride, rows,
+                     Hq, Hkv, D, theta, q, kv);
+  return hipGetLastError();
+}
+
+template hipError_t embed_rows<float>(const int*, int, int, const float*, int, int, float*, hipStream_t);
+template hipError_t embed_rows<bf16_t>(const int*, int, int, const bf16_t*, int, int, float*, hipStream_t);
+template hipError_t residual_rmsnorm<float>(float*, const float*, int, long long, const float*, float, int,
+                                            int, float*, hipStream_t);
+template hipError_t residual_rmsnorm<bf16_t>(float*, const float*, int, long long, const float*, float,
+                                             int, int, bf16_t*, hipStream_t);
+template hipError_t qkv_rope_store<float>(const float*, int, long long, const Rows&, int, int, int, float,
+                                          float*, const KVLayout&, hipStream_t);
+template hipError_t qkv_rope_store<bf16_t>(const float*, int, long long, const Rows&, int, int, int, float,
+                                           bf16_t*, const KVLayout&, hipStream_t);
+
+}  // namespace rgd

@@ -1,0 +1,128 @@
+// Launch interface of the HIP kernels (internal; not part of the C ABI).
+#pragma once
+#include "common.hpp"
+
+namespace rgd {
+
+// ---------------------------------------------------------------- GEMM ----
+// Y = X W^T with X [M][K] (row stride ldx) and W [N][K] row-major, possibly
+// given as up to three row segments (for the fused Q/K/V projection).
+struct GemmSeg {
+  const void* w;   // [n][K]
+  int n0, n;       // output columns [n0, n0 + n)
+};
+
+enum GemmMode {
+  GEMM_PARTIAL = 0,  // fp32 split-K partials: Y[split][M][N]
+  GEMM_SILU = 1,     // dual weights (gate = seg 0, up = seg 1): out_T[M][N] = silu(g) * u
+  GEMM_LOGITS = 2,   // fp32 Y[M][N] plus per-(row, 64-column tile) maxima
+};
+
+struct GemmArgs {
+  const void* x; int ldx; int M;
+  GemmSeg seg[3]; int nseg;
+  int N, K;
+  int splits;             // split-K factor (GEMM_PARTIAL only)
+  void* y; int ldy;       // output (fp32, or T for GEMM_SILU)
+  long long split_stride; // elements between split partials
+  float* tilemax; int ntiles;  // GEMM_LOGITS: [M][ntiles]
+  int mode;
+};
+
+hipError_t gemm_bf16(const GemmArgs& a, hipStream_t s);
+hipError_t gemm_f32(const GemmArgs& a, hipStream_t s);
+
+// ------------------------------------------------------- row bookkeeping ----
+// Rows of one decode step (or one prefill segment).
+struct Rows {
+  int R;
+  const int* prompt;    // [R] prompt index (selects the shared prefix)
+  const int* base_pos;  // [R] position of tail slot 0 (decode) or of the token (prefill)
+  const int* plen;      // [R] prefix positions this row attends to
+  const int* pages;     // [R][max_pages] tail pages (decode) or null
+  int max_pages;
+  int t;                // tail slot written this step (decode)
+  int prefill;          // 1: K/V go to the prefix at base_pos; no tail
+};
+
+struct KVLayout {
+  void* prefix_k; void* prefix_v;  // this layer: [B][P][Hkv][D]
+  void* pool_k; void* pool_v;      // this layer: [pages][page_size][Hkv][D]
+  int P;                           // prefix capacity per prompt
+  int page_size;
+};
+
+// ------------------------------------------------------------ elementwise ----
+template <typename T>
+hipError_t embed_rows(const int* tok, int tok_stride, int R, const T* E, int d, int V, float* x,
+                      hipStream_t s);
+// x[r] += sum_p parts[p][r]; xn[r] = rmsnorm(x[r]) * g
+template <typename T>
+hipError_t residual_rmsnorm(float* x, const float* parts, int nparts, long long part_stride,
+                            const float* g, float eps, int R, int d, T* xn, hipStream_t s);
+// q/k/v from split partials, RoPE, q -> qbuf, k/v -> cache
+template <typename T>
+hipError_t qkv_rope_store(const float* parts, int nparts, long long part_stride, const Rows& rows,
+                          int Hq, int Hkv, int D, float theta, T* q, const KVLayout& kv, hipStream_t s);
+
+// -------------------------------------------------------------- attention ----
+struct AttnArgs {
+  const void* q;            // [R][Hq][D]
+  Rows rows;
+  KVLayout kv;
+  int Hq, Hkv, D;
+  float* part_o;            // [nparts][R][Hq][D]
+  float* part_lse;          // [nparts][R][Hq]
+  int nparts;
+  // prefix (shared) part
+  const int4* rblocks; int nrblocks;  // (r0, nr, prompt, maxplen) row blocks for the MFMA path
+  int splits; int split_len;          // prefix splits (part index 0..splits-1)
+  // tail part
+  int tail_len;             // visible tail positions (decode), 0 for prefill
+  int tail_chunk; int tail_chunks;    // part index splits .. splits+tail_chunks-1
+};
+hipError_t attn_prefix_mfma_bf16(const AttnArgs& a, hipStream_t s);
+template <typename T> hipError_t attn_prefix_vec(const AttnArgs& a, hipStream_t s);
+template <typename T> hipError_t attn_tail_vec(const AttnArgs& a, hipStream_t s);
+template <typename T> hipError_t attn_combine(const AttnArgs& a, T* out, hipStream_t s);
+
+// ---------------------------------------------------------------- sampler ----
+hipError_t fill_u32(uint32_t* p, uint32_t v, long long n, hipStream_t s);
+// per-chunk maxima of fp32 rows (standalone sampler)
+hipError_t chunk_max(const float* z, long long ldz, int R, int V, int chunk, float* cmax, hipStream_t s);
+// argmax: packed (value, -index) keys, max over chunks via 64-bit atomics
+hipError_t argmax_rows(const float* z, long long ldz, int R, int V, unsigned long long* best, hipStream_t s);
+struct SampleArgs {
+  const float* z; long long ldz; int R; int V;
+  const float* pmax; int npmax;   // [R][npmax] partial maxima; row max = their max
+  float T; float p_min;
+  int chunk; int nchunks;
+  float* chunk_sums;              // [R][nchunks]
+  unsigned int* counters;         // [R] zero on entry, left zero
+  const unsigned long long* seeds;  // [R]
+  unsigned int ctr; unsigned int stream;
+  int* out; long long out_stride; int out_col;   // token of row r -> out[r*out_stride + out_col]
+  int* cur_tok;                   // optional [R] copy of the token (next step's input)
+  int* status;                    // device flag: set to 1 on a non-finite row maximum
+};
+hipError_t minp_sample(const SampleArgs& a, hipStream_t s);
+// many draws per row from precomputed chunk sums (counter (ctr, stream0 + d))
+hipError_t minp_multi_draw(const SampleArgs& a, int draws, unsigned int stream0, int* out,
+                           hipStream_t s);
+
+// ------------------------------------------------------------------- gate ----
+struct GateArgs {
+  const unsigned long long* best;  // [R] argmax keys
+  const int* row_prompt; int R;
+  int* cur_tok;
+  int* probe_tokens; int k;        // [B][k]
+  int* probe_len; int* event;      // [B]
+  const int* offsets; const int* tokens; const int* owner; int n_entries; int min_match;
+  int eos;
+  unsigned long long* best_reset;  // same as best (cleared after use)
+};
+hipError_t probe_update(const GateArgs& a, hipStream_t s);
+hipError_t gate_decide(const int* event, int B, int* decision, int* n_miss, int* miss_idx,
+                       hipStream_t s);
+
+}  // namespace rgd

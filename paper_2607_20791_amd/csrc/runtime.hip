@@ -1,0 +1,1115 @@
+// Host runtime behind the C ABI: model / KV / table handles, the page pool of
+// per-row tails, the decode step, and the probe, gate and sampling loops of
+// refusal-gated decoding (Algorithm 1).
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "kernels.hpp"
+#include "rgd.h"
+
+using namespace rgd;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define HIP_OK(expr)                                                                   \
+  do {                                                                                 \
+    hipError_t e_ = (expr);                                                            \
+    if (e_ != hipSuccess)                                                              \
+      return fail(RGD_E_HIP, "%s failed: %s", #expr, hipGetErrorString(e_));           \
+  } while (0)
+
+#define RGD_TRY(expr)            \
+  do {                           \
+    int rc_ = (expr);            \
+    if (rc_ != RGD_OK) return rc_; \
+  } while (0)
+
+inline long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
+
+constexpr int kMaxParts = 40;      // attention partials per row (prefix splits + tail chunks)
+constexpr int kSampleChunk = 4096; // logits per sampler workgroup
+constexpr int kTailChunk = 256;
+
+struct DevBuf {
+  void* p = nullptr;
+  ~DevBuf() {
+    if (p) (void)hipFree(p);
+  }
+};
+
+}  // namespace
+
+// ------------------------------------------------------------------ handles --
+struct rgd_table {
+  int n_entries = 0, min_match = 2;
+  int* d_offsets = nullptr;
+  int* d_tokens = nullptr;
+  int* d_owner = nullptr;
+  ~rgd_table() {
+    if (d_offsets) (void)hipFree(d_offsets);
+    if (d_tokens) (void)hipFree(d_tokens);
+    if (d_owner) (void)hipFree(d_owner);
+  }
+};
+
+struct rgd_model {
+  rgd_model_config cfg{};
+  bool bf16 = false;
+  const void* embed = nullptr;
+  const float* final_norm = nullptr;
+  const void* lm_head = nullptr;
+  std::vector<rgd_layer_weights> layers;
+  int max_rows = 0;
+  int part_rows = 0;  // row capacity of the split-K partial buffers
+  int nqkv = 0, ntiles = 0, nchunks = 0;
+  size_t esz = 4;
+  // workspace
+  std::vector<void*> allocs;
+  float* x = nullptr;
+  void* xn = nullptr;
+  float* qkv_part = nullptr;
+  void* q = nullptr;
+  float* part_o = nullptr;
+  float* part_lse = nullptr;
+  void* attn_out = nullptr;
+  float* o_part = nullptr;
+  void* act = nullptr;
+  float* down_part = nullptr;
+  float* logits = nullptr;
+  float* tilemax = nullptr;
+  float* chunk_sums = nullptr;
+  unsigned* counters = nullptr;
+  unsigned long long* best = nullptr;
+  int* cur_tok = nullptr;
+  int* status = nullptr;
+  int* row_map = nullptr;
+  // per-call row arrays
+  int* d_prompt = nullptr;
+  int* d_base = nullptr;
+  int* d_plen = nullptr;
+  int4* d_rblocks = nullptr;
+  int* h_stage = nullptr;  // pinned staging for uploads
+  size_t stage_ints = 0;
+  hipEvent_t stage_done = nullptr;
+  ~rgd_model() {
+    for (void* p : allocs) (void)hipFree(p);
+    if (h_stage) (void)hipHostFree(h_stage);
+    if (stage_done) (void)hipEventDestroy(stage_done);
+  }
+  template <typename P>
+  int alloc(P** out, size_t bytes) {
+    void* p = nullptr;
+    hipError_t e = hipMalloc(&p, std::max<size_t>(bytes, 256));
+    if (e != hipSuccess) return fail(RGD_E_OOM, "workspace allocation of %zu bytes failed", bytes);
+    allocs.push_back(p);
+    *out = (P*)p;
+    return RGD_OK;
+  }
+};
+
+struct rgd_kv {
+  const rgd_model* m = nullptr;
+  int max_prompts = 0, max_prefix = 0, n_pages = 0, page_size = 16;
+  void *prefix_k = nullptr, *prefix_v = nullptr, *pool_k = nullptr, *pool_v = nullptr;
+  std::vector<int> plen;
+  std::vector<int> free_pages;
+  std::vector<std::vector<int>> probe_pages;  // pages held by each prompt's probe
+  bool probe_held = false;
+  int max_pages = 0;   // page-table width per row
+  int* d_pages = nullptr;
+  ~rgd_kv() {
+    if (d_pages) (void)hipFree(d_pages);
+  }
+  KVLayout layer(int l) const {
+    const rgd_model_config& c = m->cfg;
+    const long long per_pos = (long long)c.n_kv_heads * c.head_dim;
+    const long long pre = (long long)max_prompts * max_prefix * per_pos * m->esz;
+    const long long pool = (long long)n_pages * page_size * per_pos * m->esz;
+    KVLayout k;
+    k.prefix_k = (char*)prefix_k + l * pre;
+    k.prefix_v = (char*)prefix_v + l * pre;
+    k.pool_k = (char*)pool_k + l * pool;
+    k.pool_v = (char*)pool_v + l * pool;
+    k.P = max_prefix;
+    k.page_size = page_size;
+    return k;
+  }
+};
+
+namespace {
+
+// ----------------------------------------------------------- upload helper --
+// Copies host ints to device through the model's pinned staging buffer.  The
+// previous upload is waited for before the buffer is rewritten.
+struct Upload {
+  int* dst;
+  const int* src;
+  size_t n;
+};
+
+int upload(rgd_model* m, const std::vector<Upload>& ups, hipStream_t s) {
+  size_t total = 0;
+  for (auto& u : ups) total += u.n;
+  if (total > m->stage_ints) return fail(RGD_E_OOM, "upload of %zu ints exceeds staging", total);
+  HIP_OK(hipEventSynchronize(m->stage_done));
+  size_t off = 0;
+  for (auto& u : ups) {
+    if (!u.n) continue;
+    memcpy(m->h_stage + off, u.src, u.n * sizeof(int));
+    HIP_OK(hipMemcpyAsync(u.dst, m->h_stage + off, u.n * sizeof(int), hipMemcpyHostToDevice, s));
+    off += u.n;
+  }
+  HIP_OK(hipEventRecord(m->stage_done, s));
+  return RGD_OK;
+}
+
+// Host description of the rows of one step.
+struct HostRows {
+  std::vector<int> prompt, base, plen;
+  std::vector<int4> blocks;  // row blocks of one prompt for the MFMA attention path
+  int maxplen = 0;
+};
+
+void build_blocks(const rgd_model* m, HostRows& h) {
+  const int G = m->cfg.n_heads / m->cfg.n_kv_heads;
+  const int per = std::max(1, 64 / G);
+  h.blocks.clear();
+  h.maxplen = 0;
+  const int R = (int)h.prompt.size();
+  int r = 0;
+  while (r < R) {
+    const int b = h.prompt[r];
+    int e = r;
+    int mp = 0;
+    while (e < R && h.prompt[e] == b && e - r < per) mp = std::max(mp, h.plen[e++]);
+    h.blocks.push_back(make_int4(r, e - r, b, mp));
+    h.maxplen = std::max(h.maxplen, mp);
+    r = e;
+  }
+}
+
+int upload_rows(rgd_model* m, const HostRows& h, hipStream_t s) {
+  const size_t R = h.prompt.size();
+  return upload(m,
+                {{m->d_prompt, h.prompt.data(), R},
+                 {m->d_base, h.base.data(), R},
+                 {m->d_plen, h.plen.data(), R},
+                 {(int*)m->d_rblocks, (const int*)h.blocks.data(), h.blocks.size() * 4}},
+                s);
+}
+
+Rows device_rows(const rgd_model* m, const rgd_kv* kv, int R, int t, bool prefill) {
+  Rows r;
+  r.R = R;
+  r.prompt = m->d_prompt;
+  r.base_pos = m->d_base;
+  r.plen = m->d_plen;
+  r.pages = prefill ? nullptr : kv->d_pages;
+  r.max_pages = kv ? kv->max_pages : 0;
+  r.t = t;
+  r.prefill = prefill ? 1 : 0;
+  return r;
+}
+
+int splitk(int tiles, int mblocks, int kblocks, int R, int cap_rows) {
+  int ks = (int)cdiv(512, (long long)tiles * mblocks);
+  ks = std::min(ks, kblocks);
+  ks = std::min(ks, 8);
+  ks = std::min(ks, std::max(1, cap_rows / std::max(R, 1)));
+  return std::max(ks, 1);
+}
+
+// -------------------------------------------------------------- attention --
+int run_attention(rgd_model* m, const KVLayout& kvl, const Rows& rows, const HostRows& h,
+                  int tail_len, int force_splits, void* out, hipStream_t s) {
+  const rgd_model_config& c = m->cfg;
+  AttnArgs a{};
+  a.q = m->q;
+  a.rows = rows;
+  a.kv = kvl;
+  a.Hq = c.n_heads;
+  a.Hkv = c.n_kv_heads;
+  a.D = c.head_dim;
+  a.part_o = m->part_o;
+  a.part_lse = m->part_lse;
+  a.rblocks = m->d_rblocks;
+  a.nrblocks = (int)h.blocks.size();
+  a.tail_len = tail_len;
+  a.tail_chunk = kTailChunk;
+  a.tail_chunks = (int)cdiv(tail_len, kTailChunk);
+  const int R = rows.R;
+  const int cap = (int)std::min<long long>(kMaxParts, (long long)kMaxParts * m->max_rows / std::max(R, 1));
+  if (m->bf16) {
+    int S = force_splits;
+    if (S <= 0) S = (int)cdiv(512, (long long)c.n_kv_heads * a.nrblocks);
+    S = (int)std::max<long long>(1, std::min<long long>(S, cdiv(std::max(h.maxplen, 1), 32)));
+    S = std::min(S, cap - a.tail_chunks);
+    a.split_len = (int)cdiv(cdiv(std::max(h.maxplen, 1), S), 32) * 32;
+    a.splits = (int)cdiv(std::max(h.maxplen, 1), a.split_len);
+  } else {
+    a.split_len = 256;
+    a.splits = (int)cdiv(std::max(h.maxplen, 1), 256);
+  }
+  a.nparts = a.splits + a.tail_chunks;
+  if (a.nparts > cap || a.splits < 1)
+    return fail(RGD_E_UNSUPPORTED, "attention needs %d partials for %d rows (capacity %d)", a.nparts, R, cap);
+  if (m->bf16) {
+    HIP_OK(attn_prefix_mfma_bf16(a, s));
+    HIP_OK(attn_tail_vec<bf16_t>(a, s));
+    HIP_OK(attn_combine<bf16_t>(a, (bf16_t*)out, s));
+  } else {
+    HIP_OK(attn_prefix_vec<float>(a, s));
+    HIP_OK(attn_tail_vec<float>(a, s));
+    HIP_OK(attn_combine<float>(a, (float*)out, s));
+  }
+  return RGD_OK;
+}
+
+// -------------------------------------------------------------- GEMM glue --
+int gemm(rgd_model* m, GemmArgs& g, hipStream_t s) {
+  hipError_t e = m->bf16 ? gemm_bf16(g, s) : gemm_f32(g, s);
+  if (e != hipSuccess) return fail(RGD_E_HIP, "gemm launch failed: %s", hipGetErrorString(e));
+  return RGD_OK;
+}
+
+int lm_head(rgd_model* m, const void* x, int ldx, int R, float* logits, hipStream_t s) {
+  GemmArgs g{};
+  g.x = x;
+  g.ldx = ldx;
+  g.M = R;
+  g.seg[0] = {m->lm_head, 0, m->cfg.vocab};
+  g.nseg = 1;
+  g.N = m->cfg.vocab;
+  g.K = m->cfg.d_model;
+  g.splits = 1;
+  g.y = logits;
+  g.ldy = m->cfg.vocab;
+  g.tilemax = m->tilemax;
+  g.ntiles = m->ntiles;
+  g.mode = GEMM_LOGITS;
+  return gemm(m, g, s);
+}
+
+// One forward pass of R rows through every layer.  feed: token of row r at
+// feed[r * feed_stride].  Leaves the final normalised hidden state in m->xn.
+int forward_rows(rgd_model* m, rgd_kv* kv, const Rows& rows, const HostRows& h, const int* feed,
+                 int feed_stride, hipStream_t s) {
+  const rgd_model_config& c = m->cfg;
+  const int R = rows.R, d = c.d_model, Hq = c.n_heads, Hkv = c.n_kv_heads, D = c.head_dim;
+  const int F = c.ffn_dim;
+  const int mblocks = (int)cdiv(R, 64);
+  const bool bf = m->bf16;
+  if (bf)
+    HIP_OK(embed_rows<bf16_t>(feed, feed_stride, R, (const bf16_t*)m->embed, d, c.vocab, m->x, s));
+  else
+    HIP_OK(embed_rows<float>(feed, feed_stride, R, (const float*)m->embed, d, c.vocab, m->x, s));
+  auto norm = [&](const float* parts, int np, const void* gain) -> hipError_t {
+    const long long stride = (long long)R * d;
+    return bf ? residual_rmsnorm<bf16_t>(m->x, parts, np, stride, (const float*)gain, c.rms_eps, R, d,
+                                         (bf16_t*)m->xn, s)
+              : residual_rmsnorm<float>(m->x, parts, np, stride, (const float*)gain, c.rms_eps, R, d,
+                                        (float*)m->xn, s);
+  };
+  HIP_OK(norm(nullptr, 0, m->layers[0].attn_norm));
+  for (int l = 0; l < c.n_layers; ++l) {
+    const rgd_layer_weights& L = m->layers[l];
+    const KVLayout kvl = kv->layer(l);
+    // fused Q/K/V projection (split-K partials)
+    GemmArgs g{};
+    g.x = m->xn;
+    g.ldx = d;
+    g.M = R;
+    g.seg[0] = {L.wq, 0, Hq * D};
+    g.seg[1] = {L.wk, Hq * D, Hkv * D};
+    g.seg[2] = {L.wv, (Hq + Hkv) * D, Hkv * D};
+    g.nseg = 3;
+    g.N = m->nqkv;
+    g.K = d;
+    g.splits = bf ? splitk((int)cdiv(g.N, 64), mblocks, d / 128, R, m->part_rows) : 1;
+    g.y = m->qkv_part;
+    g.ldy = g.N;
+    g.split_stride = (long long)R * g.N;
+    g.mode = GEMM_PARTIAL;
+    RGD_TRY(gemm(m, g, s));
+    if (bf)
+      HIP_OK(qkv_rope_store<bf16_t>(m->qkv_part, g.splits, g.split_stride, rows, Hq, Hkv, D, c.rope_theta,
+                                    (bf16_t*)m->q, kvl, s));
+    else
+      HIP_OK(qkv_rope_store<float>(m->qkv_part, g.splits, g.split_stride, rows, Hq, Hkv, D, c.rope_theta,
+                                   (float*)m->q, kvl, s));
+    RGD_TRY(run_attention(m, kvl, rows, h, rows.prefill ? 0 : rows.t + 1, 0, m->attn_out, s));
+    // output projection + residual + ffn norm
+    GemmArgs o{};
+    o.x = m->attn_out;
+    o.ldx = Hq * D;
+    o.M = R;
+    o.seg[0] = {L.wo, 0, d};
+    o.nseg = 1;
+    o.N = d;
+    o.K = Hq * D;
+    o.splits = bf ? splitk((int)cdiv(d, 64), mblocks, o.K / 128, R, m->part_rows) : 1;
+    o.y = m->o_part;
+    o.ldy = d;
+    o.split_stride = (long long)R * d;
+    o.mode = GEMM_PARTIAL;
+    RGD_TRY(gemm(m, o, s));
+    HIP_OK(norm(m->o_part, o.splits, L.ffn_norm));
+    // SwiGLU: act = silu(W_gate xn) * (W_up xn)
+    GemmArgs f{};
+    f.x = m->xn;
+    f.ldx = d;
+    f.M = R;
+    f.seg[0] = {L.w_gate, 0, F};
+    f.seg[1] = {L.w_up, 0, F};
+    f.nseg = 2;
+    f.N = F;
+    f.K = d;
+    f.splits = 1;
+    f.y = m->act;
+    f.ldy = F;
+    f.mode = GEMM_SILU;
+    RGD_TRY(gemm(m, f, s));
+    GemmArgs dn{};
+    dn.x = m->act;
+    dn.ldx = F;
+    dn.M = R;
+    dn.seg[0] = {L.w_down, 0, d};
+    dn.nseg = 1;
+    dn.N = d;
+    dn.K = F;
+    dn.splits = bf ? splitk((int)cdiv(d, 64), mblocks, F / 128, R, m->part_rows) : 1;
+    dn.y = m->down_part;
+    dn.ldy = d;
+    dn.split_stride = (long long)R * d;
+    dn.mode = GEMM_PARTIAL;
+    RGD_TRY(gemm(m, dn, s));
+    const void* next_gain = l + 1 < c.n_layers ? m->layers[l + 1].attn_norm : (const void*)m->final_norm;
+    HIP_OK(norm(m->down_part, dn.splits, next_gain));
+  }
+  return RGD_OK;
+}
+
+SampleArgs sample_args(rgd_model* m, const float* z, long long ldz, int R, int V, float T, float p_min,
+                       const float* pmax, int npmax, const unsigned long long* seeds, unsigned ctr, int* out,
+                       long long out_stride, int out_col, int* cur) {
+  SampleArgs a{};
+  a.z = z;
+  a.ldz = ldz;
+  a.R = R;
+  a.V = V;
+  a.pmax = pmax;
+  a.npmax = npmax;
+  a.T = T;
+  a.p_min = p_min;
+  a.chunk = kSampleChunk;
+  a.nchunks = (int)cdiv(V, kSampleChunk);
+  a.chunk_sums = m->chunk_sums;
+  a.counters = m->counters;
+  a.seeds = seeds;
+  a.ctr = ctr;
+  a.stream = 0;
+  a.out = out;
+  a.out_stride = out_stride;
+  a.out_col = out_col;
+  a.cur_tok = cur;
+  a.status = m->status;
+  return a;
+}
+
+__global__ void gather_rows_kernel(const float* src, long long lds, const int* map, int V, float* dst) {
+  const int r = blockIdx.y;
+  const float* s = src + (long long)map[r] * lds;
+  for (int i = blockIdx.x * 256 + threadIdx.x; i < V; i += 256 * gridDim.x) dst[(long long)r * V + i] = s[i];
+}
+
+__global__ void argmax_finish_kernel(unsigned long long* best, int R, int* out, long long stride, int col,
+                                     int* cur) {
+  const int r = blockIdx.x * 256 + threadIdx.x;
+  if (r >= R) return;
+  const int tok = int(0xFFFFFFFFu - uint32_t(best[r] & 0xFFFFFFFFull));
+  out[r * stride + col] = tok;
+  if (cur) cur[r] = tok;
+  best[r] = 0ull;
+}
+
+__global__ void probe_init_kernel(int B, int k, int* tokens, int* len, int* event) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < B * k) tokens[i] = 0;
+  if (i < B) {
+    len[i] = 0;
+    event[i] = -1;
+  }
+}
+
+__global__ void probe_feed_kernel(const int* prompt, int R, const int* probe_tokens, int k, int j, int* cur) {
+  const int r = blockIdx.x * 256 + threadIdx.x;
+  if (r < R) cur[r] = probe_tokens[(long long)prompt[r] * k + j];
+}
+
+// Selects one token per row from logits z (ldz) with row indirection `map`
+// (null: identity).  T == 0: argmax.
+int select_tokens(rgd_model* m, const float* z, long long ldz, int R, const float* pmax, int npmax, float T,
+                  float p_min, const unsigned long long* seeds, unsigned ctr, int* out, long long out_stride,
+                  int out_col, int* cur, hipStream_t s) {
+  const int V = m->cfg.vocab;
+  if (T == 0.f) {
+    HIP_OK(argmax_rows(z, ldz, R, V, m->best, s));
+    hipLaunchKernelGGL(argmax_finish_kernel, dim3((R + 255) / 256), dim3(256), 0, s, m->best, R, out,
+                       out_stride, out_col, cur);
+    HIP_OK(hipGetLastError());
+    return RGD_OK;
+  }
+  SampleArgs a = sample_args(m, z, ldz, R, V, T, p_min, pmax, npmax, seeds, ctr, out, out_stride, out_col, cur);
+  HIP_OK(minp_sample(a, s));
+  return RGD_OK;
+}
+
+bool valid_dtype_shapes(const rgd_model_config& c, std::string& why) {
+  if (c.n_layers < 1 || c.d_model < 1 || c.n_heads < 1 || c.n_kv_heads < 1 || c.head_dim < 2 ||
+      c.ffn_dim < 1 || c.vocab < 2 || c.max_pos < 1) {
+    why = "all sizes must be positive";
+    return false;
+  }
+  if (c.n_heads % c.n_kv_heads) {
+    why = "n_heads must be a multiple of n_kv_heads";
+    return false;
+  }
+  if (c.head_dim % 2 || c.head_dim > 256) {
+    why = "head_dim must be even and <= 256";
+    return false;
+  }
+  if (c.vocab % 4) {
+    why = "vocab must be a multiple of 4";
+    return false;
+  }
+  if ((long long)c.vocab > 256LL * kSampleChunk) {
+    why = "vocab too large";
+    return false;
+  }
+  if (c.dtype == RGD_DTYPE_BF16) {
+    if (c.head_dim != 128 || c.d_model % 128 || (c.n_heads * c.head_dim) % 128 || c.ffn_dim % 128) {
+      why = "bf16 models need head_dim 128 and d_model, Hq*D, ffn multiples of 128";
+      return false;
+    }
+    if ((c.n_heads * c.head_dim) % 64 || (c.n_kv_heads * c.head_dim) % 64 || c.ffn_dim % 32) {
+      why = "projection widths must be multiples of 64";
+      return false;
+    }
+    if (c.n_heads / c.n_kv_heads > 64) {
+      why = "at most 64 query heads per KV head";
+      return false;
+    }
+  } else if (c.dtype == RGD_DTYPE_F32) {
+    if (c.n_heads / c.n_kv_heads > 8) {
+      why = "fp32 models support at most 8 query heads per KV head";
+      return false;
+    }
+  } else {
+    why = "unknown dtype";
+    return false;
+  }
+  return true;
+}
+
+}  // namespace
+
+// ===================================================================== ABI ===
+extern "C" {
+
+const char* rgd_version(void) { return "rgd-mi355x 0.1 (gfx950)"; }
+
+const char* rgd_last_error(void) { return g_err.c_str(); }
+
+int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int32_t max_rows, rgd_model** out) {
+  g_err.clear();
+  if (!cfg || !w || !out) return fail(RGD_E_INVALID_ARG, "null argument");
+  *out = nullptr;
+  std::string why;
+  if (!valid_dtype_shapes(*cfg, why)) {
+    const bool bad_arg = cfg->dtype != RGD_DTYPE_F32 && cfg->dtype != RGD_DTYPE_BF16;
+    return fail(bad_arg ? RGD_E_INVALID_ARG : RGD_E_UNSUPPORTED, "model config: %s", why.c_str());
+  }
+  if (max_rows < 1 || max_rows > 65536) return fail(RGD_E_INVALID_ARG, "max_rows must be in [1, 65536]");
+  if (!w->embed || !w->final_norm || !w->lm_head || !w->layers)
+    return fail(RGD_E_INVALID_ARG, "null weight pointer");
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    const rgd_layer_weights& L = w->layers[l];
+    if (!L.attn_norm || !L.wq || !L.wk || !L.wv || !L.wo || !L.ffn_norm || !L.w_gate || !L.w_up || !L.w_down)
+      return fail(RGD_E_INVALID_ARG, "null weight pointer in layer %d", l);
+  }
+  rgd_model* m = new rgd_model();
+  m->cfg = *cfg;
+  m->bf16 = cfg->dtype == RGD_DTYPE_BF16;
+  m->esz = m->bf16 ? 2 : 4;
+  m->embed = w->embed;
+  m->final_norm = (const float*)w->final_norm;
+  m->lm_head = w->lm_head;
+  m->layers.assign(w->layers, w->layers + cfg->n_layers);
+  m->max_rows = max_rows;
+  m->part_rows = std::max(max_rows, 512);
+  const int R = max_rows, d = cfg->d_model, Hq = cfg->n_heads, Hkv = cfg->n_kv_heads, D = cfg->head_dim;
+  m->nqkv = (Hq + 2 * Hkv) * D;
+  m->ntiles = (int)cdiv(cfg->vocab, 64);
+  m->nchunks = (int)cdiv(cfg->vocab, kSampleChunk);
+  const size_t e = m->esz;
+  const size_t PR = m->part_rows;
+  int rc = RGD_OK;
+  auto A = [&](auto** p, size_t bytes) {
+    if (rc == RGD_OK) rc = m->alloc(p, bytes);
+  };
+  A(&m->x, (size_t)R * d * 4);
+  A(&m->xn, (size_t)R * d * e);
+  A(&m->qkv_part, PR * m->nqkv * 4);
+  A(&m->q, (size_t)R * Hq * D * e);
+  A(&m->part_o, (size_t)kMaxParts * R * Hq * D * 4);
+  A(&m->part_lse, (size_t)kMaxParts * R * Hq * 4);
+  A(&m->attn_out, (size_t)R * Hq * D * e);
+  A(&m->o_part, PR * d * 4);
+  A(&m->act, (size_t)R * cfg->ffn_dim * e);
+  A(&m->down_part, PR * d * 4);
+  A(&m->logits, (size_t)R * cfg->vocab * 4);
+  A(&m->tilemax, (size_t)R * m->ntiles * 4);
+  A(&m->chunk_sums, (size_t)R * m->nchunks * 4);
+  A(&m->counters, (size_t)R * 4);
+  A(&m->best, (size_t)R * 8);
+  A(&m->cur_tok, (size_t)R * 4);
+  A(&m->status, 4);
+  A(&m->row_map, (size_t)R * 4);
+  A(&m->d_prompt, (size_t)R * 4);
+  A(&m->d_base, (size_t)R * 4);
+  A(&m->d_plen, (size_t)R * 4);
+  A(&m->d_rblocks, (size_t)R * 16);
+  if (rc != RGD_OK) {
+    delete m;
+    return rc;
+  }
+  m->stage_ints = (size_t)R * 8 + 64;
+  if (hipHostMalloc((void**)&m->h_stage, m->stage_ints * sizeof(int), hipHostMallocDefault) != hipSuccess ||
+      hipEventCreateWithFlags(&m->stage_done, hipEventDisableTiming) != hipSuccess ||
+      hipEventRecord(m->stage_done, nullptr) != hipSuccess) {
+    delete m;
+    return fail(RGD_E_HIP, "pinned staging allocation failed");
+  }
+  // counters / maxima start cleared
+  if (hipMemset(m->counters, 0, (size_t)R * 4) != hipSuccess || hipMemset(m->best, 0, (size_t)R * 8) != hipSuccess ||
+      hipMemset(m->status, 0, 4) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+    delete m;
+    return fail(RGD_E_HIP, "workspace initialisation failed");
+  }
+  *out = m;
+  return RGD_OK;
+}
+
+void rgd_model_destroy(rgd_model* m) { delete m; }
+
+int32_t rgd_kv_create(const rgd_model* m, int32_t max_prompts, int32_t max_prefix, int32_t n_pages, int32_t page_size,
+                      void* prefix_k, void* prefix_v, void* pool_k, void* pool_v, rgd_kv** out) {
+  g_err.clear();
+  if (!m || !out || !prefix_k || !prefix_v || !pool_k || !pool_v) return fail(RGD_E_INVALID_ARG, "null argument");
+  *out = nullptr;
+  if (max_prompts < 1 || max_prefix < 1 || n_pages < 0 || page_size < 1 || page_size > 4096)
+    return fail(RGD_E_INVALID_ARG, "kv sizes out of range");
+  if (max_prefix > m->cfg.max_pos) return fail(RGD_E_INVALID_ARG, "max_prefix exceeds the model's max_pos");
+  rgd_kv* kv = new rgd_kv();
+  kv->m = m;
+  kv->max_prompts = max_prompts;
+  kv->max_prefix = max_prefix;
+  kv->n_pages = n_pages;
+  kv->page_size = page_size;
+  kv->prefix_k = prefix_k;
+  kv->prefix_v = prefix_v;
+  kv->pool_k = pool_k;
+  kv->pool_v = pool_v;
+  kv->plen.assign(max_prompts, 0);
+  kv->probe_pages.assign(max_prompts, {});
+  for (int p = n_pages - 1; p >= 0; --p) kv->free_pages.push_back(p);
+  kv->max_pages = (int)std::max<long long>(1, cdiv(m->cfg.max_pos, page_size));
+  if (hipMalloc((void**)&kv->d_pages, (size_t)m->max_rows * kv->max_pages * 4) != hipSuccess) {
+    delete kv;
+    return fail(RGD_E_OOM, "page-table allocation failed");
+  }
+  *out = kv;
+  return RGD_OK;
+}
+
+void rgd_kv_destroy(rgd_kv* kv) { delete kv; }
+
+int32_t rgd_kv_set_prefix_len(rgd_kv* kv, int32_t prompt, int32_t len) {
+  g_err.clear();
+  if (!kv) return fail(RGD_E_INVALID_ARG, "null kv");
+  if (prompt < 0 || prompt >= kv->max_prompts) return fail(RGD_E_INVALID_ARG, "prompt out of range");
+  if (len < 0 || len > kv->max_prefix) return fail(RGD_E_INVALID_ARG, "len out of range");
+  kv->plen[prompt] = len;
+  return RGD_OK;
+}
+
+int32_t rgd_table_create(const int32_t* offsets, const int32_t* tokens, int32_t n_entries, const int32_t* owner,
+                         int32_t min_match, rgd_table** out) {
+  g_err.clear();
+  if (!out) return fail(RGD_E_INVALID_ARG, "null out");
+  *out = nullptr;
+  if (n_entries < 0 || n_entries > (1 << 20)) return fail(RGD_E_INVALID_ARG, "n_entries out of range");
+  if (n_entries > 0 && (!offsets || !tokens)) return fail(RGD_E_INVALID_ARG, "null table arrays");
+  if (min_match < 1) return fail(RGD_E_INVALID_ARG, "min_match must be >= 1");
+  if (n_entries > 0) {
+    if (offsets[0] != 0) return fail(RGD_E_INVALID_ARG, "offsets[0] must be 0");
+    for (int e = 0; e < n_entries; ++e)
+      if (offsets[e + 1] < offsets[e]) return fail(RGD_E_INVALID_ARG, "offsets must be non-decreasing");
+    for (int e = 0; e < n_entries; ++e)
+      if (owner && owner[e] < -1) return fail(RGD_E_INVALID_ARG, "owner must be -1 or a prompt index");
+  }
+  rgd_table* t = new rgd_table();
+  t->n_entries = n_entries;
+  t->min_match = min_match;
+  const int ntok = n_entries ? offsets[n_entries] : 0;
+  std::vector<int> own(std::max(n_entries, 1), -1);
+  if (owner) std::copy(owner, owner + n_entries, own.begin());
+  std::vector<int> offs(n_entries + 1, 0);
+  if (n_entries) std::copy(offsets, offsets + n_entries + 1, offs.begin());
+  if (hipMalloc((void**)&t->d_offsets, offs.size() * 4) != hipSuccess ||
+      hipMalloc((void**)&t->d_tokens, std::max(ntok, 1) * 4) != hipSuccess ||
+      hipMalloc((void**)&t->d_owner, own.size() * 4) != hipSuccess) {
+    delete t;
+    return fail(RGD_E_OOM, "table allocation failed");
+  }
+  if (hipMemcpy(t->d_offsets, offs.data(), offs.size() * 4, hipMemcpyHostToDevice) != hipSuccess ||
+      (ntok && hipMemcpy(t->d_tokens, tokens, ntok * 4, hipMemcpyHostToDevice) != hipSuccess) ||
+      hipMemcpy(t->d_owner, own.data(), own.size() * 4, hipMemcpyHostToDevice) != hipSuccess) {
+    delete t;
+    return fail(RGD_E_HIP, "table upload failed");
+  }
+  *out = t;
+  return RGD_OK;
+}
+
+void rgd_table_destroy(rgd_table* t) { delete t; }
+
+int32_t rgd_prefill_kv(rgd_model* m, rgd_kv* kv, const int32_t* tokens, int32_t B, int32_t n, int32_t start_pos,
+                       float* last_logits, rgd_stream stream) {
+  g_err.clear();
+  if (!m || !kv || !tokens || !last_logits) return fail(RGD_E_INVALID_ARG, "null argument");
+  if (kv->m != m) return fail(RGD_E_INVALID_ARG, "kv belongs to another model");
+  if (B < 1 || B > kv->max_prompts || n < 1 || start_pos < 0) return fail(RGD_E_INVALID_ARG, "bad B/n/start_pos");
+  if ((long long)start_pos + n > kv->max_prefix) return fail(RGD_E_INVALID_ARG, "prompt exceeds max_prefix");
+  for (int b = 0; b < B; ++b)
+    if (kv->plen[b] != start_pos)
+      return fail(RGD_E_STATE, "prompt %d holds %d positions, prefill starts at %d", b, kv->plen[b], start_pos);
+  if (kv->probe_held) return fail(RGD_E_STATE, "probe tails not released (call rgd_gate)");
+  hipStream_t s = (hipStream_t)stream;
+  const int V = m->cfg.vocab, d = m->cfg.d_model;
+  // chunks: whole prompts when n fits in max_rows, else segments of one prompt
+  const int per_chunk = n <= m->max_rows ? m->max_rows / n : 0;
+  const int seg = n <= m->max_rows ? n : m->max_rows;
+  for (int b0 = 0; b0 < B;) {
+    const int nb = per_chunk ? std::min(per_chunk, B - b0) : 1;
+    for (int i0 = 0; i0 < n; i0 += seg) {
+      const int len = std::min(seg, n - i0);
+      HostRows h;
+      for (int bb = 0; bb < nb; ++bb)
+        for (int i = 0; i < len; ++i) {
+          const int pos = start_pos + i0 + i;
+          h.prompt.push_back(b0 + bb);
+          h.base.push_back(pos);
+          h.plen.push_back(pos + 1);
+        }
+      build_blocks(m, h);
+      const int R = (int)h.prompt.size();
+      RGD_TRY(upload_rows(m, h, s));
+      Rows rows = device_rows(m, kv, R, 0, true);
+      const int* feed = tokens + (long long)b0 * n + i0;
+      if (per_chunk) {
+        RGD_TRY(forward_rows(m, kv, rows, h, feed, 1, s));
+        // logits of each prompt's last token: rows (bb * n + n - 1)
+        RGD_TRY(lm_head(m, (const char*)m->xn + (size_t)(n - 1) * d * m->esz, n * d, nb,
+                        last_logits + (long long)b0 * V, s));
+      } else {
+        RGD_TRY(forward_rows(m, kv, rows, h, feed, 1, s));
+        if (i0 + len == n)
+          RGD_TRY(lm_head(m, (const char*)m->xn + (size_t)(len - 1) * d * m->esz, d, 1,
+                          last_logits + (long long)b0 * V, s));
+      }
+    }
+    b0 += nb;
+  }
+  for (int b = 0; b < B; ++b) kv->plen[b] = start_pos + n;
+  return RGD_OK;
+}
+
+int32_t rgd_probe(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_table* tbl, int32_t B, int32_t k,
+                  int32_t c, int32_t eos_id, int32_t* probe_tokens, int32_t* probe_len, int32_t* event,
+                  rgd_stream stream) {
+  g_err.clear();
+  if (!m || !kv || !last_logits || !tbl || !probe_tokens || !probe_len || !event)
+    return fail(RGD_E_INVALID_ARG, "null argument");
+  if (kv->m != m) return fail(RGD_E_INVALID_ARG, "kv belongs to another model");
+  if (B < 1 || B > kv->max_prompts || B > m->max_rows) return fail(RGD_E_INVALID_ARG, "B out of range");
+  if (k < 1 || c < 1) return fail(RGD_E_INVALID_ARG, "k and c must be >= 1");
+  if (eos_id >= m->cfg.vocab) return fail(RGD_E_INVALID_ARG, "eos_id out of range");
+  if (kv->probe_held) return fail(RGD_E_STATE, "previous probe tails not released (call rgd_gate)");
+  for (int b = 0; b < B; ++b) {
+    if (kv->plen[b] < 1) return fail(RGD_E_STATE, "prompt %d has no prefix (prefill first)", b);
+    if ((long long)kv->plen[b] + k - 1 > m->cfg.max_pos) return fail(RGD_E_INVALID_ARG, "probe exceeds max_pos");
+  }
+  const int pages_per = (int)cdiv(std::max(k - 1, 0), kv->page_size);
+  if (pages_per > kv->max_pages) return fail(RGD_E_INVALID_ARG, "probe longer than the page table");
+  if ((long long)pages_per * B > (long long)kv->free_pages.size())
+    return fail(RGD_E_OOM, "page pool too small for %d probes of %d tokens", B, k);
+  hipStream_t s = (hipStream_t)stream;
+  const int V = m->cfg.vocab;
+  // hold pages for every probe tail
+  for (int b = 0; b < B; ++b) {
+    kv->probe_pages[b].clear();
+    for (int i = 0; i < pages_per; ++i) {
+      kv->probe_pages[b].push_back(kv->free_pages.back());
+      kv->free_pages.pop_back();
+    }
+  }
+  kv->probe_held = true;
+  hipLaunchKernelGGL(probe_init_kernel, dim3((int)cdiv((long long)B * k, 256)), dim3(256), 0, s, B, k, probe_tokens,
+                     probe_len, event);
+  HIP_OK(hipGetLastError());
+
+  GateArgs ga{};
+  ga.best = m->best;
+  ga.best_reset = m->best;
+  ga.row_prompt = m->d_prompt;
+  ga.cur_tok = m->cur_tok;
+  ga.probe_tokens = probe_tokens;
+  ga.k = k;
+  ga.probe_len = probe_len;
+  ga.event = event;
+  ga.offsets = tbl->d_offsets;
+  ga.tokens = tbl->d_tokens;
+  ga.owner = tbl->d_owner;
+  ga.n_entries = tbl->n_entries;
+  ga.min_match = tbl->min_match;
+  ga.eos = eos_id;
+
+  std::vector<int> alive(B);
+  for (int b = 0; b < B; ++b) alive[b] = b;
+  std::vector<int> host_ev(B);
+  int* pinned_ev = nullptr;
+  HIP_OK(hipHostMalloc((void**)&pinned_ev, (size_t)B * 4, hipHostMallocDefault));
+  struct PinnedFree {
+    int* p;
+    ~PinnedFree() { (void)hipHostFree(p); }
+  } pf{pinned_ev};
+
+  auto set_rows = [&](HostRows& h, std::vector<int>& pages) -> int {
+    h.prompt.clear();
+    h.base.clear();
+    h.plen.clear();
+    pages.assign((size_t)alive.size() * kv->max_pages, 0);
+    for (size_t r = 0; r < alive.size(); ++r) {
+      const int b = alive[r];
+      h.prompt.push_back(b);
+      h.base.push_back(kv->plen[b]);
+      h.plen.push_back(kv->plen[b]);
+      for (int i = 0; i < pages_per; ++i) pages[r * kv->max_pages + i] = kv->probe_pages[b][i];
+    }
+    build_blocks(m, h);
+    return upload(m,
+                  {{m->d_prompt, h.prompt.data(), h.prompt.size()},
+                   {m->d_base, h.base.data(), h.base.size()},
+                   {m->d_plen, h.plen.data(), h.plen.size()},
+                   {(int*)m->d_rblocks, (const int*)h.blocks.data(), h.blocks.size() * 4},
+                   {kv->d_pages, pages.data(), pages.size()}},
+                  s);
+  };
+  HostRows h;
+  std::vector<int> pages;
+  RGD_TRY(set_rows(h, pages));
+  // token 1: argmax of the prompt logits (rows are prompts 0..B-1 here)
+  HIP_OK(argmax_rows(last_logits, V, B, V, m->best, s));
+  ga.R = B;
+  HIP_OK(probe_update(ga, s));
+  for (int j = 2;; ++j) {
+    const int done_tokens = j - 1;
+    const bool check = done_tokens <= c || done_tokens % c == 0 || done_tokens >= k;
+    if (check) {
+      HIP_OK(hipMemcpyAsync(pinned_ev, event, (size_t)B * 4, hipMemcpyDeviceToHost, s));
+      HIP_OK(hipStreamSynchronize(s));
+      std::vector<int> still;
+      for (int b : alive)
+        if (pinned_ev[b] == -1) still.push_back(b);
+      if (still.empty()) break;
+      if (still.size() != alive.size()) {
+        alive.swap(still);
+        RGD_TRY(set_rows(h, pages));
+      }
+    }
+    if (j > k) break;  // cannot happen: every prompt is decided after k tokens
+    const int R = (int)alive.size();
+    hipLaunchKernelGGL(probe_feed_kernel, dim3((R + 255) / 256), dim3(256), 0, s, m->d_prompt, R, probe_tokens, k,
+                       j - 2, m->cur_tok);
+    HIP_OK(hipGetLastError());
+    Rows rows = device_rows(m, kv, R, j - 2, false);
+    RGD_TRY(forward_rows(m, kv, rows, h, m->cur_tok, 1, s));
+    RGD_TRY(lm_head(m, m->xn, m->cfg.d_model, R, m->logits, s));
+    HIP_OK(argmax_rows(m->logits, V, R, V, m->best, s));
+    ga.R = R;
+    HIP_OK(probe_update(ga, s));
+  }
+  HIP_OK(hipStreamSynchronize(s));
+  return RGD_OK;
+}
+
+int32_t rgd_gate(rgd_kv* kv, const int32_t* event, int32_t B, int32_t* decision_host, int32_t* n_miss_host,
+                 int32_t* miss_idx_host, rgd_stream stream) {
+  g_err.clear();
+  if (!kv || !event || !decision_host || !n_miss_host || !miss_idx_host) return fail(RGD_E_INVALID_ARG, "null argument");
+  if (B < 1 || B > kv->max_prompts) return fail(RGD_E_INVALID_ARG, "B out of range");
+  if (!kv->probe_held) return fail(RGD_E_STATE, "no probe to gate (call rgd_probe)");
+  hipStream_t s = (hipStream_t)stream;
+  rgd_model* m = const_cast<rgd_model*>(kv->m);
+  if (B > m->max_rows) return fail(RGD_E_INVALID_ARG, "B exceeds max_rows");
+  // device decision + ordered miss list into the model's scratch ints
+  int* d_dec = m->d_base;
+  int* d_nmiss = m->row_map;
+  int* d_miss = m->d_plen;
+  HIP_OK(hipEventSynchronize(m->stage_done));
+  HIP_OK(gate_decide(event, B, d_dec, d_nmiss, d_miss, s));
+  std::vector<int> tmp(2 * (size_t)B + 1);
+  HIP_OK(hipMemcpyAsync(decision_host, d_dec, (size_t)B * 4, hipMemcpyDeviceToHost, s));
+  HIP_OK(hipMemcpyAsync(n_miss_host, d_nmiss, 4, hipMemcpyDeviceToHost, s));
+  HIP_OK(hipMemcpyAsync(miss_idx_host, d_miss, (size_t)B * 4, hipMemcpyDeviceToHost, s));
+  HIP_OK(hipStreamSynchronize(s));
+  // drop every probe tail: pages go back to the pool, nothing is copied
+  for (auto& pp : kv->probe_pages) {
+    for (int p : pp) kv->free_pages.push_back(p);
+    pp.clear();
+  }
+  kv->probe_held = false;
+  return RGD_OK;
+}
+
+int32_t rgd_sample_continuations(rgd_model* m, rgd_kv* kv, const float* last_logits, const int32_t* prompt_idx,
+                                 int32_t n, int32_t N, int32_t steps, float T, float min_p, const uint64_t* seeds,
+                                 const int32_t* forced, float* logits_tap, int32_t* out, rgd_stream stream) {
+  g_err.clear();
+  if (!m || !kv || !last_logits || !prompt_idx || !seeds || !out) return fail(RGD_E_INVALID_ARG, "null argument");
+  if (kv->m != m) return fail(RGD_E_INVALID_ARG, "kv belongs to another model");
+  if (n < 1 || N < 1 || steps < 1) return fail(RGD_E_INVALID_ARG, "n, N and steps must be >= 1");
+  if ((long long)n * N > m->max_rows) return fail(RGD_E_INVALID_ARG, "n*N exceeds max_rows");
+  if (!(T >= 0.f) || !(min_p >= 0.f && min_p <= 1.f)) return fail(RGD_E_INVALID_ARG, "T must be >= 0, min_p in [0,1]");
+  if (kv->probe_held) return fail(RGD_E_STATE, "probe tails not released (call rgd_gate)");
+  for (int i = 0; i < n; ++i) {
+    const int b = prompt_idx[i];
+    if (b < 0 || b >= kv->max_prompts) return fail(RGD_E_INVALID_ARG, "prompt_idx out of range");
+    if (kv->plen[b] < 1) return fail(RGD_E_STATE, "prompt %d has no prefix", b);
+    if ((long long)kv->plen[b] + steps - 1 > m->cfg.max_pos) return fail(RGD_E_INVALID_ARG, "steps exceed max_pos");
+  }
+  const int R = n * N;
+  const int pages_per = (int)cdiv(steps - 1, kv->page_size);
+  if (pages_per > kv->max_pages) return fail(RGD_E_INVALID_ARG, "steps exceed the page table");
+  if ((long long)pages_per * R > (long long)kv->free_pages.size())
+    return fail(RGD_E_OOM, "page pool too small for %d rows of %d tokens", R, steps);
+  hipStream_t s = (hipStream_t)stream;
+  const int V = m->cfg.vocab;
+  // rows (prompt-major), page tables, row -> prompt logits map
+  HostRows h;
+  std::vector<int> pages((size_t)R * kv->max_pages, 0), map(R);
+  std::vector<int> taken;
+  for (int i = 0; i < n; ++i)
+    for (int j = 0; j < N; ++j) {
+      const int r = i * N + j, b = prompt_idx[i];
+      h.prompt.push_back(b);
+      h.base.push_back(kv->plen[b]);
+      h.plen.push_back(kv->plen[b]);
+      map[r] = b;
+      for (int p = 0; p < pages_per; ++p) {
+        const int pg = kv->free_pages.back();
+        kv->free_pages.pop_back();
+        taken.push_back(pg);
+        pages[(size_t)r * kv->max_pages + p] = pg;
+      }
+    }
+  build_blocks(m, h);
+  struct GiveBack {
+    rgd_kv* kv;
+    std::vector<int>& t;
+    ~GiveBack() {
+      for (auto it = t.rbegin(); it != t.rend(); ++it) kv->free_pages.push_back(*it);
+    }
+  } give{kv, taken};
+  RGD_TRY(upload(m,
+                 {{m->d_prompt, h.prompt.data(), (size_t)R},
+                  {m->d_base, h.base.data(), (size_t)R},
+                  {m->d_plen, h.plen.data(), (size_t)R},
+                  {(int*)m->d_rblocks, (const int*)h.blocks.data(), h.blocks.size() * 4},
+                  {kv->d_pages, pages.data(), pages.size()},
+                  {m->row_map, map.data(), (size_t)R}},
+                 s));
+  const unsigned long long* sd = (const unsigned long long*)seeds;
+  // step 0: every branch draws from its prompt's last-position logits
+  float* z0 = logits_tap ? logits_tap : m->logits;
+  hipLaunchKernelGGL(gather_rows_kernel, dim3((int)cdiv(V, 256 * 8), R), dim3(256), 0, s, last_logits, (long long)V,
+                     m->row_map, V, z0);
+  HIP_OK(hipGetLastError());
+  if (T > 0.f) HIP_OK(chunk_max(z0, V, R, V, kSampleChunk, m->tilemax, s));
+  RGD_TRY(select_tokens(m, z0, V, R, m->tilemax, m->nchunks, T, min_p, sd, 0u, out, steps, 0, m->cur_tok, s));
+  for (int st = 1; st < steps; ++st) {
+    Rows rows = device_rows(m, kv, R, st - 1, false);
+    const int* feed = forced ? forced + (st - 1) : m->cur_tok;
+    const int fstride = forced ? steps : 1;
+    RGD_TRY(forward_rows(m, kv, rows, h, feed, fstride, s));
+    float* z = logits_tap ? logits_tap + (size_t)st * R * V : m->logits;
+    RGD_TRY(lm_head(m, m->xn, m->cfg.d_model, R, z, s));
+    RGD_TRY(select_tokens(m, z, V, R, m->tilemax, m->ntiles, T, min_p, sd, (unsigned)st, out, steps, st,
+                          m->cur_tok, s));
+  }
+  // pages are returned to the pool by `give` (work on them stays ordered on `s`)
+  return RGD_OK;
+}
+
+int32_t rgd_check_status(rgd_model* m, rgd_stream stream) {
+  g_err.clear();
+  if (!m) return fail(RGD_E_INVALID_ARG, "null model");
+  int st = 0;
+  hipStream_t s = (hipStream_t)stream;
+  HIP_OK(hipMemcpyAsync(&st, m->status, 4, hipMemcpyDeviceToHost, s));
+  HIP_OK(hipStreamSynchronize(s));
+  if (st) {
+    HIP_OK(hipMemsetAsync(m->status, 0, 4, s));
+    HIP_OK(hipStreamSynchronize(s));
+    return fail(RGD_E_NONFINITE, "a logit row had a non-finite maximum");
+  }
+  return RGD_OK;
+}
+
+// --------------------------------------------------------- kernel-level ----
+int32_t rgd_kernel_attention(rgd_model* m, const void* q, int32_t R, const int32_t* row_prompt, const int32_t* plen,
+                             const void* prefix_k, const void* prefix_v, int32_t max_prompts, int32_t max_prefix,
+                             const void* pool_k, const void* pool_v, int32_t page_size, const int32_t* pages,
+                             int32_t max_pages, int32_t tail_len, int32_t splits, void* out, rgd_stream stream) {
+  g_err.clear();
+  if (!m || !q || !row_prompt || !plen || !prefix_k || !prefix_v || !out) return fail(RGD_E_INVALID_ARG, "null argument");
+  if (R < 1 || R > m->max_rows) return fail(RGD_E_INVALID_ARG, "R out of range");
+  if (max_prompts < 1 || max_prefix < 1 || tail_len < 0 || splits < 0) return fail(RGD_E_INVALID_ARG, "bad sizes");
+  if (tail_len > 0 && (!pool_k || !pool_v || !pages || page_size < 1 || max_pages < cdiv(tail_len, page_size)))
+    return fail(RGD_E_INVALID_ARG, "tail arguments inconsistent");
+  HostRows h;
+  for (int r = 0; r < R; ++r) {
+    if (row_prompt[r] < 0 || row_prompt[r] >= max_prompts) return fail(RGD_E_INVALID_ARG, "row_prompt out of range");
+    if (plen[r] < 0 || plen[r] > max_prefix) return fail(RGD_E_INVALID_ARG, "plen out of range");
+    if (r && row_prompt[r] != row_prompt[r - 1])
+      for (int p = 0; p < r; ++p)
+        if (row_prompt[p] == row_prompt[r]) return fail(RGD_E_INVALID_ARG, "rows of one prompt must be contiguous");
+    h.prompt.push_back(row_prompt[r]);
+    h.base.push_back(plen[r]);
+    h.plen.push_back(plen[r]);
+  }
+  build_blocks(m, h);
+  hipStream_t s = (hipStream_t)stream;
+  RGD_TRY(upload_rows(m, h, s));
+  Rows rows;
+  rows.R = R;
+  rows.prompt = m->d_prompt;
+  rows.base_pos = m->d_base;
+  rows.plen = m->d_plen;
+  rows.pages = pages;
+  rows.max_pages = max_pages;
+  rows.t = tail_len - 1;
+  rows.prefill = 0;
+  KVLayout kvl;
+  kvl.prefix_k = const_cast<void*>(prefix_k);
+  kvl.prefix_v = const_cast<void*>(prefix_v);
+  kvl.pool_k = const_cast<void*>(pool_k);
+  kvl.pool_v = const_cast<void*>(pool_v);
+  kvl.P = max_prefix;
+  kvl.page_size = page_size;
+  // q is read from the model's q buffer: copy the caller's q there first
+  const size_t qbytes = (size_t)R * m->cfg.n_heads * m->cfg.head_dim * m->esz;
+  HIP_OK(hipMemcpyAsync(m->q, q, qbytes, hipMemcpyDeviceToDevice, s));
+  return run_attention(m, kvl, rows, h, tail_len, splits, out, s);
+}
+
+int32_t rgd_kernel_lm_head(rgd_model* m, const void* hvec, int32_t R, float* logits, rgd_stream stream) {
+  g_err.clear();
+  if (!m || !hvec || !logits) return fail(RGD_E_INVALID_ARG, "null argument");
+  if (R < 1 || R > m->max_rows) return fail(RGD_E_INVALID_ARG, "R out of range");
+  return lm_head(m, hvec, m->cfg.d_model, R, logits, (hipStream_t)stream);
+}
+
+uint64_t rgd_sampler_workspace_bytes(int32_t R, int32_t V) {
+  if (R < 1 || V < 1) return 0;
+  const long long nch = cdiv(V, kSampleChunk);
+  // best u64 [R], counters u32 [R], chunk maxima f32 [R][nch], chunk sums f32 [R][nch]
+  return (uint64_t)(8LL * R + 4LL * R + 8LL * R * nch + 256);
+}
+
+int32_t rgd_kernel_argmax(const float* z, int32_t R, int32_t V, void* workspace, int32_t* out, rgd_stream stream) {
+  g_err.clear();
+  if (!z || !workspace || !out) return fail(RGD_E_INVALID_ARG, "null argument");
+  if (R < 1 || V < 1) return fail(RGD_E_INVALID_ARG, "R and V must be >= 1");
+  if ((uintptr_t)workspace % 256) return fail(RGD_E_INVALID_ARG, "workspace must be 256-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  unsigned long long* best = (unsigned long long*)workspace;
+  HIP_OK(fill_u32((uint32_t*)best, 0u, 2LL * R, s));
+  HIP_OK(argmax_rows(z, V, R, V, best, s));
+  hipLaunchKernelGGL(argmax_finish_kernel, dim3((R + 255) / 256), dim3(256), 0, s, best, R, out, 1LL, 0,
+                     (int*)nullptr);
+  HIP_OK(hipGetLastError());
+  return RGD_OK;
+}
+
+int32_t rgd_kernel_sample(const float* z, int32_t R, int32_t V, float T, float min_p, const uint64_t* seeds,
+                          uint32_t ctr, uint32_t stream0, int32_t draws, void* workspace, int32_t* out,
+                          rgd_stream stream) {
+  g_err.clear();
+  if (!z || !seeds || !workspace || !out) return fail(RGD_E_INVALID_ARG, "null argument");
+  if (R < 1 || V < 4 || V % 4 || (long long)V > 256LL * kSampleChunk || draws < 1)
+    return fail(RGD_E_INVALID_ARG, "bad R/V/draws");
+  if (!(T > 0.f) || !(min_p >= 0.f && min_p <= 1.f)) return fail(RGD_E_INVALID_ARG, "T must be > 0, min_p in [0,1]");
+  if ((uintptr_t)workspace % 256) return fail(RGD_E_INVALID_ARG, "workspace must be 256-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  const int nch = (int)cdiv(V, kSampleChunk);
+  char* w = (char*)workspace;
+  unsigned* counters = (unsigned*)(w + 8LL * R);
+  float* cmax = (float*)(w + 12LL * R);
+  float* csum = cmax + (long long)R * nch;
+  HIP_OK(fill_u32(counters, 0u, R, s));
+  HIP_OK(chunk_max(z, V, R, V, kSampleChunk, cmax, s));
+  SampleArgs a{};
+  a.z = z;
+  a.ldz = V;
+  a.R = R;
+  a.V = V;
+  a.pmax = cmax;
+  a.npmax = nch;
+  a.T = T;
+  a.p_min = min_p;
+  a.chunk = kSampleChunk;
+  a.nchunks = nch;
+  a.chunk_sums = csum;
+  a.counters = counters;
+  a.seeds = (const unsigned long long*)seeds;
+  a.ctr = ctr;
+  a.stream = stream0;
+  a.out = out;
+  a.out_stride = draws;
+  a.out_col = 0;
+  a.cur_tok = nullptr;
+  a.status = nullptr;
+  HIP_OK(minp_sample(a, s));
+  if (draws > 1) HIP_OK(minp_multi_draw(a, draws, stream0, out, s));
+  return RGD_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,294 @@
+// Token selection and the refusal gate.
+//
+// min-p sampling (temperature first): with m the row maximum, a token is kept
+// when w_i = exp2((z_i - m) * log2(e) / T) >= p_min, and the draw returns the
+// smallest kept id whose running kept-weight sum exceeds u * W.  Each row is
+// split into chunks handled by independent workgroups; every chunk's kept sum
+// goes to global memory, and the last workgroup of a row to finish (found with
+// a device-scope counter, no spinning) forms the chunk prefix in chunk order,
+// locates u * W and rescans that one chunk with a block-wide prefix scan.
+// Logits are therefore read once per draw from HBM; the row maximum comes in as
+// partial maxima (from the LM-head epilogue or a chunk-max pass).
+#include "kernels.hpp"
+#include "philox.hpp"
+
+namespace rgd {
+
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+__global__ void fill_u32_kernel(uint32_t* p, uint32_t v, long long n) {
+  for (long long i = blockIdx.x * 256ll + threadIdx.x; i < n; i += 256ll * gridDim.x) p[i] = v;
+}
+
+__global__ __launch_bounds__(256) void chunk_max_kernel(const float* z, long long ldz, int V, int chunk,
+                                                        float* cmax) {
+  __shared__ float red[4];
+  const int c = blockIdx.x, r = blockIdx.y;
+  const float* zr = z + r * ldz;
+  const int lo = c * chunk, hi = min(V, lo + chunk);
+  float mx = -INFINITY;
+  for (int i = lo + threadIdx.x; i < hi; i += 256) mx = fmaxf(mx, zr[i]);
+  mx = block_max(mx, red);
+  if (threadIdx.x == 0) cmax[(long long)r * gridDim.x + c] = mx;
+}
+
+RGD_DEV unsigned long long pack_key(float v, int idx) {
+  return ((unsigned long long)ordered_u32(v) << 32) | (unsigned long long)(0xFFFFFFFFu - uint32_t(idx));
+}
+
+__global__ __launch_bounds__(256) void argmax_kernel(const float* z, long long ldz, int V, int chunk,
+                                                     unsigned long long* best) {
+  __shared__ unsigned long long red[4];
+  const int c = blockIdx.x, r = blockIdx.y;
+  const float* zr = z + r * ldz;
+  const int lo = c * chunk, hi = min(V, lo + chunk);
+  unsigned long long k = 0;
+  for (int i = lo + threadIdx.x; i < hi; i += 256) {
+    const unsigned long long ki = pack_key(zr[i], i);
+    k = ki > k ? ki : k;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const unsigned long long t = __shfl_xor(k, o, 64);
+    k = t > k ? t : k;
+  }
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = k;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned long long t = red[0];
+    for (int i = 1; i < 4; ++i) t = red[i] > t ? red[i] : t;
+    atomicMax(best + r, t);
+  }
+}
+
+RGD_DEV float row_max_from_partials(const float* pmax, int npmax, int r, float* red) {
+  float mx = -INFINITY;
+  for (int i = threadIdx.x; i < npmax; i += 256) mx = fmaxf(mx, pmax[(long long)r * npmax + i]);
+  return block_max(mx, red);
+}
+
+// Inclusive block scan (256 threads) of one float per thread.
+RGD_DEV float block_inclusive_scan(float v, float* wsum) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const float t = __shfl_up(v, o, 64);
+    if (lane >= o) v += t;
+  }
+  __syncthreads();
+  if (lane == 63) wsum[w] = v;
+  __syncthreads();
+  float off = 0.f;
+  for (int i = 0; i < w; ++i) off += wsum[i];
+  return v + off;
+}
+
+// Selects the token of row r for target u (in [0,1)) given the chunk sums.
+// Returns the token id (valid in thread 0).
+RGD_DEV int select_token(const SampleArgs& a, int r, float mx, float u) {
+  __shared__ float csum[256];
+  __shared__ int sh_chunk;
+  __shared__ float sh_base, sh_target;
+  __shared__ float wsum[4];
+  __shared__ int red_i[4];
+  const float kT = kLog2e / a.T;
+  if (threadIdx.x == 0) {
+    float acc = 0.f;
+    for (int c = 0; c < a.nchunks; ++c) {
+      acc += __hip_atomic_load(a.chunk_sums + (long long)r * a.nchunks + c, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+      csum[c] = acc;
+    }
+    const float target = u * acc;
+    int cs = -1, last_nz = 0;
+    for (int c = 0; c < a.nchunks; ++c) {
+      const float prev = c ? csum[c - 1] : 0.f;
+      if (csum[c] > prev) last_nz = c;
+      if (cs < 0 && csum[c] > target) cs = c;
+    }
+    if (cs < 0) cs = last_nz;
+    sh_chunk = cs;
+    sh_base = cs ? csum[cs - 1] : 0.f;
+    sh_target = target;
+  }
+  __syncthreads();
+  const int lo = sh_chunk * a.chunk, hi = min(a.V, lo + a.chunk);
+  const int per = a.chunk / 256;
+  const int e0 = lo + threadIdx.x * per, e1 = min(hi, e0 + per);
+  const float* zr = a.z + r * a.ldz;
+  float ts = 0.f;
+  for (int i = e0; i < e1; ++i) {
+    const float w = exp2f((zr[i] - mx) * kT);
+    if (w >= a.p_min) ts += w;
+  }
+  const float incl = block_inclusive_scan(ts, wsum);
+  float run = sh_base + (incl - ts);
+  int found = 0x7FFFFFFF, last = -1;
+  for (int i = e0; i < e1; ++i) {
+    const float w = exp2f((zr[i] - mx) * kT);
+    if (w >= a.p_min) {
+      run += w;
+      last = i;
+      if (found == 0x7FFFFFFF && run > sh_target) found = i;
+    }
+  }
+  // smallest found index, else the last kept index of the chunk
+  int f = found;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) f = min(f, __shfl_xor(f, o, 64));
+  int l = last;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) l = max(l, __shfl_xor(l, o, 64));
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red_i[threadIdx.x >> 6] = f;
+  __syncthreads();
+  int fb = red_i[0];
+  for (int i = 1; i < 4; ++i) fb = min(fb, red_i[i]);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red_i[threadIdx.x >> 6] = l;
+  __syncthreads();
+  int lb = red_i[0];
+  for (int i = 1; i < 4; ++i) lb = max(lb, red_i[i]);
+  return fb != 0x7FFFFFFF ? fb : lb;
+}
+
+__global__ __launch_bounds__(256) void minp_sum_kernel(SampleArgs a) {
+  __shared__ float red[4];
+  __shared__ int is_last;
+  const int c = blockIdx.x, r = blockIdx.y;
+  const float mx = row_max_from_partials(a.pmax, a.npmax, r, red);
+  const float kT = kLog2e / a.T;
+  const float* zr = a.z + r * a.ldz;
+  const int lo = c * a.chunk, hi = min(a.V, lo + a.chunk);
+  float sum = 0.f;
+  for (int i = lo + threadIdx.x * 4; i < hi; i += 1024) {
+    const float4 v = *(const float4*)(zr + i);  // V and chunk are multiples of 4
+    const float w0 = exp2f((v.x - mx) * kT), w1 = exp2f((v.y - mx) * kT);
+    const float w2 = exp2f((v.z - mx) * kT), w3 = exp2f((v.w - mx) * kT);
+    sum += (w0 >= a.p_min ? w0 : 0.f) + (w1 >= a.p_min ? w1 : 0.f) + (w2 >= a.p_min ? w2 : 0.f) +
+           (w3 >= a.p_min ? w3 : 0.f);
+  }
+  sum = block_sum(sum, red);
+  if (threadIdx.x == 0) {
+    __hip_atomic_store(a.chunk_sums + (long long)r * a.nchunks + c, sum, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+    __threadfence();
+    const unsigned prev = __hip_atomic_fetch_add(a.counters + r, 1u, __ATOMIC_ACQ_REL,
+                                                 __HIP_MEMORY_SCOPE_AGENT);
+    is_last = prev == unsigned(a.nchunks - 1);
+  }
+  __syncthreads();
+  if (!is_last) return;
+  __threadfence();
+  if (!(mx > -INFINITY && mx < INFINITY) && threadIdx.x == 0 && a.status) atomicOr(a.status, 1);
+  const float u = philox_uniform(a.seeds[r], a.ctr, a.stream);
+  const int tok = select_token(a, r, mx, u);
+  if (threadIdx.x == 0) {
+    a.out[r * a.out_stride + a.out_col] = tok;
+    if (a.cur_tok) a.cur_tok[r] = tok;
+    a.counters[r] = 0u;
+  }
+}
+
+__global__ __launch_bounds__(256) void minp_multi_kernel(SampleArgs a, unsigned stream0, int draws,
+                                                         int* out) {
+  __shared__ float red[4];
+  const int d = blockIdx.x, r = blockIdx.y;
+  const float mx = row_max_from_partials(a.pmax, a.npmax, r, red);
+  const float u = philox_uniform(a.seeds[r], a.ctr, stream0 + unsigned(d));
+  const int tok = select_token(a, r, mx, u);
+  if (threadIdx.x == 0) out[(long long)r * draws + d] = tok;
+}
+
+// ------------------------------------------------------------------ gate ----
+__global__ __launch_bounds__(64) void probe_update_kernel(GateArgs a) {
+  const int r = blockIdx.x;
+  const int b = a.row_prompt[r];
+  const unsigned long long key = a.best[r];
+  __syncthreads();
+  if (threadIdx.x == 0) a.best_reset[r] = 0ull;
+  if (a.event[b] != -1) return;
+  const int tok = int(0xFFFFFFFFu - uint32_t(key & 0xFFFFFFFFull));
+  const int j = a.probe_len[b];
+  const int* q = a.probe_tokens + (long long)b * a.k;
+  bool any = false;
+  for (int e = threadIdx.x; e < a.n_entries; e += 64) {
+    if (a.owner && a.owner[e] != -1 && a.owner[e] != b) continue;
+    const int o0 = a.offsets[e], len = a.offsets[e + 1] - o0;
+    if (len < a.min_match) continue;
+    const int n = min(len, j + 1);
+    bool match = true;
+    for (int i = 0; i < n && match; ++i) match = a.tokens[o0 + i] == (i < j ? q[i] : tok);
+    any = any || match;
+  }
+  const bool compat = __any(any);
+  if (threadIdx.x == 0) {
+    a.probe_tokens[(long long)b * a.k + j] = tok;
+    a.probe_len[b] = j + 1;
+    if (a.cur_tok) a.cur_tok[r] = tok;
+    a.event[b] = !compat ? 0 : (a.eos >= 0 && tok == a.eos) ? 1 : (j + 1 >= a.k) ? 2 : -1;
+  }
+}
+
+__global__ void gate_decide_kernel(const int* event, int B, int* decision, int* n_miss, int* miss_idx) {
+  if (threadIdx.x != 0) return;
+  int n = 0;
+  for (int b = 0; b < B; ++b) {
+    const int hit = (event[b] == 1 || event[b] == 2) ? 1 : 0;
+    decision[b] = hit;
+    if (!hit) miss_idx[n++] = b;
+  }
+  *n_miss = n;
+}
+
+}  // namespace
+
+hipError_t fill_u32(uint32_t* p, uint32_t v, long long n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int blocks = int(min(1024ll, (n + 255) / 256));
+  hipLaunchKernelGGL(fill_u32_kernel, dim3(blocks), dim3(256), 0, s, p, v, n);
+  return hipGetLastError();
+}
+
+hipError_t chunk_max(const float* z, long long ldz, int R, int V, int chunk, float* cmax, hipStream_t s) {
+  hipLaunchKernelGGL(chunk_max_kernel, dim3((V + chunk - 1) / chunk, R), dim3(256), 0, s, z, ldz, V, chunk,
+                     cmax);
+  return hipGetLastError();
+}
+
+hipError_t argmax_rows(const float* z, long long ldz, int R, int V, unsigned long long* best,
+                       hipStream_t s) {
+  const int chunk = 4096;
+  hipLaunchKernelGGL(argmax_kernel, dim3((V + chunk - 1) / chunk, R), dim3(256), 0, s, z, ldz, V, chunk,
+                     best);
+  return hipGetLastError();
+}
+
+hipError_t minp_sample(const SampleArgs& a, hipStream_t s) {
+  if (a.chunk % 1024 || a.chunk / 256 * 256 != a.chunk || a.V % 4 || a.nchunks > 256 ||
+      a.nchunks * a.chunk < a.V || !(a.T > 0.f))
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(minp_sum_kernel, dim3(a.nchunks, a.R), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t minp_multi_draw(const SampleArgs& a, int draws, unsigned int stream0, int* out, hipStream_t s) {
+  if (draws <= 0) return hipSuccess;
+  hipLaunchKernelGGL(minp_multi_kernel, dim3(draws, a.R), dim3(256), 0, s, a, stream0, draws, out);
+  return hipGetLastError();
+}
+
+hipError_t probe_update(const GateArgs& a, hipStream_t s) {
+  if (a.R <= 0) return hipSuccess;
+  hipLaunchKernelGGL(probe_update_kernel, dim3(a.R), dim3(64), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t gate_decide(const int* event, int B, int* decision, int* n_miss, int* miss_idx, hipStream_t s) {
+  hipLaunchKernelGGL(gate_decide_kernel, dim3(1), dim3(64), 0, s, event, B, decision, n_miss, miss_idx);
+  return hipGetLastError();
+}
+
+}  // namespace rgd

@@ -1,0 +1,187 @@
+"""The tiny fp32 decoder end to end (prefill, probe, gate, sampling) vs the
+oracle, free-running, plus the path invariants: a gated miss equals ungated
+sampling with the same seeds, the shared prefix is never modified, and runs
+are deterministic."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import gate as ogate
+from oracle import philox, rgd as orgd, sampler
+from oracle.model import Decoder, KVCache
+from tests.gpu_common import rel_err, seeds_tensor, torch
+
+pytestmark = pytest.mark.gpu
+W0 = synth.C0
+MARGIN = 1e-4
+
+
+@pytest.fixture(scope="module")
+def rgd():
+    import paper_2607_20791_amd as m
+    return m
+
+
+@pytest.fixture(scope="module")
+def world():
+    """Oracle state: prefilled prompts, greedy sequences and per-prompt tables
+    (even prompts seeded to hit with the first 4 greedy tokens)."""
+    weights = synth.model_weights(W0)
+    dec = Decoder(weights)
+    prompts = synth.prompt_tokens(W0)
+    caches, last = [], []
+    for b in range(W0.n_prompts):
+        c = KVCache(W0.n_layers)
+        last.append(dec.prefill(prompts[b], c))
+        caches.append(c)
+    greedy, gmargin = [], []
+    for b in range(W0.n_prompts):
+        tail = KVCache(W0.n_layers)
+        lg = last[b]
+        seq, mg = [], []
+        while True:
+            seq.append(sampler.argmax(lg))
+            mg.append(sampler.logit_margin_argmax(lg))
+            if len(seq) == W0.probe_k:
+                break
+            lg = dec.decode(seq[-1], caches[b], tail)
+        greedy.append(seq)
+        gmargin.append(mg)
+    tables, owners = [], []
+    for b in range(W0.n_prompts):
+        off, tok = synth.random_table(W0, f"table{b}")
+        ents = ogate.table_entries(off, tok)
+        if b % 2 == 0:
+            ents[0] = greedy[b][:4]
+        tables.append(ents)
+    return dict(weights=weights, dec=dec, prompts=prompts, caches=caches, last=last, greedy=greedy,
+                gmargin=gmargin, tables=tables)
+
+
+def _gpu_setup(rgd, world):
+    from paper_2607_20791_amd import session
+    m = session.build_model(world["weights"], max_rows=64, max_pos=128)
+    kv = session.alloc_kv(m, W0, max_prompts=W0.n_prompts, max_prefix=W0.prompt_len, n_pages=96)
+    return m, kv
+
+
+def _csr(tables):
+    offs, toks, own = [0], [], []
+    for b, ents in enumerate(tables):
+        for e in ents:
+            toks.extend(e)
+            offs.append(len(toks))
+            own.append(b)
+    return offs, toks, own
+
+
+def test_fp32_path_end_to_end(rgd, world):
+    t = torch()
+    from paper_2607_20791_amd import session
+    m, kv = _gpu_setup(rgd, world)
+    B, V = W0.n_prompts, W0.vocab
+    toks = session.to_device(world["prompts"])
+    last = t.empty(B, V, dtype=t.float32, device="cuda")
+    rgd.prefill_kv(m, kv, toks, 0, last)
+    t.cuda.synchronize()
+    err = rel_err(last.cpu().numpy(), np.stack(world["last"]))
+    print("prefill logits rel err", err.max())
+    assert err.max() <= 1e-5
+
+    # probe + gate
+    offs, tks, own = _csr(world["tables"])
+    table = rgd.Table(offs, tks, own, min_match=2)
+    k = W0.probe_k
+    ptok = t.empty(B, k, dtype=t.int32, device="cuda")
+    plen = t.empty(B, dtype=t.int32, device="cuda")
+    ev = t.empty(B, dtype=t.int32, device="cuda")
+    before = (kv.prefix_k.clone(), kv.prefix_v.clone())
+    rgd.probe(m, kv, last, table, B, k, 3, -1, ptok, plen, ev)
+    dec_h, miss = rgd.gate(kv, ev, B)
+    ptok_h, plen_h, ev_h = ptok.cpu().numpy(), plen.cpu().numpy(), ev.cpu().numpy()
+    hits = 0
+    for b in range(B):
+        # oracle probe = greedy sequence cut by the table
+        seq = world["greedy"][b]
+        q = []
+        e = None
+        for y in seq:
+            q.append(y)
+            if not ogate.compatible(q, world["tables"][b]):
+                e = ogate.INCOMPAT
+                break
+            if len(q) == k:
+                e = ogate.MAXLEN
+        n_cmp = len(q)
+        clean = all(mg >= MARGIN for mg in world["gmargin"][b][:n_cmp])
+        if clean:
+            assert plen_h[b] == len(q) and list(ptok_h[b, :len(q)]) == q, b
+            assert ev_h[b] == e and dec_h[b] == int(ogate.is_hit(e)), b
+        hits += int(dec_h[b])
+    print("hits", hits, "misses", list(miss))
+    assert hits >= 1 and len(miss) >= 1
+    assert all(dec_h[b] == 1 for b in range(0, B, 2))     # seeded prompts hit
+
+    # sampling for the misses
+    N, S = W0.n_branches, W0.steps
+    seeds = np.array([b for b in miss for _ in range(N)], dtype=np.uint64)
+    out = t.full((len(miss), N, S), -1, dtype=t.int32, device="cuda")
+    rgd.sample_continuations(m, kv, last, list(miss), N, S, W0.temperature, W0.min_p,
+                             seeds_tensor(seeds), out)
+    t.cuda.synchronize()
+    rgd.check_status(m)
+    got = out.cpu().numpy()
+    assert t.equal(before[0], kv.prefix_k) and t.equal(before[1], kv.prefix_v)
+    compared = 0
+    for i, b in enumerate(miss):
+        br = orgd.sample_branch(world["dec"], world["caches"][b], world["last"][b], int(b), S,
+                                W0.temperature, W0.min_p)
+        for s in range(S):
+            d = br.draws[s]
+            if d.cdf_margin < MARGIN or d.logit_margin < MARGIN:
+                break
+            assert got[i, 0, s] == br.tokens[s], (b, s)
+            compared += 1
+    print("sampled tokens compared", compared, "of", len(miss) * S)
+    assert compared >= len(miss) * 4
+
+    # ungated sampling from a fresh KV (no probe ever ran) gives the same tokens
+    kv2 = session.alloc_kv(m, W0, max_prompts=B, max_prefix=W0.prompt_len, n_pages=96)
+    last2 = t.empty(B, V, dtype=t.float32, device="cuda")
+    rgd.prefill_kv(m, kv2, toks, 0, last2)
+    out2 = t.full_like(out, -1)
+    rgd.sample_continuations(m, kv2, last2, list(miss), N, S, W0.temperature, W0.min_p,
+                             seeds_tensor(seeds), out2)
+    t.cuda.synchronize()
+    assert t.equal(out, out2)
+    assert t.equal(last, last2)
+
+
+def test_fp32_teacher_forced_logits(rgd, world):
+    """Logits at every step of a teacher-forced branch (synthetic history) match
+    the oracle's at 1e-5, and the drawn tokens match where margins allow."""
+    t = torch()
+    from paper_2607_20791_amd import session
+    m, kv = _gpu_setup(rgd, world)
+    B, V = W0.n_prompts, W0.vocab
+    last = t.empty(B, V, dtype=t.float32, device="cuda")
+    rgd.prefill_kv(m, kv, session.to_device(world["prompts"]), 0, last)
+    prompts, N, S = [1, 5], 2, 12
+    forced = synth.forced_history(W0, len(prompts) * N, S)
+    seeds = np.arange(len(prompts) * N, dtype=np.uint64) + 77
+    out = t.full((len(prompts), N, S), -1, dtype=t.int32, device="cuda")
+    tap = t.empty(S, len(prompts) * N, V, dtype=t.float32, device="cuda")
+    rgd.sample_continuations(m, kv, last, prompts, N, S, 1.5, 0.05, seeds_tensor(seeds), out,
+                             forced=session.to_device(forced), logits_tap=tap)
+    t.cuda.synchronize()
+    tap_h, got = tap.cpu().numpy(), out.cpu().numpy().reshape(-1, S)
+    for r in range(len(prompts) * N):
+        b = prompts[r // N]
+        br = orgd.sample_branch(world["dec"], world["caches"][b], world["last"][b], int(seeds[r]), S,
+                                1.5, 0.05, forced=forced[r], keep_logits=True)
+        err = rel_err(tap_h[:, r], np.stack(br.logits))
+        assert err.max() <= 1e-5, (r, err.max())
+        for s in range(S):
+            d = br.draws[s]
+            if d.cdf_margin >= MARGIN and d.logit_margin >= MARGIN:
+                assert got[r, s] == br.tokens[s], (r, s)

@@ -1,0 +1,116 @@
+"""Sampler and argmax kernels vs the oracle on identical fp32 logits (the
+sampler sweep workload: V=152064, 256 rows, Zipf-biased logits)."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import philox, sampler
+from tests.gpu_common import argmax_gpu, sample_gpu
+
+pytestmark = pytest.mark.gpu
+MARGIN = 1e-4
+
+
+@pytest.fixture(scope="module")
+def rgd():
+    import paper_2607_20791_amd as m
+    return m
+
+
+@pytest.fixture(scope="module")
+def z():
+    return synth.sweep_logits()
+
+
+def test_argmax_matches_oracle(rgd, z):
+    got = argmax_gpu(rgd, z)
+    want = np.array([sampler.argmax(r) for r in z])
+    assert np.array_equal(got, want)
+
+
+def test_argmax_ties_lowest_index(rgd):
+    g = np.random.default_rng(3)
+    z = g.normal(size=(5, 9000)).astype(np.float32)
+    for r, pos in enumerate([(0, 7), (100, 8191), (4095, 4096), (8999, 3), (10, 20, 8998)]):
+        for p in pos:
+            z[r, p] = 50.0
+    got = argmax_gpu(rgd, z)
+    assert list(got) == [0, 100, 4095, 3, 10]
+
+
+def _check_rows(z, T, pmin, got, seeds, ctr, stream):
+    exact = margin = 0
+    for r in range(got.shape[0]):
+        u = float(philox.uniform(int(seeds[r]), ctr, stream))
+        d = sampler.sample_minp(z[r], T, pmin, u)
+        if d.cdf_margin < MARGIN or d.logit_margin < MARGIN:
+            margin += 1
+            kept = sampler.minp_weights(z[r], T, pmin)[1]
+            assert kept[got[r]], (r, got[r])
+            continue
+        assert got[r] == d.token, (r, T, pmin, got[r], d)
+        exact += 1
+    return exact, margin
+
+
+@pytest.mark.parametrize("T", synth.C3.temperatures)
+@pytest.mark.parametrize("pmin", synth.C3.min_ps)
+def test_minp_single_draw_grid(rgd, z, T, pmin):
+    rows = z[:48]
+    seeds = np.arange(48, dtype=np.uint64)
+    got = sample_gpu(rgd, rows, T, pmin, seeds, ctr=0, stream0=0, draws=1)[:, 0]
+    exact, margin = _check_rows(rows, T, pmin, got, seeds, 0, 0)
+    print(f"T={T} p_min={pmin}: exact {exact}, margin cases {margin}")
+    assert exact >= 40
+
+
+def test_minp_all_rows_one_point(rgd, z):
+    seeds = np.arange(256, dtype=np.uint64)
+    got = sample_gpu(rgd, z, 2.0, 0.05, seeds, ctr=7, stream0=0)[:, 0]
+    exact, margin = _check_rows(z, 2.0, 0.05, got, seeds, 7, 0)
+    assert exact + margin == 256 and exact >= 240
+
+
+def test_thousand_draws_match_and_follow_kept_distribution(rgd, z):
+    from scipy import stats
+    rows = z[:6]
+    seeds = np.arange(6, dtype=np.uint64) + 1000
+    T, pmin, D = 1.5, 0.1, 1000
+    got = sample_gpu(rgd, rows, T, pmin, seeds, ctr=0, stream0=0, draws=D)
+    for r in range(rows.shape[0]):
+        us = philox.uniform(int(seeds[r]), 0, np.arange(D, dtype=np.uint64))
+        draws = sampler.sample_minp_many(rows[r], T, pmin, us)
+        ok = [d.cdf_margin >= MARGIN and d.logit_margin >= MARGIN for d in draws]
+        want = np.array([d.token for d in draws])
+        assert np.array_equal(got[r][ok], want[ok])
+        p = sampler.kept_probabilities(rows[r], T, pmin)
+        support = np.flatnonzero(p > 0)
+        assert set(np.unique(got[r])) <= set(support)
+        exp = p[support] * D
+        obs = np.bincount(got[r], minlength=len(p))[support]
+        big = exp >= 5
+        o = np.append(obs[big], obs[~big].sum())
+        e = np.append(exp[big], exp[~big].sum())
+        if e[-1] < 1e-9:
+            o, e = o[:-1], e[:-1]
+        if len(e) > 1:
+            assert stats.chisquare(o, e).pvalue > 1e-4
+
+
+def test_edge_cases_tiny_vocab(rgd):
+    z = np.array([[0.0, 3.0, 1.0, 3.0, -2.0, 0.5, 2.9, 1.0]] * 4, np.float32)
+    seeds = np.arange(4, dtype=np.uint64)
+    got = sample_gpu(rgd, z, 1.0, 1.0, seeds, draws=50)
+    assert set(np.unique(got)) == {1, 3}   # p_min = 1 keeps exactly the tied maxima
+    got = sample_gpu(rgd, z, 1.0, 0.0, seeds, draws=400)
+    assert set(np.unique(got)) == set(range(8))
+    got = sample_gpu(rgd, z, 5.0, 0.5, seeds, draws=200)
+    kept = sampler.minp_weights(z[0], 5.0, 0.5)[1]
+    assert set(np.unique(got)) <= set(np.flatnonzero(kept))
+
+
+def test_deterministic(rgd, z):
+    seeds = np.arange(64, dtype=np.uint64) * 7919
+    a = sample_gpu(rgd, z[:64], 3.0, 0.05, seeds, ctr=3, draws=4)
+    b = sample_gpu(rgd, z[:64], 3.0, 0.05, seeds, ctr=3, draws=4)
+    assert np.array_equal(a, b)

@@ -87,3 +87,14 @@ def test_margins_reported():
     assert d.logit_margin < 1e-12
     d = sampler.sample_minp(np.array([0.0, 0.0]), 1.0, 0.1, 0.5)   # u*W on the CDF edge
     assert d.cdf_margin == 0.0 and d.token == 1
+
+
+def test_many_matches_single():
+    g = np.random.default_rng(21)
+    z = g.normal(size=700) * 2
+    us = g.random(300)
+    many = sampler.sample_minp_many(z, 1.3, 0.07, us)
+    for u, d in zip(us, many):
+        one = sampler.sample_minp(z, 1.3, 0.07, u)
+        assert d.token == one.token
+        assert np.isclose(d.cdf_margin, one.cdf_margin, rtol=0, atol=1e-15)
