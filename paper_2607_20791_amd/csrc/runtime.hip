@@ -644,6 +644,20 @@ int32_t rgd_kv_create(const rgd_model* m, int32_t max_prompts, int32_t max_prefi
     delete kv;
     return fail(RGD_E_OOM, "page-table allocation failed");
   }
+  // the model's pinned staging must hold one page table plus the row arrays
+  rgd_model* mm = const_cast<rgd_model*>(m);
+  const size_t need = (size_t)m->max_rows * (kv->max_pages + 8) + 64;
+  if (mm->stage_ints < need) {
+    int* p = nullptr;
+    if (hipEventSynchronize(mm->stage_done) != hipSuccess ||
+        hipHostMalloc((void**)&p, need * sizeof(int), hipHostMallocDefault) != hipSuccess) {
+      delete kv;
+      return fail(RGD_E_OOM, "pinned staging allocation failed");
+    }
+    (void)hipHostFree(mm->h_stage);
+    mm->h_stage = p;
+    mm->stage_ints = need;
+  }
   *out = kv;
   return RGD_OK;
 }

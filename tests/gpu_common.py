@@ -46,3 +46,37 @@ def argmax_gpu(rgd, z_np):
     rgd.kernel_argmax(z, ws, out)
     t.cuda.synchronize()
     return out.cpu().numpy()
+
+
+MARGIN = 1e-4
+
+
+def judge_draw(z, T, pmin, u, got, margin=MARGIN):
+    """Classifies one GPU draw against the oracle on the same logits.
+
+    Outside margin cases (oracle CDF margin and min-p logit margin >= margin)
+    the token must be identical.  In a margin case the GPU token must still be
+    a valid outcome: kept under the mask relaxed by the margin, with its CDF
+    interval within margin * W (plus the weight of tokens whose mask decision
+    is itself within the margin) of u * W.
+    Returns "exact", "margin-equal" or "margin-diff"."""
+    from oracle import sampler
+    d = sampler.sample_minp(z, T, pmin, u)
+    if d.cdf_margin >= margin and d.logit_margin >= margin:
+        assert got == d.token, (got, d)
+        return "exact"
+    if got == d.token:
+        return "margin-equal"
+    w, _ = sampler.minp_weights(z, T, pmin)
+    lw = np.log(np.maximum(w, 1e-300))
+    amb = np.abs(lw - np.log(pmin)) < margin if pmin > 0 else np.zeros_like(w, bool)
+    kept = w >= pmin * np.exp(-margin)
+    assert kept[got], ("token outside the relaxed min-p set", got)
+    wk = np.where(w >= pmin, w, 0.0)
+    W = wk.sum()
+    c = np.cumsum(wk)
+    lo, hi = c[got] - wk[got], c[got]
+    t = u * W
+    slack = margin * W + w[amb].sum()
+    assert lo - slack <= t <= hi + slack, ("draw too far from u*W", got, d.token)
+    return "margin-diff"

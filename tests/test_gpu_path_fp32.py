@@ -9,7 +9,7 @@ import synth
 from oracle import gate as ogate
 from oracle import philox, rgd as orgd, sampler
 from oracle.model import Decoder, KVCache
-from tests.gpu_common import rel_err, seeds_tensor, torch
+from tests.gpu_common import judge_draw, rel_err, seeds_tensor, torch
 
 pytestmark = pytest.mark.gpu
 W0 = synth.C0
@@ -132,18 +132,18 @@ def test_fp32_path_end_to_end(rgd, world):
     rgd.check_status(m)
     got = out.cpu().numpy()
     assert t.equal(before[0], kv.prefix_k) and t.equal(before[1], kv.prefix_v)
-    compared = 0
+    counts = {"exact": 0, "margin-equal": 0, "margin-diff": 0}
     for i, b in enumerate(miss):
         br = orgd.sample_branch(world["dec"], world["caches"][b], world["last"][b], int(b), S,
-                                W0.temperature, W0.min_p)
+                                W0.temperature, W0.min_p, keep_logits=True)
         for s in range(S):
-            d = br.draws[s]
-            if d.cdf_margin < MARGIN or d.logit_margin < MARGIN:
-                break
-            assert got[i, 0, s] == br.tokens[s], (b, s)
-            compared += 1
-    print("sampled tokens compared", compared, "of", len(miss) * S)
-    assert compared >= len(miss) * 4
+            u = float(philox.uniform(int(b), s))
+            verdict = judge_draw(br.logits[s], W0.temperature, W0.min_p, u, int(got[i, 0, s]))
+            counts[verdict] += 1
+            if verdict == "margin-diff":
+                break       # the histories differ from here on
+    print("sampled tokens:", counts, "of", len(miss) * S)
+    assert counts["exact"] + counts["margin-equal"] >= len(miss) * S // 2
 
     # ungated sampling from a fresh KV (no probe ever ran) gives the same tokens
     kv2 = session.alloc_kv(m, W0, max_prompts=B, max_prefix=W0.prompt_len, n_pages=96)
@@ -182,6 +182,4 @@ def test_fp32_teacher_forced_logits(rgd, world):
         err = rel_err(tap_h[:, r], np.stack(br.logits))
         assert err.max() <= 1e-5, (r, err.max())
         for s in range(S):
-            d = br.draws[s]
-            if d.cdf_margin >= MARGIN and d.logit_margin >= MARGIN:
-                assert got[r, s] == br.tokens[s], (r, s)
+            judge_draw(br.logits[s], 1.5, 0.05, float(philox.uniform(int(seeds[r]), s)), int(got[r, s]))
