@@ -1,0 +1,238 @@
+#!/usr/bin/env python3
+"""Benchmark of the refusal-gated decode hot path on one MI355X.
+
+Workload: one Llama-3-8B-shaped decoder layer in bf16 (d=4096, 32/8 heads,
+D=128, SwiGLU 14336, vocab 128256, random init) over a shared prompt KV of 8192
+synthetic N(0,1) positions plus one prefilled last prompt token; a greedy probe
+of up to k=16 tokens against a 64-entry refusal table; the gate; and N=64
+min-p branches (T=2.0, min_p=0.05) of 128 tokens each on paged tails.
+
+One step = prefill of the last prompt token + probe + gate + (on a miss) all
+sampling steps.  `value` counts decoded tokens (probe tokens + branch tokens)
+per second over the timed steps.  Kernel durations come from HIP events the
+library records on its own stream during the timed sampling calls.
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "gated decode tokens/sec (probe+N branches) + % HBM roofline, attn & sampler"
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic(w, R, P, tails):
+    """Algorithmic bytes / flops per launch of the three named kernels."""
+    d, V, Hq, Hkv, D = w.d_model, w.vocab, w.n_heads, w.n_kv_heads, w.head_dim
+    ntiles = (V + 63) // 64
+    lm_bytes = V * d * 2 + R * d * 2 + R * V * 4 + R * ntiles * 4
+    lm_flops = 2.0 * R * d * V
+    att_bytes = [2 * P * Hkv * D * 2 + R * 2 * t * Hkv * D * 2 + 2 * R * Hq * D * 2 for t in tails]
+    att_flops = [4.0 * R * Hq * D * (P + t) for t in tails]
+    samp_bytes = R * V * 4 + R * ntiles * 4
+    return lm_bytes, lm_flops, att_bytes, att_flops, samp_bytes
+
+
+def cpu_baseline(weights, w, P, last_tok, kp, vp, budget_s=15.0):
+    """The oracle on the host: prefill of the last prompt token, then one
+    branch's draws and decode steps until the time budget is spent."""
+    import numpy as np
+    from oracle import philox, sampler
+    from oracle.model import Decoder, KVCache
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count() or 1
+    dec = Decoder(weights)
+    cache = KVCache.from_arrays([kp[0]], [vp[0]])
+    t0 = time.perf_counter()
+    logits = dec.prefill([int(last_tok)], cache, start_pos=P)
+    tail = KVCache(w.n_layers)
+    n = 0
+    while True:
+        u = float(philox.uniform(12345, n))
+        d = sampler.sample_minp(logits, w.temperature, w.min_p, u)
+        n += 1
+        if time.perf_counter() - t0 > budget_s or n >= w.steps:
+            break
+        logits = dec.decode(d.token, cache, tail)
+    el = time.perf_counter() - t0
+    return {"value": n / el, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"prefill of the last prompt token over the 8192-position prefix, then {n} "
+                      f"min-p draws and {n - 1} decode steps of one branch (float64 numpy), "
+                      f"{el:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=8)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--table", choices=("typical", "adversarial"), default="typical")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU (got --gpus {args.gpus}); the path is built and "
+              "measured on one MI355X only", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synth
+    import paper_2607_20791_amd as rgd
+    from paper_2607_20791_amd import session
+
+    assert torch.cuda.is_available(), "no GPU visible"
+    w = synth.C2
+    P = w.synthetic_prefix
+    Pp = w.prefix_positions
+    k, c, N, S = w.probe_k, 3, w.n_branches, w.steps
+    t_setup = time.perf_counter()
+    log("generating weights ...")
+    weights = synth.model_weights(w)
+    kp, vp = synth.synthetic_prefix_kv(w, 0)
+    last_tok = synth.prompt_tokens(w)[0, 0]
+    log(f"weights ready in {time.perf_counter() - t_setup:.1f} s; uploading")
+    model = session.build_model(weights, max_rows=N, max_pos=Pp + S + k)
+    kv = session.alloc_kv(model, w, max_prompts=1, max_prefix=Pp,
+                          n_pages=N * ((S - 1 + 15) // 16) + 4)
+    session.fill_prefix(kv, 0, kp, vp)
+    dev = "cuda"
+    tok = torch.tensor([[int(last_tok)]], dtype=torch.int32, device=dev)
+    last = torch.empty(1, w.vocab, dtype=torch.float32, device=dev)
+    ptok = torch.empty(1, k, dtype=torch.int32, device=dev)
+    plen = torch.empty(1, dtype=torch.int32, device=dev)
+    ev = torch.empty(1, dtype=torch.int32, device=dev)
+    out = torch.empty(1, N, S, dtype=torch.int32, device=dev)
+    seeds = torch.arange(N, dtype=torch.int64, device=dev)
+
+    def prefill():
+        kv.set_prefix_len(0, P)
+        rgd.prefill_kv(model, kv, tok, P, last)
+
+    if args.table == "typical":
+        off, toks = synth.random_table(w)
+    else:
+        # entry equal to the first 15 greedy tokens, differing at token 16: a
+        # full-length miss (greedy tokens from a T=0 run of the same path)
+        prefill()
+        g = torch.empty(1, 1, k, dtype=torch.int32, device=dev)
+        rgd.sample_continuations(model, kv, last, [0], 1, k, 0.0, 0.0, seeds[:1], g)
+        gl = g[0, 0].cpu().numpy()
+        ent = list(gl[:15]) + [int((gl[15] + 1) % w.vocab)]
+        off0, toks0 = synth.random_table(w)
+        off = np.concatenate([[0, 16], off0[1:] + 16]).astype(np.int32)
+        toks = np.concatenate([ent, toks0]).astype(np.int32)
+    table = rgd.Table(off, toks)
+
+    def step(timed=False):
+        prefill()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        rgd.probe(model, kv, last, table, 1, k, c, -1, ptok, plen, ev)
+        dec, miss = rgd.gate(kv, ev, 1)
+        t1 = time.perf_counter()
+        if len(miss):
+            if timed:
+                rgd.timing_enable(model, True)
+            rgd.sample_continuations(model, kv, last, list(miss), N, S, w.temperature, w.min_p,
+                                     seeds, out)
+            if timed:
+                rgd.timing_enable(model, False)
+        torch.cuda.synchronize()
+        t2 = time.perf_counter()
+        n_probe = int(plen.item())
+        return n_probe, len(miss), t1 - t0, t2 - t1
+
+    log("warmup ...")
+    for _ in range(args.warmup):
+        step()
+    rgd.timing_read(model)
+    torch.cuda.synchronize()
+    log("timed steps ...")
+    t_start = time.perf_counter()
+    recs = [step(timed=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    rgd.check_status(model)
+    tim = rgd.timing_read(model)
+    tokens = sum(r[0] + r[1] * N * S for r in recs)
+    returned = sum((r[1] * N * S) if r[1] else r[0] for r in recs)
+    probe_s = sum(r[2] for r in recs)
+    sample_s = sum(r[3] for r in recs)
+
+    lm_b, lm_f, att_b, att_f, samp_b = algorithmic(w, N, Pp, range(1, S))
+    n_miss_steps = sum(1 for r in recs if r[1])
+    res = {}
+    if n_miss_steps:
+        lm_ms, lm_n = tim["lm_head"]
+        at_ms, at_n = tim["attention"]
+        ap_ms, ap_n = tim["attn_prefix"]
+        sp_ms, sp_n = tim["sampler"]
+        st_ms, st_n = tim["step"]
+        lm_avg = lm_ms / lm_n
+        lm_gbs = lm_b / (lm_avg * 1e-3) / 1e9
+        att_total_b = sum(att_b) * n_miss_steps
+        att_gbs = att_total_b / (at_ms * 1e-3) / 1e9
+        attp_total_b = (2 * Pp * w.n_kv_heads * w.head_dim * 2) * ap_n
+        attp_gbs = attp_total_b / (ap_ms * 1e-3) / 1e9
+        att_tflops = sum(att_f) * n_miss_steps / (at_ms * 1e-3) / 1e12
+        samp_gbs = samp_b * sp_n / (sp_ms * 1e-3) / 1e9
+        res = {
+            "roofline": {"bound": "hbm", "kernel": "lm_head_gemm_bf16", "achieved": round(lm_gbs, 1),
+                         "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(lm_gbs / HBM_PEAK_GBS, 4),
+                         "traffic": None, "avg_us": round(lm_avg * 1e3, 2),
+                         "bytes_per_launch": lm_b,
+                         "mfma_util": round(lm_f / (lm_avg * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4)},
+            "kernels": {
+                "attention": {"bound": "hbm", "achieved": round(att_gbs, 1), "peak": HBM_PEAK_GBS,
+                              "unit": "GB/s", "frac": round(att_gbs / HBM_PEAK_GBS, 4),
+                              "avg_us": round(at_ms / at_n * 1e3, 2), "launches": at_n,
+                              "tflops": round(att_tflops, 1),
+                              "mfma_frac": round(att_tflops / BF16_PEAK_TFLOPS, 4)},
+                "attention_prefix_kernel": {"achieved": round(attp_gbs, 1), "unit": "GB/s",
+                                            "frac": round(attp_gbs / HBM_PEAK_GBS, 4),
+                                            "avg_us": round(ap_ms / ap_n * 1e3, 2)},
+                "sampler": {"bound": "hbm", "achieved": round(samp_gbs, 1), "peak": HBM_PEAK_GBS,
+                            "unit": "GB/s", "frac": round(samp_gbs / HBM_PEAK_GBS, 4),
+                            "avg_us": round(sp_ms / sp_n * 1e3, 2), "bytes_per_launch": samp_b},
+                "decode_step": {"avg_us": round(st_ms / st_n * 1e3, 2), "launches": st_n},
+            },
+        }
+    line = {
+        "metric": METRIC, "value": round(tokens / elapsed, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "prefix_positions": Pp, "branches": N, "steps": S,
+                   "probe_k": k, "check_cadence": c, "temperature": w.temperature,
+                   "min_p": w.min_p, "table": args.table, "page_size": 16},
+        "tokens_decoded": tokens, "tokens_returned": returned,
+        "gate_overhead": round(probe_s / sample_s, 5) if sample_s > 0 else None,
+        "probe_gate_ms_per_step": round(probe_s / args.steps * 1e3, 3),
+        "sampling_ms_per_step": round(sample_s / args.steps * 1e3, 3),
+    }
+    line.update(res)
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle ...")
+        line["cpu_baseline"] = cpu_baseline(weights, w, P, last_tok, kp, vp)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

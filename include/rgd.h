@@ -197,6 +197,32 @@ int32_t rgd_sample_continuations(rgd_model* m, rgd_kv* kv, const float* last_log
  * maximum) and clears it.  Synchronous. */
 int32_t rgd_check_status(rgd_model* m, rgd_stream stream);
 
+/* ---- in-situ kernel timing (measurement hooks for the benchmark) ---- */
+
+/* Timed units: the LM-head GEMM; the whole attention stage (shared-prefix
+ * kernel, tail kernel and combine); the shared-prefix attention kernel alone;
+ * the min-p sampler kernel of a decode step; one whole decode step (all layers,
+ * LM head and token selection). */
+enum rgd_timer {
+  RGD_TIMER_LM_HEAD = 0,
+  RGD_TIMER_ATTENTION = 1,
+  RGD_TIMER_ATTN_PREFIX = 2,
+  RGD_TIMER_SAMPLER = 3,
+  RGD_TIMER_STEP = 4,
+  RGD_TIMER_COUNT = 5
+};
+
+/* enable != 0: from now on the model records HIP events on the work stream
+ * around each timed unit (at most 65536 launches per unit between reads; later
+ * launches are not timed).  enable == 0 stops recording.  Events are created
+ * here, not on the decode path. */
+int32_t rgd_timing_enable(rgd_model* m, int32_t enable);
+
+/* Waits for the recorded events and returns, per timed unit, the summed
+ * duration in milliseconds (ms[RGD_TIMER_COUNT]) and the number of launches
+ * (launches[RGD_TIMER_COUNT]); then clears the records.  Synchronous. */
+int32_t rgd_timing_read(rgd_model* m, double* ms, int64_t* launches);
+
 /* ---- kernel-level entry points (used by the tests and the benchmark) ---- */
 
 /* Decode attention for R rows of one layer: q dev [R][Hq][D] (model dtype)

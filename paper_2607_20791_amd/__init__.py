@@ -13,7 +13,7 @@ import os
 __all__ = [
     "RGDError", "lib", "ModelConfig", "Model", "KV", "Table", "prefill_kv", "probe", "gate",
     "sample_continuations", "check_status", "kernel_attention", "kernel_lm_head", "kernel_argmax",
-    "kernel_sample", "sampler_workspace_bytes", "EVENT_INCOMPAT", "EVENT_STOP", "EVENT_MAXLEN",
+    "kernel_sample", "sampler_workspace_bytes", "timing_enable", "timing_read", "TIMERS", "EVENT_INCOMPAT", "EVENT_STOP", "EVENT_MAXLEN",
     "DTYPE_F32", "DTYPE_BF16",
 ]
 
@@ -23,7 +23,7 @@ EXPORTS = (
     "rgd_kv_destroy", "rgd_kv_set_prefix_len", "rgd_table_create", "rgd_table_destroy",
     "rgd_prefill_kv", "rgd_probe", "rgd_gate", "rgd_sample_continuations", "rgd_check_status",
     "rgd_kernel_attention", "rgd_kernel_lm_head", "rgd_sampler_workspace_bytes",
-    "rgd_kernel_argmax", "rgd_kernel_sample",
+    "rgd_kernel_argmax", "rgd_kernel_sample", "rgd_timing_enable", "rgd_timing_read",
 )
 
 DTYPE_F32, DTYPE_BF16 = 0, 1
@@ -82,6 +82,10 @@ _sig("rgd_kernel_lm_head", I32, VP, VP, I32, VP, VP)
 _sig("rgd_sampler_workspace_bytes", U64, I32, I32)
 _sig("rgd_kernel_argmax", I32, VP, I32, I32, VP, VP, VP)
 _sig("rgd_kernel_sample", I32, VP, I32, I32, F32, F32, VP, U32, U32, I32, VP, VP, VP)
+_sig("rgd_timing_enable", I32, VP, I32)
+_sig("rgd_timing_read", I32, VP, C.POINTER(C.c_double), C.POINTER(C.c_int64))
+
+TIMERS = ("lm_head", "attention", "attn_prefix", "sampler", "step")
 
 
 class RGDError(RuntimeError):
@@ -241,6 +245,18 @@ def kernel_attention(model, q, row_prompt, plen, prefix_k, prefix_v, max_prompts
 
 def kernel_lm_head(model, h, logits):
     _check(lib.rgd_kernel_lm_head(model.h, _ptr(h), h.shape[0], _ptr(logits), _stream()))
+
+
+def timing_enable(model, on=True):
+    _check(lib.rgd_timing_enable(model.h, 1 if on else 0))
+
+
+def timing_read(model):
+    """{unit: (total ms, launches)} since the last read."""
+    ms = (C.c_double * len(TIMERS))()
+    n = (C.c_int64 * len(TIMERS))()
+    _check(lib.rgd_timing_read(model.h, ms, n))
+    return {k: (ms[i], n[i]) for i, k in enumerate(TIMERS)}
 
 
 def sampler_workspace_bytes(R, V):

@@ -107,7 +107,13 @@ struct rgd_model {
   int* h_stage = nullptr;  // pinned staging for uploads
   size_t stage_ints = 0;
   hipEvent_t stage_done = nullptr;
+  // in-situ timing: event pairs per timed unit
+  bool timing = false;
+  std::vector<hipEvent_t> tev[RGD_TIMER_COUNT];
+  int tused[RGD_TIMER_COUNT] = {0};
   ~rgd_model() {
+    for (auto& v : tev)
+      for (hipEvent_t e : v) (void)hipEventDestroy(e);
     for (void* p : allocs) (void)hipFree(p);
     if (h_stage) (void)hipHostFree(h_stage);
     if (stage_done) (void)hipEventDestroy(stage_done);
@@ -153,6 +159,26 @@ struct rgd_kv {
 };
 
 namespace {
+
+// ------------------------------------------------------------ timing hooks --
+constexpr int kTimerPairs = 65536;
+
+struct TimeScope {
+  rgd_model* m;
+  int unit;
+  hipStream_t s;
+  bool on;
+  TimeScope(rgd_model* m_, int unit_, hipStream_t s_) : m(m_), unit(unit_), s(s_) {
+    on = m->timing && m->tused[unit] < (int)m->tev[unit].size() / 2;
+    if (on) (void)hipEventRecord(m->tev[unit][2 * m->tused[unit]], s);
+  }
+  ~TimeScope() {
+    if (on) {
+      (void)hipEventRecord(m->tev[unit][2 * m->tused[unit] + 1], s);
+      ++m->tused[unit];
+    }
+  }
+};
 
 // ----------------------------------------------------------- upload helper --
 // Copies host ints to device through the model's pinned staging buffer.  The
@@ -269,8 +295,12 @@ int run_attention(rgd_model* m, const KVLayout& kvl, const Rows& rows, const Hos
   a.nparts = a.splits + a.tail_chunks;
   if (a.nparts > cap || a.splits < 1)
     return fail(RGD_E_UNSUPPORTED, "attention needs %d partials for %d rows (capacity %d)", a.nparts, R, cap);
+  TimeScope ts(m, RGD_TIMER_ATTENTION, s);
   if (m->bf16) {
-    HIP_OK(attn_prefix_mfma_bf16(a, s));
+    {
+      TimeScope tp(m, RGD_TIMER_ATTN_PREFIX, s);
+      HIP_OK(attn_prefix_mfma_bf16(a, s));
+    }
     HIP_OK(attn_tail_vec<bf16_t>(a, s));
     HIP_OK(attn_combine<bf16_t>(a, (bf16_t*)out, s));
   } else {
@@ -303,6 +333,7 @@ int lm_head(rgd_model* m, const void* x, int ldx, int R, float* logits, hipStrea
   g.tilemax = m->tilemax;
   g.ntiles = m->ntiles;
   g.mode = GEMM_LOGITS;
+  TimeScope ts(m, RGD_TIMER_LM_HEAD, s);
   return gemm(m, g, s);
 }
 
@@ -476,6 +507,7 @@ int select_tokens(rgd_model* m, const float* z, long long ldz, int R, const floa
     return RGD_OK;
   }
   SampleArgs a = sample_args(m, z, ldz, R, V, T, p_min, pmax, npmax, seeds, ctr, out, out_stride, out_col, cur);
+  TimeScope ts(m, RGD_TIMER_SAMPLER, s);
   HIP_OK(minp_sample(a, s));
   return RGD_OK;
 }
@@ -979,6 +1011,7 @@ int32_t rgd_sample_continuations(rgd_model* m, rgd_kv* kv, const float* last_log
   if (T > 0.f) HIP_OK(chunk_max(z0, V, R, V, kSampleChunk, m->tilemax, s));
   RGD_TRY(select_tokens(m, z0, V, R, m->tilemax, m->nchunks, T, min_p, sd, 0u, out, steps, 0, m->cur_tok, s));
   for (int st = 1; st < steps; ++st) {
+    TimeScope tstep(m, RGD_TIMER_STEP, s);
     Rows rows = device_rows(m, kv, R, st - 1, false);
     const int* feed = forced ? forced + (st - 1) : m->cur_tok;
     const int fstride = forced ? steps : 1;
@@ -1003,6 +1036,37 @@ int32_t rgd_check_status(rgd_model* m, rgd_stream stream) {
     HIP_OK(hipMemsetAsync(m->status, 0, 4, s));
     HIP_OK(hipStreamSynchronize(s));
     return fail(RGD_E_NONFINITE, "a logit row had a non-finite maximum");
+  }
+  return RGD_OK;
+}
+
+int32_t rgd_timing_enable(rgd_model* m, int32_t enable) {
+  g_err.clear();
+  if (!m) return fail(RGD_E_INVALID_ARG, "null model");
+  if (enable && m->tev[0].empty()) {
+    for (int u = 0; u < RGD_TIMER_COUNT; ++u) {
+      m->tev[u].resize(2 * kTimerPairs);
+      for (auto& e : m->tev[u]) HIP_OK(hipEventCreate(&e));
+    }
+  }
+  m->timing = enable != 0;
+  return RGD_OK;
+}
+
+int32_t rgd_timing_read(rgd_model* m, double* ms, int64_t* launches) {
+  g_err.clear();
+  if (!m || !ms || !launches) return fail(RGD_E_INVALID_ARG, "null argument");
+  for (int u = 0; u < RGD_TIMER_COUNT; ++u) {
+    double tot = 0.0;
+    for (int i = 0; i < m->tused[u]; ++i) {
+      HIP_OK(hipEventSynchronize(m->tev[u][2 * i + 1]));
+      float t = 0.f;
+      HIP_OK(hipEventElapsedTime(&t, m->tev[u][2 * i], m->tev[u][2 * i + 1]));
+      tot += t;
+    }
+    ms[u] = tot;
+    launches[u] = m->tused[u];
+    m->tused[u] = 0;
   }
   return RGD_OK;
 }
