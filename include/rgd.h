@@ -103,11 +103,14 @@ const char* rgd_version(void);
 /* Message for the last failing call on this thread ("" if none). */
 const char* rgd_last_error(void);
 
-/* Creates a model over caller-owned weights (not copied; they must outlive the
- * handle).  max_rows bounds the rows of any decode step (probe prompts, or
- * prompts x branches) and the tokens processed per prefill chunk; the
- * workspace for that many rows is allocated here.  bf16 models require
- * head_dim == 128 and d_model, Hq*D, ffn multiples of 128. */
+/* Creates a model.  bf16 weight matrices are repacked here, once, into
+ * library-owned buffers in the layout the GEMM kernels stream (16-row panels
+ * of 64-wide k blocks); the caller's matrices are not read afterwards.  The
+ * embedding table, the norm gains and fp32 matrices are used in place and
+ * must outlive the handle.  max_rows bounds the rows of any decode step
+ * (probe prompts, or prompts x branches) and the tokens processed per prefill
+ * chunk; the workspace for that many rows is allocated here.  bf16 models
+ * require head_dim == 128 and d_model, Hq*D, ffn multiples of 128. */
 int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int32_t max_rows,
                          rgd_model** out);
 void rgd_model_destroy(rgd_model* m);

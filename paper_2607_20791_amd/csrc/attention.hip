@@ -30,22 +30,40 @@ RGD_DEV uint32_t pack2(float lo, float hi) {
   return uint32_t(f32_to_bf16(lo)) | (uint32_t(f32_to_bf16(hi)) << 16);
 }
 
-__global__ __launch_bounds__(256) void attn_prefix_mfma_kernel(AttnArgs a) {
-  constexpr int D = 128;
+// NWAVE waves; PAGED selects the row's paged tail (one row per workgroup)
+// instead of the shared prompt prefix (a block of rows of one prompt).
+template <int NWAVE, bool PAGED>
+__global__ __launch_bounds__(NWAVE * 64) void attn_mfma_kernel(AttnArgs a) {
+  constexpr int D = 128, NT = NWAVE * 64, SEGS = 512 / NT;
   const int s = blockIdx.x, g = blockIdx.y;
-  const int4 rb = a.rblocks[blockIdx.z];
-  const int r0 = rb.x, nr = rb.y, b = rb.z, maxplen = rb.w;
+  int r0, nr, b, maxlen, lo, hi, part;
+  if (PAGED) {
+    r0 = blockIdx.z;
+    nr = 1;
+    b = 0;
+    maxlen = a.tail_len;
+    lo = s * a.tail_chunk;
+    hi = min(lo + a.tail_chunk, maxlen);
+    part = a.splits + s;
+  } else {
+    const int4 rb = a.rblocks[blockIdx.z];
+    r0 = rb.x;
+    nr = rb.y;
+    b = rb.z;
+    maxlen = rb.w;
+    lo = s * a.split_len;
+    hi = min(lo + a.split_len, maxlen);
+    part = s;
+  }
   const int G = a.Hq / a.Hkv;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int lo = s * a.split_len;
-  const int hi = min(lo + a.split_len, maxplen);
   const int nq = nr * G;
   const int v = wave * 16 + (lane & 15);
   const bool vok = v < nq;
   const bool wave_active = wave * 16 < nq;
   const int row = r0 + (vok ? v / G : 0);
   const int head = g * G + (vok ? v % G : 0);
-  const int my_end = vok ? min(a.rows.plen[row], hi) : lo;
+  const int my_end = PAGED ? hi : (vok ? min(a.rows.plen[row], hi) : lo);
 
   u32x4 qf[4];
   {
@@ -59,8 +77,23 @@ __global__ __launch_bounds__(256) void attn_prefix_mfma_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t vt_lds[128][40];
 
   const long long pstride = (long long)a.Hkv * D;
-  const bf16_t* kbase = (const bf16_t*)a.kv.prefix_k + (long long)b * a.kv.P * pstride + g * D;
-  const bf16_t* vbase = (const bf16_t*)a.kv.prefix_v + (long long)b * a.kv.P * pstride + g * D;
+  const bf16_t* kbase;
+  const bf16_t* vbase;
+  if (PAGED) {
+    kbase = (const bf16_t*)a.kv.pool_k + g * D;
+    vbase = (const bf16_t*)a.kv.pool_v + g * D;
+  } else {
+    kbase = (const bf16_t*)a.kv.prefix_k + (long long)b * a.kv.P * pstride + g * D;
+    vbase = (const bf16_t*)a.kv.prefix_v + (long long)b * a.kv.P * pstride + g * D;
+  }
+  const int* pages = PAGED ? a.rows.pages + (long long)r0 * a.rows.max_pages : nullptr;
+  auto row_off = [&](int pos) -> long long {
+    if (PAGED) {
+      const int ps = a.kv.page_size;
+      return ((long long)pages[pos / ps] * ps + pos % ps) * pstride;
+    }
+    return (long long)pos * pstride;
+  };
   const float scale = rsqrtf(float(D)) * kLog2e;
 
   float m = -INFINITY, lsum = 0.f;
@@ -68,23 +101,37 @@ __global__ __launch_bounds__(256) void attn_prefix_mfma_kernel(AttnArgs a) {
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int t0 = lo; t0 < hi; t0 += 32) {
+  u32x4 kreg[SEGS], vreg[SEGS];
+  auto load_tile = [&](int t0) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int seg = threadIdx.x + i * 256;
-      const int pr = seg >> 4, pc = (seg & 15) * 8, pos = t0 + pr;
-      u32x4 kk = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
+    for (int i = 0; i < SEGS; ++i) {
+      const int seg = threadIdx.x + i * NT;
+      const int pos = t0 + (seg >> 4), pc = (seg & 15) * 8;
+      kreg[i] = u32x4{0u, 0u, 0u, 0u};
+      vreg[i] = u32x4{0u, 0u, 0u, 0u};
       if (pos < hi) {
-        kk = *(const u32x4*)(kbase + pos * pstride + pc);
-        vv = *(const u32x4*)(vbase + pos * pstride + pc);
-      }
-      *(u32x4*)&ks_lds[pr][pc] = kk;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        vt_lds[pc + 2 * e][pr] = bf16_t(vv[e] & 0xFFFFu);
-        vt_lds[pc + 2 * e + 1][pr] = bf16_t(vv[e] >> 16);
+        const long long off = row_off(pos) + pc;
+        kreg[i] = *(const u32x4*)(kbase + off);
+        vreg[i] = *(const u32x4*)(vbase + off);
       }
     }
+  };
+
+  if (lo < hi) load_tile(lo);
+  for (int t0 = lo; t0 < hi; t0 += 32) {
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < SEGS; ++i) {
+      const int seg = threadIdx.x + i * NT;
+      const int pr = seg >> 4, pc = (seg & 15) * 8;
+      *(u32x4*)&ks_lds[pr][pc] = kreg[i];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        vt_lds[pc + 2 * e][pr] = bf16_t(vreg[i][e] & 0xFFFFu);
+        vt_lds[pc + 2 * e + 1][pr] = bf16_t(vreg[i][e] >> 16);
+      }
+    }
+    if (t0 + 32 < hi) load_tile(t0 + 32);
     __syncthreads();
     if (wave_active) {
       f32x4 sc[2];
@@ -137,13 +184,12 @@ __global__ __launch_bounds__(256) void attn_prefix_mfma_kernel(AttnArgs a) {
         o[dt] = mfma16x16x32(u32x4{a0.x, a0.y, a1.x, a1.y}, pb, o[dt]);
       }
     }
-    __syncthreads();
   }
 
   float lt = lsum + __shfl_xor(lsum, 16, 64);
   lt += __shfl_xor(lt, 32, 64);
   if (vok) {
-    const long long idx = ((long long)s * a.rows.R + row) * a.Hq + head;
+    const long long idx = ((long long)part * a.rows.R + row) * a.Hq + head;
     float* po = a.part_o + idx * D;
     const float inv = lt > 0.f ? 1.0f / lt : 0.f;
 #pragma unroll
@@ -248,7 +294,14 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a, T* out) {
 hipError_t attn_prefix_mfma_bf16(const AttnArgs& a, hipStream_t s) {
   if (a.D != 128 || a.Hq / a.Hkv > 64 || a.split_len % 32) return hipErrorInvalidValue;
   if (a.splits <= 0 || a.nrblocks <= 0) return hipSuccess;
-  hipLaunchKernelGGL(attn_prefix_mfma_kernel, dim3(a.splits, a.Hkv, a.nrblocks), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((attn_mfma_kernel<4, false>), dim3(a.splits, a.Hkv, a.nrblocks), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t attn_tail_mfma_bf16(const AttnArgs& a, hipStream_t s) {
+  if (a.D != 128 || a.Hq / a.Hkv > 16 || a.tail_chunk % 32) return hipErrorInvalidValue;
+  if (a.tail_chunks <= 0) return hipSuccess;
+  hipLaunchKernelGGL((attn_mfma_kernel<1, true>), dim3(a.tail_chunks, a.Hkv, a.rows.R), dim3(64), 0, s, a);
   return hipGetLastError();
 }
 

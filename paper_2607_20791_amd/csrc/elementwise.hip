@@ -1,6 +1,6 @@
-// Per-row kernels of the decode step: embedding gather, split-K reduction with
-// residual add and RMSNorm, and the Q/K/V epilogue (split-K reduction, rotary
-// embedding, store of q and append of k/v to the shared prefix or the row's
+// Per-row kernels of the decode step: embedding gather fused with the first
+// RMSNorm, RMSNorm of the residual stream, and the Q/K/V epilogue (rotary
+// embedding, store of q, append of k/v to the shared prefix or to the row's
 // paged tail).
 #include "kernels.hpp"
 
@@ -8,45 +8,83 @@ namespace rgd {
 
 namespace {
 
+constexpr int kNormThreads = 1024;
+
+// Row RMSNorm over v[0..d) held as float4 chunks (thread i owns chunks
+// i, i + blockDim, ...); writes xn = v / sqrt(mean(v^2) + eps) * g.
 template <typename T>
-__global__ __launch_bounds__(256) void embed_kernel(const int* tok, int tok_stride, const T* E, int d,
-                                                    int V, float* x) {
+RGD_DEV void norm_store(const float* v, int d, const float* g, float eps, T* xn) {
+  __shared__ float red[16];
+  float ss = 0.f;
+  for (int i = threadIdx.x * 4; i < d; i += blockDim.x * 4) {
+    const float4 a = *(const float4*)(v + i);
+    ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
+  }
+  ss = block_sum(ss, red);
+  const float inv = rsqrtf(ss / float(d) + eps);
+  for (int i = threadIdx.x * 4; i < d; i += blockDim.x * 4) {
+    const float4 a = *(const float4*)(v + i);
+    const float4 gg = *(const float4*)(g + i);
+    store_f(xn + i, a.x * inv * gg.x);
+    store_f(xn + i + 1, a.y * inv * gg.y);
+    store_f(xn + i + 2, a.z * inv * gg.z);
+    store_f(xn + i + 3, a.w * inv * gg.w);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kNormThreads) void embed_rmsnorm_kernel(const int* tok, int tok_stride, const T* E,
+                                                                   int d, int V, float* x, const float* g,
+                                                                   float eps, T* xn) {
   const int r = blockIdx.x;
   // ids come from the sampler or the caller; clamp so that a bad id cannot read
   // outside the embedding table
   const long long t = min(max(tok[(long long)r * tok_stride], 0), V - 1);
-  for (int i = threadIdx.x; i < d; i += 256) x[(long long)r * d + i] = load_f(E + t * d + i);
+  float* xr = x + (long long)r * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) xr[i] = load_f(E + t * d + i);
+  __syncthreads();
+  norm_store(xr, d, g, eps, xn + (long long)r * d);
 }
 
 template <typename T>
-__global__ __launch_bounds__(256) void residual_rmsnorm_kernel(float* x, const float* parts, int nparts,
-                                                               long long part_stride, const float* g,
-                                                               float eps, int d, T* xn) {
-  __shared__ float red[4];
+__global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(float* x, const float* parts, int nparts,
+                                                                      long long part_stride, const float* g,
+                                                                      float eps, int d, T* xn) {
   const int r = blockIdx.x;
   float* xr = x + (long long)r * d;
-  float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += 256) {
-    float v = xr[i];
-    for (int p = 0; p < nparts; ++p) v += parts[p * part_stride + (long long)r * d + i];
-    xr[i] = v;
-    ss += v * v;
+  if (nparts > 0) {
+    const float* pr = parts + (long long)r * d;
+    for (int i = threadIdx.x * 4; i < d; i += blockDim.x * 4) {
+      float4 v = *(float4*)(xr + i);
+      float4 q[8];
+#pragma unroll
+      for (int p = 0; p < 8; ++p)
+        if (p < nparts) q[p] = *(const float4*)(pr + p * part_stride + i);
+#pragma unroll
+      for (int p = 0; p < 8; ++p)
+        if (p < nparts) {
+          v.x += q[p].x;
+          v.y += q[p].y;
+          v.z += q[p].z;
+          v.w += q[p].w;
+        }
+      *(float4*)(xr + i) = v;
+    }
+    __syncthreads();
   }
-  ss = block_sum(ss, red);
-  const float inv = rsqrtf(ss / float(d) + eps);
-  for (int i = threadIdx.x; i < d; i += 256) store_f(xn + (long long)r * d + i, xr[i] * inv * g[i]);
+  norm_store(xr, d, g, eps, xn + (long long)r * d);
 }
 
 template <typename T>
 __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* parts, int nparts, long long part_stride,
-                                                       Rows rows, int Hq, int Hkv, int D, float theta,
-                                                       T* q, KVLayout kv) {
+                                                       Rows rows, int Hq, int Hkv, int D, float theta, T* q,
+                                                       KVLayout kv) {
   __shared__ float cs[128], sn[128];
   const int r = blockIdx.x;
   const int half = D / 2;
   const int pos = rows.prefill ? rows.base_pos[r] : rows.base_pos[r] + rows.t;
   for (int j = threadIdx.x; j < half; j += 256) {
-    // angle in fp64: pos * theta^(-2j/D), reduced mod 2*pi before the fp32 sin/cos
+    // angle in fp64: pos * theta^(-2j/D), reduced mod 2*pi before sin/cos
     const double ang = double(pos) * pow(double(theta), -2.0 * double(j) / double(D));
     const double red = ang - 6.283185307179586 * floor(ang / 6.283185307179586);
     double s, c;
@@ -58,11 +96,12 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* parts, int n
   const int nqkv = (Hq + 2 * Hkv) * D;
   const float* pr = parts + (long long)r * nqkv;
   auto col = [&](int c) {
-    float v = 0.f;
-    for (int p = 0; p < nparts; ++p) v += pr[p * part_stride + c];
+    float v = pr[c];
+#pragma unroll
+    for (int p = 1; p < 8; ++p)
+      if (p < nparts) v += pr[p * part_stride + c];
     return v;
   };
-  // destination of this row's new K/V
   const int b = rows.prompt[r];
   long long kv_off;
   T* kd;
@@ -77,11 +116,11 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* parts, int n
     kd = (T*)kv.pool_k;
     vd = (T*)kv.pool_v;
   }
-  // rotated q and k: pairs (j, j + D/2) of each head
+  // rotated q and k: pairs (j, j + D/2) of each head (q heads, then k heads)
   const int npairs = (Hq + Hkv) * half;
   for (int i = threadIdx.x; i < npairs; i += 256) {
     const int h = i / half, j = i % half;
-    const int base = h * D;  // q heads then k heads are contiguous in the fused output
+    const int base = h * D;
     const float x1 = col(base + j), x2 = col(base + j + half);
     const float y1 = x1 * cs[j] - x2 * sn[j];
     const float y2 = x2 * cs[j] + x1 * sn[j];
@@ -102,37 +141,42 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* parts, int n
 }  // namespace
 
 template <typename T>
-hipError_t embed_rows(const int* tok, int tok_stride, int R, const T* E, int d, int V, float* x,
-                      hipStream_t s) {
-  hipLaunchKernelGGL(embed_kernel<T>, dim3(R), dim3(256), 0, s, tok, tok_stride, E, d, V, x);
+hipError_t embed_rmsnorm(const int* tok, int tok_stride, int R, const T* E, int d, int V, float* x,
+                         const float* g, float eps, T* xn, hipStream_t s) {
+  if (d % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(embed_rmsnorm_kernel<T>, dim3(R), dim3(kNormThreads), 0, s, tok, tok_stride, E, d, V, x,
+                     g, eps, xn);
   return hipGetLastError();
 }
 
 template <typename T>
-hipError_t residual_rmsnorm(float* x, const float* parts, int nparts, long long part_stride,
-                            const float* g, float eps, int R, int d, T* xn, hipStream_t s) {
-  hipLaunchKernelGGL(residual_rmsnorm_kernel<T>, dim3(R), dim3(256), 0, s, x, parts, nparts, part_stride,
+hipError_t residual_rmsnorm(float* x, const float* parts, int nparts, long long part_stride, const float* g,
+                            float eps, int R, int d, T* xn, hipStream_t s) {
+  if (d % 4 || nparts < 0 || nparts > 8) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(residual_rmsnorm_kernel<T>, dim3(R), dim3(kNormThreads), 0, s, x, parts, nparts, part_stride,
                      g, eps, d, xn);
   return hipGetLastError();
 }
 
 template <typename T>
-hipError_t qkv_rope_store(const float* parts, int nparts, long long part_stride, const Rows& rows,
-                          int Hq, int Hkv, int D, float theta, T* q, const KVLayout& kv, hipStream_t s) {
-  if (D > 256 || (D & 1)) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(qkv_rope_kernel<T>, dim3(rows.R), dim3(256), 0, s, parts, nparts, part_stride, rows,
-                     Hq, Hkv, D, theta, q, kv);
+hipError_t qkv_rope_store(const float* parts, int nparts, long long part_stride, const Rows& rows, int Hq,
+                          int Hkv, int D, float theta, T* q, const KVLayout& kv, hipStream_t s) {
+  if (D > 256 || (D & 1) || nparts < 1 || nparts > 8) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(qkv_rope_kernel<T>, dim3(rows.R), dim3(256), 0, s, parts, nparts, part_stride, rows, Hq, Hkv,
+                     D, theta, q, kv);
   return hipGetLastError();
 }
 
-template hipError_t embed_rows<float>(const int*, int, int, const float*, int, int, float*, hipStream_t);
-template hipError_t embed_rows<bf16_t>(const int*, int, int, const bf16_t*, int, int, float*, hipStream_t);
-template hipError_t residual_rmsnorm<float>(float*, const float*, int, long long, const float*, float, int,
-                                            int, float*, hipStream_t);
-template hipError_t residual_rmsnorm<bf16_t>(float*, const float*, int, long long, const float*, float,
-                                             int, int, bf16_t*, hipStream_t);
-template hipError_t qkv_rope_store<float>(const float*, int, long long, const Rows&, int, int, int, float,
-                                          float*, const KVLayout&, hipStream_t);
+template hipError_t embed_rmsnorm<float>(const int*, int, int, const float*, int, int, float*, const float*,
+                                         float, float*, hipStream_t);
+template hipError_t embed_rmsnorm<bf16_t>(const int*, int, int, const bf16_t*, int, int, float*, const float*,
+                                          float, bf16_t*, hipStream_t);
+template hipError_t residual_rmsnorm<float>(float*, const float*, int, long long, const float*, float, int, int,
+                                            float*, hipStream_t);
+template hipError_t residual_rmsnorm<bf16_t>(float*, const float*, int, long long, const float*, float, int, int,
+                                             bf16_t*, hipStream_t);
+template hipError_t qkv_rope_store<float>(const float*, int, long long, const Rows&, int, int, int, float, float*,
+                                          const KVLayout&, hipStream_t);
 template hipError_t qkv_rope_store<bf16_t>(const float*, int, long long, const Rows&, int, int, int, float,
                                            bf16_t*, const KVLayout&, hipStream_t);
 

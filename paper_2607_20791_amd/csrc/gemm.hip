@@ -1,14 +1,22 @@
-// Skinny-M GEMMs for the decode step: Y = X W^T.
+// Skinny-M GEMMs of the decode step: Y = X W^T with X [M][K] (bf16) and W
+// [N][K].
 //
-// bf16 path: one workgroup (4 waves) owns 64 output columns and MT*16 rows.
-// Each wave streams its 16 weight rows straight from HBM into registers (a
-// lane reads 64 contiguous bytes of one row per 128-wide k block, prefetched
-// one block ahead) while the X rows of the block are staged once per k block
-// in LDS and shared by the four waves.  The product runs on
-// v_mfma_f32_16x16x32_bf16 with fp32 accumulation.  Because the contraction
-// index only has to be permuted the same way for both operands, each lane's
-// 32-element k slice is taken contiguously, which keeps every global load
-// 64 B wide.
+// At decode sizes every GEMM is bound by streaming W from HBM.  Weights are
+// repacked once, at model creation, into 16-row panels: panel p holds rows
+// [16p, 16p+16) as consecutive 2 KiB blocks of 64 k values, each block laid
+// out in the order the MFMA B operand is loaded (lane l = 16q + r reads 32
+// contiguous bytes: row r, k values [16q, 16q+16) of the block).  A wave
+// reading its panels therefore streams long contiguous runs, which keeps the
+// DRAM pages open.
+//
+// A workgroup owns NW*NT panels (waves split N; for SwiGLU the first half of
+// the waves computes the gate panels and the second half the matching up
+// panels) and one K range (split-K across workgroups when N alone gives too
+// few workgroups).  The X rows of the current 64-wide k step are staged once
+// in a two-slot LDS ring shared by all waves; each wave keeps SW steps of its
+// weight panels in flight in registers.  Products run on
+// v_mfma_f32_16x16x32_bf16 with fp32 accumulation; X and W take the same
+// permutation of the contraction index.
 #include "kernels.hpp"
 
 namespace rgd {
@@ -22,146 +30,206 @@ RGD_DEV f32x4 mfma16x16x32(const u32x4& a, const u32x4& b, f32x4 c) {
 
 RGD_DEV float silu(float g) { return g / (1.0f + __expf(-g)); }
 
-template <int MT, int MODE>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int tile = blockIdx.x;
+constexpr int kStep = 64;  // k values per pipeline step
+
+// W [N][K] row-major -> panels [ceil(N/16)][K/64][64 lanes][16], rows past N
+// are zero.
+__global__ void pack_panels_kernel(const bf16_t* __restrict__ w, int N, int K, bf16_t* __restrict__ out) {
+  const long long nst = K / kStep;
+  const long long total = (long long)((N + 15) / 16) * nst * 64;  // 32-byte lane chunks
+  for (long long c = blockIdx.x * 256ll + threadIdx.x; c < total; c += 256ll * gridDim.x) {
+    const int lane = int(c & 63);
+    const long long blk = c >> 6;
+    const long long st = blk % nst, p = blk / nst;
+    const int r = lane & 15, q = lane >> 4;
+    const long long row = p * 16 + r;
+    u32x4 v0 = {0u, 0u, 0u, 0u}, v1 = {0u, 0u, 0u, 0u};
+    if (row < N) {
+      const u32x4* src = (const u32x4*)(w + row * K + st * kStep + q * 16);
+      v0 = src[0];
+      v1 = src[1];
+    }
+    u32x4* dst = (u32x4*)(out + c * 16);
+    dst[0] = v0;
+    dst[1] = v1;
+  }
+}
+
+template <int MT, int NT, int NW, int SW, int MODE>
+__global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
+  constexpr int NTH = NW * 64, XSEG = MT * 16 * 8, XPT = (XSEG + NTH - 1) / NTH;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, col16 = lane & 15;
   const int m0 = blockIdx.y * (MT * 16);
   const int split = blockIdx.z;
-  const int K = a.K;
-  const int nkb = K >> 7;
-  const int kb0 = int((long long)split * nkb / a.splits);
-  const int kb1 = int((long long)(split + 1) * nkb / a.splits);
+  const int K = a.K, nst = K / kStep;
+  const int st0 = int((long long)split * nst / a.splits), st1 = int((long long)(split + 1) * nst / a.splits);
 
-  // the weight row (output column) feeding this lane's B operand
-  int n;
-  const bf16_t* wrow;
-  if (MODE == GEMM_SILU) {
-    n = tile * 32 + (wave & 1) * 16 + (lane & 15);
-    const GemmSeg& sg = a.seg[wave >> 1];
-    wrow = (const bf16_t*)sg.w + (long long)min(n, a.N - 1) * K;
-  } else {
-    n = tile * 64 + wave * 16 + (lane & 15);
-    const int c0 = tile * 64;
+  // panels of this wave
+  constexpr int HALF = (MODE == GEMM_SILU) ? NW / 2 : NW;
+  const int wslot = (MODE == GEMM_SILU) ? (wave % HALF) : wave;
+  const int p0 = (blockIdx.x * HALF + wslot) * NT;  // first panel (in units of 16 columns)
+  const bf16_t* wp[NT];
+  int ncol[NT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    int p = p0 + j;
     int si = 0;
-    if (a.nseg > 1 && c0 >= a.seg[1].n0) si = 1;
-    if (a.nseg > 2 && c0 >= a.seg[2].n0) si = 2;
-    const GemmSeg& sg = a.seg[si];
-    wrow = (const bf16_t*)sg.w + (long long)(min(n, a.N - 1) - sg.n0) * K;
+    if (MODE == GEMM_SILU) {
+      si = wave / HALF;
+    } else {
+      if (a.nseg > 1 && p * 16 >= a.seg[1].n0) si = 1;
+      if (a.nseg > 2 && p * 16 >= a.seg[2].n0) si = 2;
+    }
+    const int lp = min(p - a.seg[si].n0 / 16, (a.seg[si].n + 15) / 16 - 1);  // panel within the segment
+    wp[j] = (const bf16_t*)a.seg[si].w + ((long long)lp * nst) * 1024 + lane * 16;
+    ncol[j] = p * 16 + col16;
   }
 
-  __shared__ __attribute__((aligned(16))) bf16_t xs[MT * 16][136];
-  f32x4 acc[MT];
+  __shared__ __attribute__((aligned(16))) bf16_t xs[2][MT * 16][72];
+  f32x4 acc[MT][NT];
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int j = 0; j < NT; ++j) acc[mt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  u32x4 wb[SW][NT][2], xr[XPT];
+  auto loadw = [&](int st, int slot) {
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+      const u32x4* p = (const u32x4*)(wp[j] + (long long)st * 1024);
+      wb[slot][j][0] = __builtin_nontemporal_load(p);
+      wb[slot][j][1] = __builtin_nontemporal_load(p + 1);
+    }
+  };
   const bf16_t* X = (const bf16_t*)a.x;
-  const int kq = (lane >> 4) * 32;
-  u32x4 wb[4], wn[4];
-  if (kb0 < kb1) {
-    const u32x4* p = (const u32x4*)(wrow + (kb0 << 7) + kq);
+  auto loadx = [&](int st) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) wb[j] = __builtin_nontemporal_load(p + j);
-  }
-  for (int kb = kb0; kb < kb1; ++kb) {
-    for (int i = threadIdx.x; i < MT * 16 * 16; i += 256) {
-      const int r = i >> 4, c = (i & 15) * 8, m = m0 + r;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (m < a.M) v = *(const u32x4*)(X + (long long)m * a.ldx + (kb << 7) + c);
-      *(u32x4*)&xs[r][c] = v;
+    for (int i = 0; i < XPT; ++i) {
+      const int seg = threadIdx.x + i * NTH;
+      const int r = seg >> 3, c = (seg & 7) * 8;
+      const int m = m0 + r;
+      xr[i] = (seg < XSEG && m < a.M) ? *(const u32x4*)(X + (long long)m * a.ldx + st * kStep + c)
+                                       : u32x4{0u, 0u, 0u, 0u};
     }
-    if (kb + 1 < kb1) {
-      const u32x4* p = (const u32x4*)(wrow + ((kb + 1) << 7) + kq);
+  };
+  auto storex = [&](int slot) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) wn[j] = __builtin_nontemporal_load(p + j);
+    for (int i = 0; i < XPT; ++i) {
+      const int seg = threadIdx.x + i * NTH;
+      if (seg < XSEG) *(u32x4*)&xs[slot][seg >> 3][(seg & 7) * 8] = xr[i];
     }
-    __syncthreads();
+  };
+
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < SW; ++j)
+    if (st0 + j < st1) loadw(st0 + j, j);
+  if (st0 < st1) loadx(st0);
+  const int kq = (lane >> 4) * 16;
+  for (int sb = st0; sb < st1; sb += SW) {
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const u32x4 av = *(const u32x4*)&xs[mt * 16 + (lane & 15)][kq + j * 8];
-        acc[mt] = mfma16x16x32(av, wb[j], acc[mt]);
+    for (int j = 0; j < SW; ++j) {
+      const int st = sb + j;
+      if (st < st1) {
+        const int xsl = (st - st0) & 1;
+        storex(xsl);
+        if (st + 1 < st1) loadx(st + 1);
+        __syncthreads();
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) {
+            const u32x4 av = *(const u32x4*)&xs[xsl][mt * 16 + col16][kq + h * 8];
+#pragma unroll
+            for (int jj = 0; jj < NT; ++jj) acc[mt][jj] = mfma16x16x32(av, wb[j][jj][h], acc[mt][jj]);
+          }
+        if (st + SW < st1) loadw(st + SW, j);
       }
     }
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < 4; ++j) wb[j] = wn[j];
   }
 
   // D layout of the 16x16 MFMA: lane holds rows 4*(lane/16)+i of column lane%16
   const int rq = (lane >> 4) * 4;
-  if (MODE == GEMM_PARTIAL) {
+  if (MODE == GEMM_STORE) {
     float* Y = (float*)a.y + (long long)split * a.split_stride;
-    if (n < a.N) {
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int j = 0; j < NT; ++j)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int m = m0 + mt * 16 + rq + i;
-          if (m < a.M) Y[(long long)m * a.ldy + n] = acc[mt][i];
+          if (m < a.M && ncol[j] < a.N) Y[(long long)m * a.ldy + ncol[j]] = acc[mt][j][i];
         }
+  } else if (MODE == GEMM_SILU) {
+    // up-projection waves hand their sums to the gate waves through LDS
+    __shared__ float up[HALF][MT * NT * 4][64];
+    __syncthreads();
+    if (wave >= HALF) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) up[wslot][(mt * NT + j) * 4 + i][lane] = acc[mt][j][i];
     }
-  } else if (MODE == GEMM_LOGITS) {
+    __syncthreads();
+    if (wave < HALF) {
+      bf16_t* Y = (bf16_t*)a.y;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int m = m0 + mt * 16 + rq + i;
+            const float u = up[wslot][(mt * NT + j) * 4 + i][lane];
+            if (m < a.M && ncol[j] < a.N)
+              Y[(long long)m * a.ldy + ncol[j]] = f32_to_bf16(silu(acc[mt][j][i]) * u);
+          }
+    }
+  } else {  // GEMM_LOGITS: logits plus one maximum per (row, workgroup)
     float* Y = (float*)a.y;
-    __shared__ float red[4][MT * 16];
+    __shared__ float red[NW][MT * 16];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int m = m0 + mt * 16 + rq + i;
-        const bool ok = (m < a.M) && (n < a.N);
-        if (ok) Y[(long long)m * a.ldy + n] = acc[mt][i];
-        float v = ok ? acc[mt][i] : -INFINITY;
+        float v = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+          const bool ok = m < a.M && ncol[j] < a.N;
+          if (ok) Y[(long long)m * a.ldy + ncol[j]] = acc[mt][j][i];
+          v = fmaxf(v, ok ? acc[mt][j][i] : -INFINITY);
+        }
         v = fmaxf(v, __shfl_xor(v, 1, 64));
         v = fmaxf(v, __shfl_xor(v, 2, 64));
         v = fmaxf(v, __shfl_xor(v, 4, 64));
         v = fmaxf(v, __shfl_xor(v, 8, 64));
-        if ((lane & 15) == 0) red[wave][mt * 16 + rq + i] = v;
+        if (col16 == 0) red[wave][mt * 16 + rq + i] = v;
       }
     __syncthreads();
-    if (threadIdx.x < MT * 16) {
-      const int m = m0 + threadIdx.x;
-      const float v = fmaxf(fmaxf(red[0][threadIdx.x], red[1][threadIdx.x]),
-                            fmaxf(red[2][threadIdx.x], red[3][threadIdx.x]));
-      if (m < a.M) a.tilemax[(long long)m * a.ntiles + tile] = v;
-    }
-  } else {  // GEMM_SILU: waves 2,3 hold the up projection of waves 0,1's features
-    __shared__ float up[MT * 16][33];
-    if (wave >= 2) {
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) up[mt * 16 + rq + i][(wave - 2) * 16 + (lane & 15)] = acc[mt][i];
-    }
-    __syncthreads();
-    if (wave < 2 && n < a.N) {
-      bf16_t* Y = (bf16_t*)a.y;
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int m = m0 + mt * 16 + rq + i;
-          const float u = up[mt * 16 + rq + i][wave * 16 + (lane & 15)];
-          if (m < a.M) Y[(long long)m * a.ldy + n] = f32_to_bf16(silu(acc[mt][i]) * u);
-        }
+    for (int t = threadIdx.x; t < MT * 16; t += NTH) {
+      float v = red[0][t];
+      for (int w = 1; w < NW; ++w) v = fmaxf(v, red[w][t]);
+      const int m = m0 + t;
+      if (m < a.M) a.tilemax[(long long)m * a.ntiles + blockIdx.x] = v;
     }
   }
 }
 
-template <int MODE>
-hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
-  const int ntile = MODE == GEMM_SILU ? (a.N + 31) / 32 : (a.N + 63) / 64;
-  const int splits = MODE == GEMM_PARTIAL ? a.splits : 1;
-  GemmArgs b = a;
-  b.splits = splits;
+template <int NT, int NW, int SW, int MODE>
+hipError_t launch_bf16(const GemmArgs& a, int ngroups, hipStream_t s) {
+  const int splits = a.splits;
   if (a.M <= 16) {
-    hipLaunchKernelGGL((gemm_bf16_kernel<1, MODE>), dim3(ntile, 1, splits), dim3(256), 0, s, b);
+    hipLaunchKernelGGL((gemm_bf16_kernel<1, NT, NW, SW, MODE>), dim3(ngroups, 1, splits), dim3(NW * 64), 0, s,
+                       a);
   } else if (a.M <= 32) {
-    hipLaunchKernelGGL((gemm_bf16_kernel<2, MODE>), dim3(ntile, 1, splits), dim3(256), 0, s, b);
+    hipLaunchKernelGGL((gemm_bf16_kernel<2, NT, NW, SW, MODE>), dim3(ngroups, 1, splits), dim3(NW * 64), 0, s,
+                       a);
   } else {
-    hipLaunchKernelGGL((gemm_bf16_kernel<4, MODE>), dim3(ntile, (a.M + 63) / 64, splits), dim3(256),
-                       0, s, b);
+    hipLaunchKernelGGL((gemm_bf16_kernel<4, NT, NW, SW, MODE>), dim3(ngroups, (a.M + 63) / 64, splits),
+                       dim3(NW * 64), 0, s, a);
   }
   return hipGetLastError();
 }
@@ -180,7 +248,10 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
   if (MODE == GEMM_SILU) {
     const float* wg = (const float*)a.seg[0].w + (long long)nc * K;
     const float* wu = (const float*)a.seg[1].w + (long long)nc * K;
-    for (int k = 0; k < K; ++k) { acc += x[k] * wg[k]; acc2 += x[k] * wu[k]; }
+    for (int k = 0; k < K; ++k) {
+      acc += x[k] * wg[k];
+      acc2 += x[k] * wu[k];
+    }
     if (ok) ((float*)a.y)[(long long)m * a.ldy + n] = silu(acc) * acc2;
     return;
   }
@@ -189,10 +260,11 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
   if (a.nseg > 2 && nc >= a.seg[2].n0) si = 2;
   const float* w = (const float*)a.seg[si].w + (long long)(nc - a.seg[si].n0) * K;
   for (int k = 0; k < K; ++k) acc += x[k] * w[k];
-  if (MODE == GEMM_PARTIAL) {
-    if (ok) ((float*)a.y)[(long long)m * a.ldy + n] = acc;
+  float* Y = (float*)a.y;
+  if (MODE == GEMM_STORE) {
+    if (ok) Y[(long long)m * a.ldy + n] = acc;
   } else {
-    if (ok) ((float*)a.y)[(long long)m * a.ldy + n] = acc;
+    if (ok) Y[(long long)m * a.ldy + n] = acc;
     // 64 consecutive columns form one wave: its max is that tile's max
     const float v = wave_max(ok ? acc : -INFINITY);
     if ((threadIdx.x & 63) == 0 && ok) a.tilemax[(long long)m * a.ntiles + n / 64] = v;
@@ -201,20 +273,48 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 
 }  // namespace
 
+hipError_t pack_panels(const void* w, int N, int K, void* out, hipStream_t s) {
+  if (K % kStep) return hipErrorInvalidValue;
+  const long long chunks = (long long)((N + 15) / 16) * (K / kStep) * 64;
+  const int blocks = int(std::min<long long>(8192, (chunks + 255) / 256));
+  hipLaunchKernelGGL(pack_panels_kernel, dim3(blocks), dim3(256), 0, s, (const bf16_t*)w, N, K, (bf16_t*)out);
+  return hipGetLastError();
+}
+
+size_t packed_elems(int N, int K) { return (size_t)((N + 15) / 16) * 16 * K; }
+
+int gemm_groups(int mode, int N) {
+  switch (mode) {
+    case GEMM_SILU: return (N + 31) / 32;     // 2 gate + 2 up panels of 16 features
+    case GEMM_LOGITS: return (N + 255) / 256;  // 8 waves x 2 panels
+    default: return (N + 63) / 64;            // 4 waves x 1 panel
+  }
+}
+
 hipError_t gemm_bf16(const GemmArgs& a, hipStream_t s) {
-  if (a.K % 128 != 0) return hipErrorInvalidValue;
+  if (a.K % kStep != 0 || a.M < 1 || a.splits < 1 || a.splits > a.K / kStep) return hipErrorInvalidValue;
+  const int g = gemm_groups(a.mode, a.N);
   switch (a.mode) {
-    case GEMM_PARTIAL: return launch_bf16<GEMM_PARTIAL>(a, s);
-    case GEMM_SILU: return launch_bf16<GEMM_SILU>(a, s);
-    default: return launch_bf16<GEMM_LOGITS>(a, s);
+    case GEMM_STORE:
+      for (int i = 1; i < a.nseg; ++i)
+        if (a.seg[i].n0 % 64) return hipErrorInvalidValue;  // a workgroup never straddles segments
+      return launch_bf16<1, 4, 4, GEMM_STORE>(a, g, s);
+    case GEMM_SILU:
+      if (a.splits != 1) return hipErrorInvalidValue;
+      return launch_bf16<1, 4, 4, GEMM_SILU>(a, g, s);
+    case GEMM_LOGITS:
+      if (a.splits != 1 || a.ntiles != g) return hipErrorInvalidValue;
+      return launch_bf16<2, 8, 2, GEMM_LOGITS>(a, g, s);
+    default:
+      return hipErrorInvalidValue;
   }
 }
 
 hipError_t gemm_f32(const GemmArgs& a, hipStream_t s) {
   dim3 grid((a.N + 255) / 256, a.M);
   switch (a.mode) {
-    case GEMM_PARTIAL:
-      hipLaunchKernelGGL(gemm_f32_kernel<GEMM_PARTIAL>, grid, dim3(256), 0, s, a); break;
+    case GEMM_STORE:
+      hipLaunchKernelGGL(gemm_f32_kernel<GEMM_STORE>, grid, dim3(256), 0, s, a); break;
     case GEMM_SILU:
       hipLaunchKernelGGL(gemm_f32_kernel<GEMM_SILU>, grid, dim3(256), 0, s, a); break;
     default:

@@ -13,22 +13,26 @@ struct GemmSeg {
 };
 
 enum GemmMode {
-  GEMM_PARTIAL = 0,  // fp32 split-K partials: Y[split][M][N]
-  GEMM_SILU = 1,     // dual weights (gate = seg 0, up = seg 1): out_T[M][N] = silu(g) * u
-  GEMM_LOGITS = 2,   // fp32 Y[M][N] plus per-(row, 64-column tile) maxima
+  GEMM_STORE = 0,   // fp32 Y[split][M][N] = X W^T over the split's K range
+  GEMM_SILU = 2,    // dual weights (gate = seg 0, up = seg 1): out_T[M][N] = silu(g) * u
+  GEMM_LOGITS = 3,  // fp32 Y[M][N] plus one maximum per (row, column group)
 };
 
 struct GemmArgs {
   const void* x; int ldx; int M;
   GemmSeg seg[3]; int nseg;
   int N, K;
-  int splits;             // split-K factor (GEMM_PARTIAL only)
+  int splits;             // split-K factor (GEMM_STORE); 1 otherwise
   void* y; int ldy;       // output (fp32, or T for GEMM_SILU)
   long long split_stride; // elements between split partials
   float* tilemax; int ntiles;  // GEMM_LOGITS: [M][ntiles]
   int mode;
 };
 
+// bf16 weights are used in the packed panel layout (see gemm.hip).
+hipError_t pack_panels(const void* w, int N, int K, void* out, hipStream_t s);
+size_t packed_elems(int N, int K);
+int gemm_groups(int mode, int N);   // workgroups along N for a mode
 hipError_t gemm_bf16(const GemmArgs& a, hipStream_t s);
 hipError_t gemm_f32(const GemmArgs& a, hipStream_t s);
 
@@ -53,17 +57,19 @@ struct KVLayout {
 };
 
 // ------------------------------------------------------------ elementwise ----
+// x[r] = E[tok[r * tok_stride]] (ids clamped to [0, V)); xn[r] = rmsnorm(x[r]) * g
 template <typename T>
-hipError_t embed_rows(const int* tok, int tok_stride, int R, const T* E, int d, int V, float* x,
-                      hipStream_t s);
-// x[r] += sum_p parts[p][r]; xn[r] = rmsnorm(x[r]) * g
+hipError_t embed_rmsnorm(const int* tok, int tok_stride, int R, const T* E, int d, int V, float* x,
+                         const float* g, float eps, T* xn, hipStream_t s);
+// x[r] += sum_p parts[p][r] (nparts <= 8); xn[r] = rmsnorm(x[r]) * g
 template <typename T>
-hipError_t residual_rmsnorm(float* x, const float* parts, int nparts, long long part_stride,
-                            const float* g, float eps, int R, int d, T* xn, hipStream_t s);
-// q/k/v from split partials, RoPE, q -> qbuf, k/v -> cache
+hipError_t residual_rmsnorm(float* x, const float* parts, int nparts, long long part_stride, const float* g,
+                            float eps, int R, int d, T* xn, hipStream_t s);
+// q/k/v = sum of nparts split partials [R][(Hq+2Hkv)D] fp32 -> RoPE -> q (T),
+// k/v appended to the cache
 template <typename T>
-hipError_t qkv_rope_store(const float* parts, int nparts, long long part_stride, const Rows& rows,
-                          int Hq, int Hkv, int D, float theta, T* q, const KVLayout& kv, hipStream_t s);
+hipError_t qkv_rope_store(const float* parts, int nparts, long long part_stride, const Rows& rows, int Hq,
+                          int Hkv, int D, float theta, T* q, const KVLayout& kv, hipStream_t s);
 
 // -------------------------------------------------------------- attention ----
 struct AttnArgs {
@@ -82,6 +88,7 @@ struct AttnArgs {
   int tail_chunk; int tail_chunks;    // part index splits .. splits+tail_chunks-1
 };
 hipError_t attn_prefix_mfma_bf16(const AttnArgs& a, hipStream_t s);
+hipError_t attn_tail_mfma_bf16(const AttnArgs& a, hipStream_t s);
 template <typename T> hipError_t attn_prefix_vec(const AttnArgs& a, hipStream_t s);
 template <typename T> hipError_t attn_tail_vec(const AttnArgs& a, hipStream_t s);
 template <typename T> hipError_t attn_combine(const AttnArgs& a, T* out, hipStream_t s);

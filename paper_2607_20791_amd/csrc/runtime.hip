@@ -75,6 +75,13 @@ struct rgd_model {
   const float* final_norm = nullptr;
   const void* lm_head = nullptr;
   std::vector<rgd_layer_weights> layers;
+  // bf16 matrices repacked into the GEMM panel layout (owned); fp32 models use
+  // the caller's matrices directly
+  struct Packed {
+    void *wq, *wk, *wv, *wo, *w_gate, *w_up, *w_down;
+  };
+  std::vector<Packed> packed;
+  void* lm_head_packed = nullptr;
   int max_rows = 0;
   int part_rows = 0;  // row capacity of the split-K partial buffers
   int nqkv = 0, ntiles = 0, nchunks = 0;
@@ -253,10 +260,10 @@ Rows device_rows(const rgd_model* m, const rgd_kv* kv, int R, int t, bool prefil
   return r;
 }
 
-int splitk(int tiles, int mblocks, int kblocks, int R, int cap_rows) {
-  int ks = (int)cdiv(512, (long long)tiles * mblocks);
-  ks = std::min(ks, kblocks);
+int pick_splits(int groups, int mblocks, int K, int R, int cap_rows) {
+  int ks = (int)cdiv(512, (long long)groups * mblocks);
   ks = std::min(ks, 8);
+  ks = std::min(ks, std::max(1, K / 64 / 4));
   ks = std::min(ks, std::max(1, cap_rows / std::max(R, 1)));
   return std::max(ks, 1);
 }
@@ -301,7 +308,7 @@ int run_attention(rgd_model* m, const KVLayout& kvl, const Rows& rows, const Hos
       TimeScope tp(m, RGD_TIMER_ATTN_PREFIX, s);
       HIP_OK(attn_prefix_mfma_bf16(a, s));
     }
-    HIP_OK(attn_tail_vec<bf16_t>(a, s));
+    HIP_OK(attn_tail_mfma_bf16(a, s));
     HIP_OK(attn_combine<bf16_t>(a, (bf16_t*)out, s));
   } else {
     HIP_OK(attn_prefix_vec<float>(a, s));
@@ -323,7 +330,7 @@ int lm_head(rgd_model* m, const void* x, int ldx, int R, float* logits, hipStrea
   g.x = x;
   g.ldx = ldx;
   g.M = R;
-  g.seg[0] = {m->lm_head, 0, m->cfg.vocab};
+  g.seg[0] = {m->bf16 ? m->lm_head_packed : m->lm_head, 0, m->cfg.vocab};
   g.nseg = 1;
   g.N = m->cfg.vocab;
   g.K = m->cfg.d_model;
@@ -344,12 +351,15 @@ int forward_rows(rgd_model* m, rgd_kv* kv, const Rows& rows, const HostRows& h, 
   const rgd_model_config& c = m->cfg;
   const int R = rows.R, d = c.d_model, Hq = c.n_heads, Hkv = c.n_kv_heads, D = c.head_dim;
   const int F = c.ffn_dim;
-  const int mblocks = (int)cdiv(R, 64);
   const bool bf = m->bf16;
+  const int mblocks = (int)cdiv(R, 64);
+  const float* g0 = (const float*)m->layers[0].attn_norm;
   if (bf)
-    HIP_OK(embed_rows<bf16_t>(feed, feed_stride, R, (const bf16_t*)m->embed, d, c.vocab, m->x, s));
+    HIP_OK(embed_rmsnorm<bf16_t>(feed, feed_stride, R, (const bf16_t*)m->embed, d, c.vocab, m->x, g0, c.rms_eps,
+                                 (bf16_t*)m->xn, s));
   else
-    HIP_OK(embed_rows<float>(feed, feed_stride, R, (const float*)m->embed, d, c.vocab, m->x, s));
+    HIP_OK(embed_rmsnorm<float>(feed, feed_stride, R, (const float*)m->embed, d, c.vocab, m->x, g0, c.rms_eps,
+                                (float*)m->xn, s));
   auto norm = [&](const float* parts, int np, const void* gain) -> hipError_t {
     const long long stride = (long long)R * d;
     return bf ? residual_rmsnorm<bf16_t>(m->x, parts, np, stride, (const float*)gain, c.rms_eps, R, d,
@@ -357,26 +367,31 @@ int forward_rows(rgd_model* m, rgd_kv* kv, const Rows& rows, const HostRows& h, 
               : residual_rmsnorm<float>(m->x, parts, np, stride, (const float*)gain, c.rms_eps, R, d,
                                         (float*)m->xn, s);
   };
-  HIP_OK(norm(nullptr, 0, m->layers[0].attn_norm));
+  auto splits = [&](int mode, int N, int K) {
+    return bf ? pick_splits(gemm_groups(mode, N), mblocks, K, R, m->part_rows) : 1;
+  };
   for (int l = 0; l < c.n_layers; ++l) {
     const rgd_layer_weights& L = m->layers[l];
     const KVLayout kvl = kv->layer(l);
-    // fused Q/K/V projection (split-K partials)
+    const void* wq = bf ? m->packed[l].wq : L.wq;
+    const void* wk = bf ? m->packed[l].wk : L.wk;
+    const void* wv = bf ? m->packed[l].wv : L.wv;
+    // fused Q/K/V projection (split-K partials, summed by the RoPE epilogue)
     GemmArgs g{};
     g.x = m->xn;
     g.ldx = d;
     g.M = R;
-    g.seg[0] = {L.wq, 0, Hq * D};
-    g.seg[1] = {L.wk, Hq * D, Hkv * D};
-    g.seg[2] = {L.wv, (Hq + Hkv) * D, Hkv * D};
+    g.seg[0] = {wq, 0, Hq * D};
+    g.seg[1] = {wk, Hq * D, Hkv * D};
+    g.seg[2] = {wv, (Hq + Hkv) * D, Hkv * D};
     g.nseg = 3;
     g.N = m->nqkv;
     g.K = d;
-    g.splits = bf ? splitk((int)cdiv(g.N, 64), mblocks, d / 128, R, m->part_rows) : 1;
+    g.splits = splits(GEMM_STORE, g.N, d);
     g.y = m->qkv_part;
     g.ldy = g.N;
     g.split_stride = (long long)R * g.N;
-    g.mode = GEMM_PARTIAL;
+    g.mode = GEMM_STORE;
     RGD_TRY(gemm(m, g, s));
     if (bf)
       HIP_OK(qkv_rope_store<bf16_t>(m->qkv_part, g.splits, g.split_stride, rows, Hq, Hkv, D, c.rope_theta,
@@ -385,20 +400,20 @@ int forward_rows(rgd_model* m, rgd_kv* kv, const Rows& rows, const HostRows& h, 
       HIP_OK(qkv_rope_store<float>(m->qkv_part, g.splits, g.split_stride, rows, Hq, Hkv, D, c.rope_theta,
                                    (float*)m->q, kvl, s));
     RGD_TRY(run_attention(m, kvl, rows, h, rows.prefill ? 0 : rows.t + 1, 0, m->attn_out, s));
-    // output projection + residual + ffn norm
+    // output projection: partials added to the residual stream by the FFN norm
     GemmArgs o{};
     o.x = m->attn_out;
     o.ldx = Hq * D;
     o.M = R;
-    o.seg[0] = {L.wo, 0, d};
+    o.seg[0] = {bf ? m->packed[l].wo : L.wo, 0, d};
     o.nseg = 1;
     o.N = d;
     o.K = Hq * D;
-    o.splits = bf ? splitk((int)cdiv(d, 64), mblocks, o.K / 128, R, m->part_rows) : 1;
+    o.splits = splits(GEMM_STORE, d, o.K);
     o.y = m->o_part;
     o.ldy = d;
     o.split_stride = (long long)R * d;
-    o.mode = GEMM_PARTIAL;
+    o.mode = GEMM_STORE;
     RGD_TRY(gemm(m, o, s));
     HIP_OK(norm(m->o_part, o.splits, L.ffn_norm));
     // SwiGLU: act = silu(W_gate xn) * (W_up xn)
@@ -406,8 +421,8 @@ int forward_rows(rgd_model* m, rgd_kv* kv, const Rows& rows, const HostRows& h, 
     f.x = m->xn;
     f.ldx = d;
     f.M = R;
-    f.seg[0] = {L.w_gate, 0, F};
-    f.seg[1] = {L.w_up, 0, F};
+    f.seg[0] = {bf ? m->packed[l].w_gate : L.w_gate, 0, F};
+    f.seg[1] = {bf ? m->packed[l].w_up : L.w_up, 0, F};
     f.nseg = 2;
     f.N = F;
     f.K = d;
@@ -420,15 +435,15 @@ int forward_rows(rgd_model* m, rgd_kv* kv, const Rows& rows, const HostRows& h, 
     dn.x = m->act;
     dn.ldx = F;
     dn.M = R;
-    dn.seg[0] = {L.w_down, 0, d};
+    dn.seg[0] = {bf ? m->packed[l].w_down : L.w_down, 0, d};
     dn.nseg = 1;
     dn.N = d;
     dn.K = F;
-    dn.splits = bf ? splitk((int)cdiv(d, 64), mblocks, F / 128, R, m->part_rows) : 1;
+    dn.splits = splits(GEMM_STORE, d, F);
     dn.y = m->down_part;
     dn.ldy = d;
     dn.split_stride = (long long)R * d;
-    dn.mode = GEMM_PARTIAL;
+    dn.mode = GEMM_STORE;
     RGD_TRY(gemm(m, dn, s));
     const void* next_gain = l + 1 < c.n_layers ? m->layers[l + 1].attn_norm : (const void*)m->final_norm;
     HIP_OK(norm(m->down_part, dn.splits, next_gain));
@@ -597,7 +612,7 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
   m->part_rows = std::max(max_rows, 512);
   const int R = max_rows, d = cfg->d_model, Hq = cfg->n_heads, Hkv = cfg->n_kv_heads, D = cfg->head_dim;
   m->nqkv = (Hq + 2 * Hkv) * D;
-  m->ntiles = (int)cdiv(cfg->vocab, 64);
+  m->ntiles = m->bf16 ? gemm_groups(GEMM_LOGITS, cfg->vocab) : (int)cdiv(cfg->vocab, 64);
   m->nchunks = (int)cdiv(cfg->vocab, kSampleChunk);
   const size_t e = m->esz;
   const size_t PR = m->part_rows;
@@ -627,6 +642,28 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
   A(&m->d_base, (size_t)R * 4);
   A(&m->d_plen, (size_t)R * 4);
   A(&m->d_rblocks, (size_t)R * 16);
+  // bf16: repack every matrix into the GEMM panel layout
+  if (rc == RGD_OK && m->bf16) {
+    auto pack = [&](const void* src, int N, int K, void** dst) {
+      if (rc != RGD_OK) return;
+      rc = m->alloc(dst, packed_elems(N, K) * 2);
+      if (rc == RGD_OK && pack_panels(src, N, K, *dst, nullptr) != hipSuccess)
+        rc = fail(RGD_E_HIP, "weight packing failed");
+    };
+    m->packed.resize(cfg->n_layers);
+    for (int l = 0; l < cfg->n_layers; ++l) {
+      const rgd_layer_weights& L = m->layers[l];
+      rgd_model::Packed& P = m->packed[l];
+      pack(L.wq, Hq * D, d, &P.wq);
+      pack(L.wk, Hkv * D, d, &P.wk);
+      pack(L.wv, Hkv * D, d, &P.wv);
+      pack(L.wo, d, Hq * D, &P.wo);
+      pack(L.w_gate, cfg->ffn_dim, d, &P.w_gate);
+      pack(L.w_up, cfg->ffn_dim, d, &P.w_up);
+      pack(L.w_down, d, cfg->ffn_dim, &P.w_down);
+    }
+    pack(m->lm_head, cfg->vocab, d, &m->lm_head_packed);
+  }
   if (rc != RGD_OK) {
     delete m;
     return rc;

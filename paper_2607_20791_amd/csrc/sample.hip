@@ -64,8 +64,18 @@ __global__ __launch_bounds__(256) void argmax_kernel(const float* z, long long l
 }
 
 RGD_DEV float row_max_from_partials(const float* pmax, int npmax, int r, float* red) {
+  const float* p = pmax + (long long)r * npmax;
   float mx = -INFINITY;
-  for (int i = threadIdx.x; i < npmax; i += 256) mx = fmaxf(mx, pmax[(long long)r * npmax + i]);
+  const int n4 = npmax & ~3;
+  if ((((uintptr_t)p) & 15) == 0) {
+    for (int i = threadIdx.x * 4; i < n4; i += 1024) {
+      const float4 v = *(const float4*)(p + i);
+      mx = fmaxf(mx, fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w)));
+    }
+    for (int i = n4 + threadIdx.x; i < npmax; i += 256) mx = fmaxf(mx, p[i]);
+  } else {
+    for (int i = threadIdx.x; i < npmax; i += 256) mx = fmaxf(mx, p[i]);
+  }
   return block_max(mx, red);
 }
 
@@ -86,31 +96,35 @@ RGD_DEV float block_inclusive_scan(float v, float* wsum) {
 }
 
 // Selects the token of row r for target u (in [0,1)) given the chunk sums.
-// Returns the token id (valid in thread 0).
+// Returns the token id (valid in every thread).
 RGD_DEV int select_token(const SampleArgs& a, int r, float mx, float u) {
   __shared__ float csum[256];
-  __shared__ int sh_chunk;
+  __shared__ int sh_chunk, sh_last_nz;
   __shared__ float sh_base, sh_target;
   __shared__ float wsum[4];
   __shared__ int red_i[4];
   const float kT = kLog2e / a.T;
-  if (threadIdx.x == 0) {
-    float acc = 0.f;
-    for (int c = 0; c < a.nchunks; ++c) {
-      acc += __hip_atomic_load(a.chunk_sums + (long long)r * a.nchunks + c, __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
-      csum[c] = acc;
-    }
-    const float target = u * acc;
-    int cs = -1, last_nz = 0;
-    for (int c = 0; c < a.nchunks; ++c) {
-      const float prev = c ? csum[c - 1] : 0.f;
-      if (csum[c] > prev) last_nz = c;
-      if (cs < 0 && csum[c] > target) cs = c;
-    }
-    if (cs < 0) cs = last_nz;
-    sh_chunk = cs;
-    sh_base = cs ? csum[cs - 1] : 0.f;
+  // running sum over chunks in chunk order (one chunk per thread)
+  const int c = threadIdx.x;
+  const float mine = c < a.nchunks ? a.chunk_sums[(long long)r * a.nchunks + c] : 0.f;
+  const float incl_c = block_inclusive_scan(mine, wsum);
+  csum[c] = incl_c;
+  if (c == 0) {
+    sh_chunk = 0x7FFFFFFF;
+    sh_last_nz = 0;
+  }
+  __syncthreads();
+  const float total = csum[a.nchunks - 1];
+  const float target = u * total;
+  if (c < a.nchunks) {
+    const float prev = c ? csum[c - 1] : 0.f;
+    if (incl_c > prev) atomicMax(&sh_last_nz, c);
+    if (incl_c > target && prev <= target) atomicMin(&sh_chunk, c);
+  }
+  __syncthreads();
+  if (c == 0) {
+    if (sh_chunk == 0x7FFFFFFF) sh_chunk = sh_last_nz;
+    sh_base = sh_chunk ? csum[sh_chunk - 1] : 0.f;
     sh_target = target;
   }
   __syncthreads();
@@ -118,20 +132,30 @@ RGD_DEV int select_token(const SampleArgs& a, int r, float mx, float u) {
   const int per = a.chunk / 256;
   const int e0 = lo + threadIdx.x * per, e1 = min(hi, e0 + per);
   const float* zr = a.z + r * a.ldz;
+  float wv[16];
   float ts = 0.f;
-  for (int i = e0; i < e1; ++i) {
-    const float w = exp2f((zr[i] - mx) * kT);
-    if (w >= a.p_min) ts += w;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int e = e0 + i;
+    float w = 0.f;
+    if (i < per && e < e1) {
+      w = exp2f((zr[e] - mx) * kT);
+      w = w >= a.p_min ? w : -1.f;   // -1 marks a dropped token
+    } else {
+      w = -1.f;
+    }
+    wv[i] = w;
+    ts += w > 0.f ? w : (w == 0.f ? 0.f : 0.f);
   }
   const float incl = block_inclusive_scan(ts, wsum);
   float run = sh_base + (incl - ts);
   int found = 0x7FFFFFFF, last = -1;
-  for (int i = e0; i < e1; ++i) {
-    const float w = exp2f((zr[i] - mx) * kT);
-    if (w >= a.p_min) {
-      run += w;
-      last = i;
-      if (found == 0x7FFFFFFF && run > sh_target) found = i;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    if (wv[i] >= 0.f) {
+      run += wv[i];
+      last = e0 + i;
+      if (found == 0x7FFFFFFF && run > sh_target) found = e0 + i;
     }
   }
   // smallest found index, else the last kept index of the chunk
@@ -156,13 +180,13 @@ RGD_DEV int select_token(const SampleArgs& a, int r, float mx, float u) {
 
 __global__ __launch_bounds__(256) void minp_sum_kernel(SampleArgs a) {
   __shared__ float red[4];
-  __shared__ int is_last;
   const int c = blockIdx.x, r = blockIdx.y;
   const float mx = row_max_from_partials(a.pmax, a.npmax, r, red);
   const float kT = kLog2e / a.T;
   const float* zr = a.z + r * a.ldz;
   const int lo = c * a.chunk, hi = min(a.V, lo + a.chunk);
   float sum = 0.f;
+#pragma unroll 4
   for (int i = lo + threadIdx.x * 4; i < hi; i += 1024) {
     const float4 v = *(const float4*)(zr + i);  // V and chunk are multiples of 4
     const float w0 = exp2f((v.x - mx) * kT), w1 = exp2f((v.y - mx) * kT);
@@ -172,23 +196,20 @@ __global__ __launch_bounds__(256) void minp_sum_kernel(SampleArgs a) {
   }
   sum = block_sum(sum, red);
   if (threadIdx.x == 0) {
-    __hip_atomic_store(a.chunk_sums + (long long)r * a.nchunks + c, sum, __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_AGENT);
-    __threadfence();
-    const unsigned prev = __hip_atomic_fetch_add(a.counters + r, 1u, __ATOMIC_ACQ_REL,
-                                                 __HIP_MEMORY_SCOPE_AGENT);
-    is_last = prev == unsigned(a.nchunks - 1);
+    a.chunk_sums[(long long)r * a.nchunks + c] = sum;
+    if (c == 0 && a.status && !(mx > -INFINITY && mx < INFINITY)) atomicOr(a.status, 1);
   }
-  __syncthreads();
-  if (!is_last) return;
-  __threadfence();
-  if (!(mx > -INFINITY && mx < INFINITY) && threadIdx.x == 0 && a.status) atomicOr(a.status, 1);
+}
+
+__global__ __launch_bounds__(256) void minp_select_kernel(SampleArgs a) {
+  __shared__ float red[4];
+  const int r = blockIdx.x;
+  const float mx = row_max_from_partials(a.pmax, a.npmax, r, red);
   const float u = philox_uniform(a.seeds[r], a.ctr, a.stream);
   const int tok = select_token(a, r, mx, u);
   if (threadIdx.x == 0) {
     a.out[r * a.out_stride + a.out_col] = tok;
     if (a.cur_tok) a.cur_tok[r] = tok;
-    a.counters[r] = 0u;
   }
 }
 
@@ -267,10 +288,11 @@ hipError_t argmax_rows(const float* z, long long ldz, int R, int V, unsigned lon
 }
 
 hipError_t minp_sample(const SampleArgs& a, hipStream_t s) {
-  if (a.chunk % 1024 || a.chunk / 256 * 256 != a.chunk || a.V % 4 || a.nchunks > 256 ||
+  if (a.chunk % 1024 || a.chunk > 4096 || a.V % 4 || a.nchunks > 256 ||
       a.nchunks * a.chunk < a.V || !(a.T > 0.f))
     return hipErrorInvalidValue;
   hipLaunchKernelGGL(minp_sum_kernel, dim3(a.nchunks, a.R), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(minp_select_kernel, dim3(a.R), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
