@@ -116,13 +116,18 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
 void rgd_model_destroy(rgd_model* m);
 
 /* KV state for up to max_prompts prompts of up to max_prefix positions each.
- *  prefix_k/prefix_v: dev [n_layers][max_prompts][max_prefix][Hkv][D] - the
- *    shared prompt KV (rotated keys), written only by rgd_prefill_kv or by the
- *    caller, read in place by every probe and branch, never copied.
- *  pool_k/pool_v: dev [n_layers][n_pages][page_size][Hkv][D] - pages of the
- *    per-row tails (probe positions, branch positions).
- * The handle keeps per-prompt prefix lengths, page tables and the page free
- * list.  All four buffers are caller owned. */
+ * Keys are stored position-major, values head-dim-major (transposed per KV
+ * head), with VP = max_prefix rounded up to a multiple of 16:
+ *  prefix_k: dev [n_layers][max_prompts][max_prefix][Hkv][D]
+ *  prefix_v: dev [n_layers][max_prompts][Hkv][D][VP]
+ *    - the shared prompt KV (rotated keys), written only by rgd_prefill_kv
+ *    or by the caller, read in place by every probe and branch, never copied.
+ *  pool_k: dev [n_layers][n_pages][page_size][Hkv][D]
+ *  pool_v: dev [n_layers][n_pages][Hkv][D][page_size]
+ *    - pages of the per-row tails (probe positions, branch positions).
+ * bf16 models need page_size % 16 == 0.  The handle keeps per-prompt prefix
+ * lengths, page tables and the page free list.  All four buffers are caller
+ * owned. */
 int32_t rgd_kv_create(const rgd_model* m, int32_t max_prompts, int32_t max_prefix, int32_t n_pages,
                       int32_t page_size, void* prefix_k, void* prefix_v, void* pool_k, void* pool_v,
                       rgd_kv** out);
@@ -231,9 +236,9 @@ int32_t rgd_timing_read(rgd_model* m, double* ms, int64_t* launches);
 /* Decode attention for R rows of one layer: q dev [R][Hq][D] (model dtype)
  * over prompt row_prompt[r]'s first plen[r] prefix positions followed by
  * tail_len positions of the row's own tail.  row_prompt and plen are HOST int32
- * [R]; rows of one prompt must be contiguous.  prefix_k/v dev
- * [max_prompts][max_prefix][Hkv][D]; pool_k/v dev [n_pages][page_size][Hkv][D];
- * pages dev int32 [R][max_pages] (may be NULL when tail_len == 0).  out dev
+ * [R]; rows of one prompt must be contiguous.  prefix_k, prefix_v, pool_k,
+ * pool_v are one layer of the layouts of rgd_kv_create; pages dev int32
+ * [R][max_pages] (may be NULL when tail_len == 0).  out dev
  * [R][Hq*D] (model dtype).  splits = 0 picks the prefix split count.
  * Asynchronous. */
 int32_t rgd_kernel_attention(rgd_model* m, const void* q, int32_t R, const int32_t* row_prompt,

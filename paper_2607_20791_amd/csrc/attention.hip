@@ -6,8 +6,10 @@
 // all query vectors of the row block (rows x the G query heads of the KV head,
 // up to 64) consume it with MFMA.  Scores are computed transposed,
 // S^T = K Q^T, so that each lane ends up holding eight probabilities of one
-// query vector; those feed O^T += V^T P^T directly as the B operand, with V
-// staged transposed in LDS.  Online softmax runs in the exp2 domain with the
+// query vector; those feed O^T += V^T P^T directly as the B operand.  The V
+// cache is kept head-dim-major (transposed per KV head), so the V^T tile is a
+// plain copy into LDS.  The next tile is fetched into registers while the
+// current one is consumed.  Online softmax runs in the exp2 domain with the
 // row statistics reduced by lane shuffles across the four lane groups.
 //
 // Each row's own tail (paged) is handled by a vector kernel, and a combine
@@ -77,22 +79,25 @@ __global__ __launch_bounds__(NWAVE * 64) void attn_mfma_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t vt_lds[128][40];
 
   const long long pstride = (long long)a.Hkv * D;
+  const int ps = a.kv.page_size;
   const bf16_t* kbase;
   const bf16_t* vbase;
   if (PAGED) {
     kbase = (const bf16_t*)a.kv.pool_k + g * D;
-    vbase = (const bf16_t*)a.kv.pool_v + g * D;
+    vbase = (const bf16_t*)a.kv.pool_v + (long long)g * D * ps;
   } else {
     kbase = (const bf16_t*)a.kv.prefix_k + (long long)b * a.kv.P * pstride + g * D;
-    vbase = (const bf16_t*)a.kv.prefix_v + (long long)b * a.kv.P * pstride + g * D;
+    vbase = (const bf16_t*)a.kv.prefix_v + ((long long)b * a.Hkv + g) * D * a.kv.VP;
   }
   const int* pages = PAGED ? a.rows.pages + (long long)r0 * a.rows.max_pages : nullptr;
-  auto row_off = [&](int pos) -> long long {
-    if (PAGED) {
-      const int ps = a.kv.page_size;
-      return ((long long)pages[pos / ps] * ps + pos % ps) * pstride;
-    }
+  auto krow_off = [&](int pos) -> long long {
+    if (PAGED) return ((long long)pages[pos / ps] * ps + pos % ps) * pstride;
     return (long long)pos * pstride;
+  };
+  // start of the 8 V values (d, pos0 .. pos0+7); pos0 is a multiple of 8
+  auto v_off = [&](int d, int pos0) -> long long {
+    if (PAGED) return ((long long)pages[pos0 / ps] * a.Hkv * D + d) * ps + pos0 % ps;
+    return (long long)d * a.kv.VP + pos0;
   };
   const float scale = rsqrtf(float(D)) * kLog2e;
 
@@ -106,14 +111,25 @@ __global__ __launch_bounds__(NWAVE * 64) void attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < SEGS; ++i) {
       const int seg = threadIdx.x + i * NT;
+      // K: 32 positions x 16 segments of 8 dims
       const int pos = t0 + (seg >> 4), pc = (seg & 15) * 8;
       kreg[i] = u32x4{0u, 0u, 0u, 0u};
-      vreg[i] = u32x4{0u, 0u, 0u, 0u};
-      if (pos < hi) {
-        const long long off = row_off(pos) + pc;
-        kreg[i] = *(const u32x4*)(kbase + off);
-        vreg[i] = *(const u32x4*)(vbase + off);
+      if (pos < hi) kreg[i] = *(const u32x4*)(kbase + krow_off(pos) + pc);
+      // V^T: 128 dims x 4 segments of 8 positions; positions >= hi read as 0
+      const int d = seg >> 2, p0 = t0 + (seg & 3) * 8;
+      const int nv = hi - p0;
+      u32x4 vv = {0u, 0u, 0u, 0u};
+      if (nv > 0) {
+        vv = *(const u32x4*)(vbase + v_off(d, p0));
+        if (nv < 8) {
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            if (2 * w >= nv) vv[w] = 0u;
+            else if (2 * w + 1 >= nv) vv[w] &= 0xFFFFu;
+          }
+        }
       }
+      vreg[i] = vv;
     }
   };
 
@@ -123,13 +139,8 @@ __global__ __launch_bounds__(NWAVE * 64) void attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < SEGS; ++i) {
       const int seg = threadIdx.x + i * NT;
-      const int pr = seg >> 4, pc = (seg & 15) * 8;
-      *(u32x4*)&ks_lds[pr][pc] = kreg[i];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        vt_lds[pc + 2 * e][pr] = bf16_t(vreg[i][e] & 0xFFFFu);
-        vt_lds[pc + 2 * e + 1][pr] = bf16_t(vreg[i][e] >> 16);
-      }
+      *(u32x4*)&ks_lds[seg >> 4][(seg & 15) * 8] = kreg[i];
+      *(u32x4*)&vt_lds[seg >> 2][(seg & 3) * 8] = vreg[i];
     }
     if (t0 + 32 < hi) load_tile(t0 + 32);
     __syncthreads();
@@ -221,14 +232,17 @@ __global__ __launch_bounds__(256) void attn_vec_kernel(AttnArgs a) {
     qs[i / D][i % D] = load_f((const T*)a.q + ((long long)r * a.Hq + g * G) * D + i);
   __syncthreads();
 
-  auto kv_row = [&](int pos, bool want_v) -> const T* {
-    if (PREFIX) {
-      const T* base = (const T*)(want_v ? a.kv.prefix_v : a.kv.prefix_k);
-      return base + ((long long)a.rows.prompt[r] * a.kv.P + pos) * pstride + g * D;
-    }
+  auto k_row = [&](int pos) -> const T* {
+    if (PREFIX) return (const T*)a.kv.prefix_k + ((long long)a.rows.prompt[r] * a.kv.P + pos) * pstride + g * D;
     const int page = a.rows.pages[(long long)r * a.rows.max_pages + pos / a.kv.page_size];
-    const T* base = (const T*)(want_v ? a.kv.pool_v : a.kv.pool_k);
-    return base + ((long long)page * a.kv.page_size + pos % a.kv.page_size) * pstride + g * D;
+    return (const T*)a.kv.pool_k + ((long long)page * a.kv.page_size + pos % a.kv.page_size) * pstride + g * D;
+  };
+  auto v_at = [&](int pos, int d) -> float {
+    if (PREFIX)
+      return load_f((const T*)a.kv.prefix_v + (((long long)a.rows.prompt[r] * a.Hkv + g) * D + d) * a.kv.VP + pos);
+    const int ps = a.kv.page_size;
+    const int page = a.rows.pages[(long long)r * a.rows.max_pages + pos / ps];
+    return load_f((const T*)a.kv.pool_v + (((long long)page * a.Hkv + g) * D + d) * ps + pos % ps);
   };
 
   const float scale = rsqrtf(float(D));
@@ -236,7 +250,7 @@ __global__ __launch_bounds__(256) void attn_vec_kernel(AttnArgs a) {
   const int pos = lo + t;
   if (t < kChunk) {
     if (pos < hi) {
-      const T* kr = kv_row(pos, false);
+      const T* kr = k_row(pos);
       float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
       for (int d = 0; d < D; ++d) {
         const float kd = load_f(kr + d);
@@ -261,7 +275,7 @@ __global__ __launch_bounds__(256) void attn_vec_kernel(AttnArgs a) {
   for (int i = threadIdx.x; i < G * D; i += 256) {
     const int h = i / D, d = i % D;
     float acc = 0.f;
-    for (int p = lo; p < hi; ++p) acc += sc[h][p - lo] * load_f(kv_row(p, true) + d);
+    for (int p = lo; p < hi; ++p) acc += sc[h][p - lo] * v_at(p, d);
     const long long idx = ((long long)c + (PREFIX ? 0 : a.splits)) * a.rows.R + r;
     const int head = g * G + h;
     a.part_o[(idx * a.Hq + head) * D + d] = lh[h] > 0.f ? acc / lh[h] : 0.f;
@@ -292,14 +306,14 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a, T* out) {
 }  // namespace
 
 hipError_t attn_prefix_mfma_bf16(const AttnArgs& a, hipStream_t s) {
-  if (a.D != 128 || a.Hq / a.Hkv > 64 || a.split_len % 32) return hipErrorInvalidValue;
+  if (a.D != 128 || a.Hq / a.Hkv > 64 || a.split_len % 32 || a.kv.VP % 16) return hipErrorInvalidValue;
   if (a.splits <= 0 || a.nrblocks <= 0) return hipSuccess;
   hipLaunchKernelGGL((attn_mfma_kernel<4, false>), dim3(a.splits, a.Hkv, a.nrblocks), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t attn_tail_mfma_bf16(const AttnArgs& a, hipStream_t s) {
-  if (a.D != 128 || a.Hq / a.Hkv > 16 || a.tail_chunk % 32) return hipErrorInvalidValue;
+  if (a.D != 128 || a.Hq / a.Hkv > 16 || a.tail_chunk % 32 || a.kv.page_size % 16) return hipErrorInvalidValue;
   if (a.tail_chunks <= 0) return hipSuccess;
   hipLaunchKernelGGL((attn_mfma_kernel<1, true>), dim3(a.tail_chunks, a.Hkv, a.rows.R), dim3(64), 0, s, a);
   return hipGetLastError();

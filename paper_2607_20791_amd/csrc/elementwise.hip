@@ -75,22 +75,26 @@ __global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(float* x
   norm_store(xr, d, g, eps, xn + (long long)r * d);
 }
 
+// One workgroup per (row, group of 8 heads of the fused q|k|v output).
 template <typename T>
 __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* parts, int nparts, long long part_stride,
                                                        Rows rows, int Hq, int Hkv, int D, float theta, T* q,
                                                        KVLayout kv) {
   __shared__ float cs[128], sn[128];
   const int r = blockIdx.x;
+  const int h0 = blockIdx.y * 8, h1 = min(h0 + 8, Hq + 2 * Hkv);
   const int half = D / 2;
   const int pos = rows.prefill ? rows.base_pos[r] : rows.base_pos[r] + rows.t;
-  for (int j = threadIdx.x; j < half; j += 256) {
-    // angle in fp64: pos * theta^(-2j/D), reduced mod 2*pi before sin/cos
-    const double ang = double(pos) * pow(double(theta), -2.0 * double(j) / double(D));
-    const double red = ang - 6.283185307179586 * floor(ang / 6.283185307179586);
-    double s, c;
-    sincos(red, &s, &c);
-    cs[j] = float(c);
-    sn[j] = float(s);
+  if (h0 < Hq + Hkv) {
+    for (int j = threadIdx.x; j < half; j += 256) {
+      // angle in fp64: pos * theta^(-2j/D), reduced mod 2*pi before sin/cos
+      const double ang = double(pos) * pow(double(theta), -2.0 * double(j) / double(D));
+      const double red = ang - 6.283185307179586 * floor(ang / 6.283185307179586);
+      double sv, cv;
+      sincos(red, &sv, &cv);
+      cs[j] = float(cv);
+      sn[j] = float(sv);
+    }
   }
   __syncthreads();
   const int nqkv = (Hq + 2 * Hkv) * D;
@@ -103,39 +107,39 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* parts, int n
     return v;
   };
   const int b = rows.prompt[r];
-  long long kv_off;
+  long long kv_off;  // K row of this position
   T* kd;
-  T* vd;
+  T* vd;             // V of head h, dim d at vd[(h * D + d) * vstride]
+  long long vstride;
   if (rows.prefill) {
     kv_off = ((long long)b * kv.P + pos) * Hkv * D;
     kd = (T*)kv.prefix_k;
-    vd = (T*)kv.prefix_v;
+    vd = (T*)kv.prefix_v + (long long)b * Hkv * D * kv.VP + pos;
+    vstride = kv.VP;
   } else {
     const int page = rows.pages[(long long)r * rows.max_pages + rows.t / kv.page_size];
     kv_off = ((long long)page * kv.page_size + rows.t % kv.page_size) * Hkv * D;
     kd = (T*)kv.pool_k;
-    vd = (T*)kv.pool_v;
+    vd = (T*)kv.pool_v + (long long)page * Hkv * D * kv.page_size + rows.t % kv.page_size;
+    vstride = kv.page_size;
   }
-  // rotated q and k: pairs (j, j + D/2) of each head (q heads, then k heads)
-  const int npairs = (Hq + Hkv) * half;
-  for (int i = threadIdx.x; i < npairs; i += 256) {
-    const int h = i / half, j = i % half;
+  const int nh = h1 - h0;
+  for (int i = threadIdx.x; i < nh * half; i += 256) {
+    const int h = h0 + i / half, j = i % half;
     const int base = h * D;
-    const float x1 = col(base + j), x2 = col(base + j + half);
-    const float y1 = x1 * cs[j] - x2 * sn[j];
-    const float y2 = x2 * cs[j] + x1 * sn[j];
-    if (h < Hq) {
-      T* qr = q + ((long long)r * Hq + h) * D;
-      store_f(qr + j, y1);
-      store_f(qr + j + half, y2);
-    } else {
-      T* kr = kd + kv_off + (long long)(h - Hq) * D;
-      store_f(kr + j, y1);
-      store_f(kr + j + half, y2);
+    if (h < Hq + Hkv) {  // rotated q or k pair (j, j + D/2)
+      const float x1 = col(base + j), x2 = col(base + j + half);
+      const float y1 = x1 * cs[j] - x2 * sn[j];
+      const float y2 = x2 * cs[j] + x1 * sn[j];
+      T* dst = h < Hq ? q + ((long long)r * Hq + h) * D : kd + kv_off + (long long)(h - Hq) * D;
+      store_f(dst + j, y1);
+      store_f(dst + j + half, y2);
+    } else {             // v: dims j and j + D/2 of head h - Hq - Hkv
+      const int hv = h - Hq - Hkv;
+      store_f(vd + ((long long)hv * D + j) * vstride, col(base + j));
+      store_f(vd + ((long long)hv * D + j + half) * vstride, col(base + j + half));
     }
   }
-  const int vbase = (Hq + Hkv) * D;
-  for (int i = threadIdx.x; i < Hkv * D; i += 256) store_f(vd + kv_off + i, col(vbase + i));
 }
 
 }  // namespace
@@ -162,8 +166,8 @@ template <typename T>
 hipError_t qkv_rope_store(const float* parts, int nparts, long long part_stride, const Rows& rows, int Hq,
                           int Hkv, int D, float theta, T* q, const KVLayout& kv, hipStream_t s) {
   if (D > 256 || (D & 1) || nparts < 1 || nparts > 8) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(qkv_rope_kernel<T>, dim3(rows.R), dim3(256), 0, s, parts, nparts, part_stride, rows, Hq, Hkv,
-                     D, theta, q, kv);
+  hipLaunchKernelGGL(qkv_rope_kernel<T>, dim3(rows.R, (Hq + 2 * Hkv + 7) / 8), dim3(256), 0, s, parts, nparts,
+                     part_stride, rows, Hq, Hkv, D, theta, q, kv);
   return hipGetLastError();
 }
 

@@ -49,12 +49,19 @@ struct Rows {
   int prefill;          // 1: K/V go to the prefix at base_pos; no tail
 };
 
+// K is stored position-major and V head-dim-major (transposed per KV head) so
+// that both MFMA operand tiles of attention are plain row copies.
 struct KVLayout {
-  void* prefix_k; void* prefix_v;  // this layer: [B][P][Hkv][D]
-  void* pool_k; void* pool_v;      // this layer: [pages][page_size][Hkv][D]
-  int P;                           // prefix capacity per prompt
+  void* prefix_k;  // this layer: [B][P][Hkv][D]
+  void* prefix_v;  // this layer: [B][Hkv][D][VP]
+  void* pool_k;    // this layer: [pages][page_size][Hkv][D]
+  void* pool_v;    // this layer: [pages][Hkv][D][page_size]
+  int P;           // prefix capacity per prompt
+  int VP;          // V row stride: P rounded up to a multiple of 16
   int page_size;
 };
+
+inline int v_stride(int P) { return (P + 15) / 16 * 16; }
 
 // ------------------------------------------------------------ elementwise ----
 // x[r] = E[tok[r * tok_stride]] (ids clamped to [0, V)); xn[r] = rmsnorm(x[r]) * g

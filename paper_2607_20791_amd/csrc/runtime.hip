@@ -152,14 +152,16 @@ struct rgd_kv {
   KVLayout layer(int l) const {
     const rgd_model_config& c = m->cfg;
     const long long per_pos = (long long)c.n_kv_heads * c.head_dim;
-    const long long pre = (long long)max_prompts * max_prefix * per_pos * m->esz;
+    const long long pre_k = (long long)max_prompts * max_prefix * per_pos * m->esz;
+    const long long pre_v = (long long)max_prompts * v_stride(max_prefix) * per_pos * m->esz;
     const long long pool = (long long)n_pages * page_size * per_pos * m->esz;
     KVLayout k;
-    k.prefix_k = (char*)prefix_k + l * pre;
-    k.prefix_v = (char*)prefix_v + l * pre;
+    k.prefix_k = (char*)prefix_k + l * pre_k;
+    k.prefix_v = (char*)prefix_v + l * pre_v;
     k.pool_k = (char*)pool_k + l * pool;
     k.pool_v = (char*)pool_v + l * pool;
     k.P = max_prefix;
+    k.VP = v_stride(max_prefix);
     k.page_size = page_size;
     return k;
   }
@@ -695,6 +697,7 @@ int32_t rgd_kv_create(const rgd_model* m, int32_t max_prompts, int32_t max_prefi
   if (max_prompts < 1 || max_prefix < 1 || n_pages < 0 || page_size < 1 || page_size > 4096)
     return fail(RGD_E_INVALID_ARG, "kv sizes out of range");
   if (max_prefix > m->cfg.max_pos) return fail(RGD_E_INVALID_ARG, "max_prefix exceeds the model's max_pos");
+  if (m->bf16 && page_size % 16) return fail(RGD_E_UNSUPPORTED, "bf16 models need page_size % 16 == 0");
   rgd_kv* kv = new rgd_kv();
   kv->m = m;
   kv->max_prompts = max_prompts;
@@ -1119,6 +1122,7 @@ int32_t rgd_kernel_attention(rgd_model* m, const void* q, int32_t R, const int32
   if (max_prompts < 1 || max_prefix < 1 || tail_len < 0 || splits < 0) return fail(RGD_E_INVALID_ARG, "bad sizes");
   if (tail_len > 0 && (!pool_k || !pool_v || !pages || page_size < 1 || max_pages < cdiv(tail_len, page_size)))
     return fail(RGD_E_INVALID_ARG, "tail arguments inconsistent");
+  if (m->bf16 && tail_len > 0 && page_size % 16) return fail(RGD_E_UNSUPPORTED, "bf16 needs page_size % 16 == 0");
   HostRows h;
   for (int r = 0; r < R; ++r) {
     if (row_prompt[r] < 0 || row_prompt[r] >= max_prompts) return fail(RGD_E_INVALID_ARG, "row_prompt out of range");
@@ -1148,6 +1152,7 @@ int32_t rgd_kernel_attention(rgd_model* m, const void* q, int32_t R, const int32
   kvl.pool_k = const_cast<void*>(pool_k);
   kvl.pool_v = const_cast<void*>(pool_v);
   kvl.P = max_prefix;
+  kvl.VP = v_stride(max_prefix);
   kvl.page_size = page_size;
   // q is read from the model's q buffer: copy the caller's q there first
   const size_t qbytes = (size_t)R * m->cfg.n_heads * m->cfg.head_dim * m->esz;

@@ -49,17 +49,25 @@ def alloc_kv(model: Model, w, max_prompts: int, max_prefix: int, n_pages: int,
              page_size: int = 16) -> KV:
     torch = _torch()
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
-    pre = (w.n_layers, max_prompts, max_prefix, w.n_kv_heads, w.head_dim)
-    pool = (w.n_layers, max(n_pages, 1), page_size, w.n_kv_heads, w.head_dim)
-    pk = torch.zeros(pre, dtype=dt, device="cuda")
-    pv = torch.zeros(pre, dtype=dt, device="cuda")
-    qk = torch.zeros(pool, dtype=dt, device="cuda")
-    qv = torch.zeros(pool, dtype=dt, device="cuda")
+    pre_k = (w.n_layers, max_prompts, max_prefix, w.n_kv_heads, w.head_dim)
+    pre_v = (w.n_layers, max_prompts, w.n_kv_heads, w.head_dim, v_stride(max_prefix))
+    pool_k = (w.n_layers, max(n_pages, 1), page_size, w.n_kv_heads, w.head_dim)
+    pool_v = (w.n_layers, max(n_pages, 1), w.n_kv_heads, w.head_dim, page_size)
+    pk = torch.zeros(pre_k, dtype=dt, device="cuda")
+    pv = torch.zeros(pre_v, dtype=dt, device="cuda")
+    qk = torch.zeros(pool_k, dtype=dt, device="cuda")
+    qv = torch.zeros(pool_v, dtype=dt, device="cuda")
     return KV(model, max_prompts, max_prefix, n_pages, page_size, pk, pv, qk, qv)
 
 
+def v_stride(max_prefix: int) -> int:
+    """Row stride of the head-dim-major V cache: max_prefix rounded up to 16."""
+    return (max_prefix + 15) // 16 * 16
+
+
 def fill_prefix(kv: KV, layer: int, k: np.ndarray, v: np.ndarray):
-    """Writes caller-generated prefix K/V [B][P][Hkv][D] into positions [0, P)."""
+    """Writes caller-generated prefix K/V [B][P][Hkv][D] into positions [0, P)
+    (V goes to the head-dim-major layout)."""
     B, P = k.shape[:2]
     kv.prefix_k[layer, :B, :P].copy_(to_device(k))
-    kv.prefix_v[layer, :B, :P].copy_(to_device(v))
+    kv.prefix_v[layer, :B, :, :, :P].copy_(to_device(np.ascontiguousarray(v.transpose(0, 2, 3, 1))))
