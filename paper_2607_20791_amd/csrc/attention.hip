@@ -28,15 +28,16 @@ RGD_DEV f32x4 mfma16x16x32(const u32x4& a, const u32x4& b, f32x4 c) {
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
-RGD_DEV uint32_t pack2(float lo, float hi) {
-  return uint32_t(f32_to_bf16(lo)) | (uint32_t(f32_to_bf16(hi)) << 16);
-}
+RGD_DEV uint32_t pack2(float lo, float hi) { return pack_bf16x2(lo, hi); }
 
 // NWAVE waves; PAGED selects the row's paged tail (one row per workgroup)
 // instead of the shared prompt prefix (a block of rows of one prompt).
+// Tiles hold TP = 64 positions; the next tile is fetched into registers while
+// the current one is consumed from LDS.
 template <int NWAVE, bool PAGED>
 __global__ __launch_bounds__(NWAVE * 64) void attn_mfma_kernel(AttnArgs a) {
-  constexpr int D = 128, NT = NWAVE * 64, SEGS = 512 / NT;
+  constexpr int D = 128, NT = NWAVE * 64, TP = 64;
+  constexpr int KSEG = TP * 16 / NT, VSEG = D * (TP / 8) / NT;  // 16-byte segments per thread
   const int s = blockIdx.x, g = blockIdx.y;
   int r0, nr, b, maxlen, lo, hi, part;
   if (PAGED) {
@@ -59,8 +60,9 @@ __global__ __launch_bounds__(NWAVE * 64) void attn_mfma_kernel(AttnArgs a) {
   }
   const int G = a.Hq / a.Hkv;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int l16 = lane & 15, grp = lane >> 4;
   const int nq = nr * G;
-  const int v = wave * 16 + (lane & 15);
+  const int v = wave * 16 + l16;
   const bool vok = v < nq;
   const bool wave_active = wave * 16 < nq;
   const int row = r0 + (vok ? v / G : 0);
@@ -69,14 +71,14 @@ __global__ __launch_bounds__(NWAVE * 64) void attn_mfma_kernel(AttnArgs a) {
 
   u32x4 qf[4];
   {
-    const bf16_t* qp = (const bf16_t*)a.q + ((long long)row * a.Hq + head) * D + (lane >> 4) * 8;
+    const bf16_t* qp = (const bf16_t*)a.q + ((long long)row * a.Hq + head) * D + grp * 8;
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks)
       qf[ks] = vok ? *(const u32x4*)(qp + ks * 32) : u32x4{0u, 0u, 0u, 0u};
   }
 
-  __shared__ __attribute__((aligned(16))) bf16_t ks_lds[32][136];
-  __shared__ __attribute__((aligned(16))) bf16_t vt_lds[128][40];
+  __shared__ __attribute__((aligned(16))) bf16_t ks_lds[TP][136];
+  __shared__ __attribute__((aligned(16))) bf16_t vt_lds[D][TP + 8];
 
   const long long pstride = (long long)a.Hkv * D;
   const int ps = a.kv.page_size;
@@ -90,15 +92,6 @@ __global__ __launch_bounds__(NWAVE * 64) void attn_mfma_kernel(AttnArgs a) {
     vbase = (const bf16_t*)a.kv.prefix_v + ((long long)b * a.Hkv + g) * D * a.kv.VP;
   }
   const int* pages = PAGED ? a.rows.pages + (long long)r0 * a.rows.max_pages : nullptr;
-  auto krow_off = [&](int pos) -> long long {
-    if (PAGED) return ((long long)pages[pos / ps] * ps + pos % ps) * pstride;
-    return (long long)pos * pstride;
-  };
-  // start of the 8 V values (d, pos0 .. pos0+7); pos0 is a multiple of 8
-  auto v_off = [&](int d, int pos0) -> long long {
-    if (PAGED) return ((long long)pages[pos0 / ps] * a.Hkv * D + d) * ps + pos0 % ps;
-    return (long long)d * a.kv.VP + pos0;
-  };
   const float scale = rsqrtf(float(D)) * kLog2e;
 
   float m = -INFINITY, lsum = 0.f;
@@ -106,22 +99,31 @@ __global__ __launch_bounds__(NWAVE * 64) void attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  u32x4 kreg[SEGS], vreg[SEGS];
-  auto load_tile = [&](int t0) {
+  constexpr int NSET = 1;  // tile sets in registers (one tile in flight while one is consumed)
+  u32x4 kreg[NSET][KSEG], vreg[NSET][VSEG];
+  auto load_tile = [&](int t0, int set) {
 #pragma unroll
-    for (int i = 0; i < SEGS; ++i) {
+    for (int i = 0; i < KSEG; ++i) {
       const int seg = threadIdx.x + i * NT;
-      // K: 32 positions x 16 segments of 8 dims
       const int pos = t0 + (seg >> 4), pc = (seg & 15) * 8;
-      kreg[i] = u32x4{0u, 0u, 0u, 0u};
-      if (pos < hi) kreg[i] = *(const u32x4*)(kbase + krow_off(pos) + pc);
-      // V^T: 128 dims x 4 segments of 8 positions; positions >= hi read as 0
-      const int d = seg >> 2, p0 = t0 + (seg & 3) * 8;
+      u32x4 kk = {0u, 0u, 0u, 0u};
+      if (pos < hi) {
+        const long long ro = PAGED ? ((long long)pages[pos / ps] * ps + pos % ps) * pstride : (long long)pos * pstride;
+        kk = *(const u32x4*)(kbase + ro + pc);
+      }
+      kreg[set][i] = kk;
+    }
+#pragma unroll
+    for (int i = 0; i < VSEG; ++i) {
+      const int seg = threadIdx.x + i * NT;
+      const int d = seg >> 3, p0 = t0 + (seg & 7) * 8;
       const int nv = hi - p0;
       u32x4 vv = {0u, 0u, 0u, 0u};
       if (nv > 0) {
-        vv = *(const u32x4*)(vbase + v_off(d, p0));
-        if (nv < 8) {
+        const long long vo = PAGED ? ((long long)pages[p0 / ps] * a.Hkv * D + d) * ps + p0 % ps
+                                   : (long long)d * a.kv.VP + p0;
+        vv = *(const u32x4*)(vbase + vo);
+        if (nv < 8) {  // positions past the range read as 0
 #pragma unroll
           for (int w = 0; w < 4; ++w) {
             if (2 * w >= nv) vv[w] = 0u;
@@ -129,72 +131,91 @@ __global__ __launch_bounds__(NWAVE * 64) void attn_mfma_kernel(AttnArgs a) {
           }
         }
       }
-      vreg[i] = vv;
+      vreg[set][i] = vv;
     }
   };
 
-  if (lo < hi) load_tile(lo);
-  for (int t0 = lo; t0 < hi; t0 += 32) {
+  auto consume = [&](int t0, int set) {
     __syncthreads();
 #pragma unroll
-    for (int i = 0; i < SEGS; ++i) {
+    for (int i = 0; i < KSEG; ++i) {
       const int seg = threadIdx.x + i * NT;
-      *(u32x4*)&ks_lds[seg >> 4][(seg & 15) * 8] = kreg[i];
-      *(u32x4*)&vt_lds[seg >> 2][(seg & 3) * 8] = vreg[i];
+      *(u32x4*)&ks_lds[seg >> 4][(seg & 15) * 8] = kreg[set][i];
     }
-    if (t0 + 32 < hi) load_tile(t0 + 32);
+#pragma unroll
+    for (int i = 0; i < VSEG; ++i) {
+      const int seg = threadIdx.x + i * NT;
+      *(u32x4*)&vt_lds[seg >> 3][(seg & 7) * 8] = vreg[set][i];
+    }
+    if (t0 + NSET * TP < hi) load_tile(t0 + NSET * TP, set);
     __syncthreads();
-    if (wave_active) {
-      f32x4 sc[2];
+    if (!wave_active) return;
+    // S^T = K Q^T: 4 position blocks of 16; lane holds positions 16*mt + 4*grp + i
+    f32x4 sc[4];
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt) {
-        sc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int mt = 0; mt < 4; ++mt) {
+      sc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-          const u32x4 ka = *(const u32x4*)&ks_lds[mt * 16 + (lane & 15)][ks * 32 + (lane >> 4) * 8];
-          sc[mt] = mfma16x16x32(ka, qf[ks], sc[mt]);
-        }
-      }
-      float x[8];
-      float tmax = -INFINITY;
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int pos = t0 + mt * 16 + (lane >> 4) * 4 + i;
-          const float val = pos < my_end ? sc[mt][i] * scale : -INFINITY;
-          x[mt * 4 + i] = val;
-          tmax = fmaxf(tmax, val);
-        }
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-      const float mnew = fmaxf(m, tmax);
-      float p[8];
-      float alpha = 1.f, ps = 0.f;
-      if (mnew == -INFINITY) {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) p[j] = 0.f;
-      } else {
-        alpha = exp2f(m - mnew);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          p[j] = exp2f(x[j] - mnew);
-          ps += p[j];
-        }
-      }
-      m = mnew;
-      lsum = lsum * alpha + ps;
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) o[dt] *= alpha;
-      const u32x4 pb = {pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]), pack2(p[6], p[7])};
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) {
-        const bf16_t* vr = &vt_lds[dt * 16 + (lane & 15)][0];
-        const u32x2 a0 = *(const u32x2*)(vr + (lane >> 4) * 4);
-        const u32x2 a1 = *(const u32x2*)(vr + 16 + (lane >> 4) * 4);
-        o[dt] = mfma16x16x32(u32x4{a0.x, a0.y, a1.x, a1.y}, pb, o[dt]);
+      for (int ks = 0; ks < 4; ++ks) {
+        const u32x4 ka = *(const u32x4*)&ks_lds[mt * 16 + l16][ks * 32 + grp * 8];
+        sc[mt] = mfma16x16x32(ka, qf[ks], sc[mt]);
       }
     }
+    float tmax = -INFINITY;
+    const bool full = t0 + TP <= my_end;
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float val = sc[mt][i] * scale;
+        if (!full && t0 + mt * 16 + grp * 4 + i >= my_end) val = -INFINITY;
+        sc[mt][i] = val;
+        tmax = fmaxf(tmax, val);
+      }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    const float mnew = fmaxf(m, tmax);
+    // a query with nothing visible yet (only possible past a causal end) keeps
+    // m = -inf: its probabilities are 0 and its state is left unscaled
+    const bool none = mnew == -INFINITY;
+    const float alpha = none ? 1.f : exp2f(m - mnew);
+    const float msub = none ? 0.f : mnew;
+    m = mnew;
+    float ps_ = 0.f;
+    u32x4 pb[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      float p[8];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        p[i] = exp2f(sc[2 * h][i] - msub);
+        p[4 + i] = exp2f(sc[2 * h + 1][i] - msub);
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) ps_ += p[i];
+      pb[h] = u32x4{pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]), pack2(p[6], p[7])};
+    }
+    lsum = lsum * alpha + ps_;
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) {
+      o[dt] *= alpha;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const bf16_t* vr = &vt_lds[dt * 16 + l16][h * 32 + grp * 4];
+        const u32x2 a0 = *(const u32x2*)vr;
+        const u32x2 a1 = *(const u32x2*)(vr + 16);
+        o[dt] = mfma16x16x32(u32x4{a0.x, a0.y, a1.x, a1.y}, pb[h], o[dt]);
+      }
+    }
+  };
+
+#pragma unroll
+  for (int k = 0; k < NSET; ++k)
+    if (lo + k * TP < hi) load_tile(lo + k * TP, k);
+  for (int t0 = lo; t0 < hi; t0 += NSET * TP) {
+#pragma unroll
+    for (int k = 0; k < NSET; ++k)
+      if (t0 + k * TP < hi) consume(t0 + k * TP, k);
   }
 
   float lt = lsum + __shfl_xor(lsum, 16, 64);
@@ -206,8 +227,8 @@ __global__ __launch_bounds__(NWAVE * 64) void attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) po[dt * 16 + (lane >> 4) * 4 + i] = o[dt][i] * inv;
-    if ((lane >> 4) == 0) a.part_lse[idx] = lt > 0.f ? (m + __log2f(lt)) * kLn2 : -INFINITY;
+      for (int i = 0; i < 4; ++i) po[dt * 16 + grp * 4 + i] = o[dt][i] * inv;
+    if (grp == 0) a.part_lse[idx] = lt > 0.f ? (m + __log2f(lt)) * kLn2 : -INFINITY;
   }
 }
 
@@ -283,6 +304,176 @@ __global__ __launch_bounds__(256) void attn_vec_kernel(AttnArgs a) {
   }
 }
 
+// Tail attention fused with the merge of all partials: one workgroup per
+// (row, KV head).  The row's own tail positions are attended on the vector
+// units (each K row and each V value is loaded once and used by all G query
+// heads of the KV head), then the prefix-split partials of those heads are
+// merged with the tail in log-sum-exp form and the final output is written.
+constexpr int kTailBlk = 256;
+constexpr int kMaxSplits = 40;
+
+// 8 consecutive elements starting at p (16-byte aligned for bf16, 32 for fp32)
+RGD_DEV void load8(const bf16_t* p, float* out) {
+  const u32x4 v = *(const u32x4*)p;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    out[2 * w] = __uint_as_float(v[w] << 16);
+    out[2 * w + 1] = __uint_as_float(v[w] & 0xFFFF0000u);
+  }
+}
+RGD_DEV void load8(const float* p, float* out) {
+  const float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
+  out[0] = a.x; out[1] = a.y; out[2] = a.z; out[3] = a.w;
+  out[4] = b.x; out[5] = b.y; out[6] = b.z; out[7] = b.w;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void attn_tail_combine_kernel(AttnArgs a, T* out) {
+  const int r = blockIdx.x, g = blockIdx.y;
+  const int D = a.D, G = a.Hq / a.Hkv;
+  const long long R = a.rows.R;
+  __shared__ __attribute__((aligned(16))) float qs[8][256];
+  __shared__ float sc[8][kTailBlk];
+  __shared__ float red[4];
+  __shared__ float accx[2048];  // [part][head][dim], part * D == 256
+  for (int i = threadIdx.x; i < G * D; i += 256)
+    qs[i / D][i % D] = load_f((const T*)a.q + ((long long)r * a.Hq + g * G) * D + i) * rsqrtf(float(D));
+  // the prefix-split partials do not depend on the tail: request them now so
+  // their latency overlaps the tail attention (first 16 splits, 2 pairs/thread)
+  constexpr int kPre = 16;
+  const int S = a.splits;
+  const long long pstep = R * a.Hq * D;
+  float pre[2][kPre];
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int i = threadIdx.x + k * 256;
+    const int h = i / D, dd = i % D;
+    const float* po = a.part_o + ((long long)r * a.Hq + g * G + h) * D + dd;
+#pragma unroll
+    for (int sp = 0; sp < kPre; ++sp) pre[k][sp] = (i < G * D && sp < S) ? po[sp * pstep] : 0.f;
+  }
+  __syncthreads();
+
+  // tail attention, online softmax over blocks of 256 positions
+  const int ps = a.kv.page_size;
+  const int* pages = a.rows.pages ? a.rows.pages + (long long)r * a.rows.max_pages : nullptr;
+  const long long pstride = (long long)a.Hkv * D;
+  // weighted sum layout: thread = (part, d); part handles 8-position blocks
+  const int nparts = 256 / D;
+  const int d = threadIdx.x % D, part = threadIdx.x / D;
+  float mh[8], lh[8], acc[8];
+#pragma unroll
+  for (int h = 0; h < 8; ++h) {
+    mh[h] = -INFINITY;
+    lh[h] = 0.f;
+    acc[h] = 0.f;
+  }
+  for (int c0 = 0; c0 < a.tail_len; c0 += kTailBlk) {
+    const int n = min(kTailBlk, a.tail_len - c0);
+    const int j = threadIdx.x;
+    float dot[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if (j < n) {
+      const int pos = c0 + j;
+      const T* kr = (const T*)a.kv.pool_k + ((long long)pages[pos / ps] * ps + pos % ps) * pstride + g * D;
+      for (int e0 = 0; e0 < D; e0 += 8) {
+        float kv[8];
+        load8(kr + e0, kv);
+#pragma unroll
+        for (int h = 0; h < 8; ++h) {
+          if (h < G) {
+            const float4 q0 = *(const float4*)&qs[h][e0], q1 = *(const float4*)&qs[h][e0 + 4];
+            dot[h] += q0.x * kv[0] + q0.y * kv[1] + q0.z * kv[2] + q0.w * kv[3] + q1.x * kv[4] + q1.y * kv[5] +
+                      q1.z * kv[6] + q1.w * kv[7];
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int h = 0; h < 8; ++h)
+      if (h < G) sc[h][j] = j < n ? dot[h] : -INFINITY;
+    __syncthreads();
+    float alpha[8];
+#pragma unroll
+    for (int h = 0; h < 8; ++h) {
+      if (h >= G) break;
+      const float cm = block_max(sc[h][j], red);
+      const float mnew = fmaxf(mh[h], cm);
+      const float e = sc[h][j] == -INFINITY ? 0.f : __expf(sc[h][j] - mnew);
+      __syncthreads();
+      sc[h][j] = e;
+      const float bs = block_sum(e, red);
+      alpha[h] = mh[h] == -INFINITY ? 0.f : __expf(mh[h] - mnew);
+      lh[h] = lh[h] * alpha[h] + bs;
+      mh[h] = mnew;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int h = 0; h < 8; ++h)
+      if (h < G) acc[h] *= alpha[h];
+    for (int b0 = part * 8; b0 < n; b0 += nparts * 8) {
+      const int pos = c0 + b0;  // 8 positions inside one page (pages hold a multiple of 8)
+      float v[8];
+      load8((const T*)a.kv.pool_v + (((long long)pages[pos / ps] * a.Hkv + g) * D + d) * ps + pos % ps, v);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float ve = b0 + e < n ? v[e] : 0.f;
+#pragma unroll
+        for (int h = 0; h < 8; ++h)
+          if (h < G) acc[h] += sc[h][b0 + e < n ? b0 + e : 0] * ve;
+      }
+    }
+    __syncthreads();
+  }
+  // tail outputs per (head, dim): sum of the position parts in fixed order
+  __shared__ float wts[8][kMaxSplits + 1];  // merge weights; column `splits` is the tail
+  __syncthreads();
+#pragma unroll
+  for (int h = 0; h < 8; ++h)
+    if (h < G) accx[(part * 8 + h) * D + d] = acc[h];
+  // log-sum-exp of every prefix split of the G heads, loaded in parallel
+  for (int i = threadIdx.x; i < G * S; i += 256) {
+    const int h = i / S, sp = i % S;
+    wts[h][sp] = a.part_lse[(sp * R + r) * a.Hq + g * G + h];
+  }
+  __syncthreads();
+  if (threadIdx.x < G) {
+    const int h = threadIdx.x;
+    const float lt = lh[h] > 0.f ? mh[h] + __logf(lh[h]) : -INFINITY;
+    float M = lt;
+    for (int sp = 0; sp < S; ++sp) M = fmaxf(M, wts[h][sp]);
+    float den = 0.f;
+    for (int sp = 0; sp < S; ++sp) {
+      const float w = wts[h][sp] == -INFINITY ? 0.f : __expf(wts[h][sp] - M);
+      wts[h][sp] = w;
+      den += w;
+    }
+    const float wt = lt == -INFINITY ? 0.f : __expf(lt - M);
+    den += wt;
+    const float inv = den > 0.f ? 1.0f / den : 0.f;
+    for (int sp = 0; sp < S; ++sp) wts[h][sp] *= inv;
+    wts[h][S] = lh[h] > 0.f ? wt * inv / lh[h] : 0.f;  // applied to the unnormalised tail sum
+  }
+  __syncthreads();
+  for (int k = 0; k * 256 < G * D; ++k) {
+    const int i = threadIdx.x + k * 256;
+    if (i >= G * D) break;
+    const int h = i / D, dd = i % D;
+    const int head = g * G + h;
+    float tail = 0.f;
+    for (int pp = 0; pp < nparts; ++pp) tail += accx[(pp * 8 + h) * D + dd];
+    float o = wts[h][S] * tail;
+    if (k < 2) {
+#pragma unroll
+      for (int sp = 0; sp < kPre; ++sp)
+        if (sp < S) o += wts[h][sp] * pre[k & 1][sp];
+    }
+    const float* po = a.part_o + ((long long)r * a.Hq + head) * D + dd;
+#pragma unroll 4
+    for (int sp = k < 2 ? kPre : 0; sp < S; ++sp) o += wts[h][sp] * po[sp * pstep];
+    store_f(out + ((long long)r * a.Hq + head) * D + dd, o);
+  }
+}
+
 template <typename T>
 __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a, T* out) {
   const int r = blockIdx.x, h = blockIdx.y;
@@ -306,14 +497,14 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a, T* out) {
 }  // namespace
 
 hipError_t attn_prefix_mfma_bf16(const AttnArgs& a, hipStream_t s) {
-  if (a.D != 128 || a.Hq / a.Hkv > 64 || a.split_len % 32 || a.kv.VP % 16) return hipErrorInvalidValue;
+  if (a.D != 128 || a.Hq / a.Hkv > 64 || a.split_len % 64 || a.kv.VP % 16) return hipErrorInvalidValue;
   if (a.splits <= 0 || a.nrblocks <= 0) return hipSuccess;
   hipLaunchKernelGGL((attn_mfma_kernel<4, false>), dim3(a.splits, a.Hkv, a.nrblocks), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t attn_tail_mfma_bf16(const AttnArgs& a, hipStream_t s) {
-  if (a.D != 128 || a.Hq / a.Hkv > 16 || a.tail_chunk % 32 || a.kv.page_size % 16) return hipErrorInvalidValue;
+  if (a.D != 128 || a.Hq / a.Hkv > 16 || a.tail_chunk % 64 || a.kv.page_size % 16) return hipErrorInvalidValue;
   if (a.tail_chunks <= 0) return hipSuccess;
   hipLaunchKernelGGL((attn_mfma_kernel<1, true>), dim3(a.tail_chunks, a.Hkv, a.rows.R), dim3(64), 0, s, a);
   return hipGetLastError();
@@ -336,6 +527,15 @@ hipError_t attn_tail_vec(const AttnArgs& a, hipStream_t s) {
 }
 
 template <typename T>
+hipError_t attn_tail_combine(const AttnArgs& a, T* out, hipStream_t s) {
+  if (a.D > 128 || a.D < 8 || 256 % a.D || a.Hq / a.Hkv > 8 || (a.tail_len > 0 && !a.rows.pages) ||
+      (a.tail_len > 0 && a.kv.page_size % 8) || a.splits > kMaxSplits)
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(attn_tail_combine_kernel<T>, dim3(a.rows.R, a.Hkv), dim3(256), 0, s, a, out);
+  return hipGetLastError();
+}
+
+template <typename T>
 hipError_t attn_combine(const AttnArgs& a, T* out, hipStream_t s) {
   hipLaunchKernelGGL(attn_combine_kernel<T>, dim3(a.rows.R, a.Hq), dim3(128), 0, s, a, out);
   return hipGetLastError();
@@ -346,6 +546,8 @@ template hipError_t attn_prefix_vec<bf16_t>(const AttnArgs&, hipStream_t);
 template hipError_t attn_tail_vec<float>(const AttnArgs&, hipStream_t);
 template hipError_t attn_tail_vec<bf16_t>(const AttnArgs&, hipStream_t);
 template hipError_t attn_combine<float>(const AttnArgs&, float*, hipStream_t);
+template hipError_t attn_tail_combine<float>(const AttnArgs&, float*, hipStream_t);
+template hipError_t attn_tail_combine<bf16_t>(const AttnArgs&, bf16_t*, hipStream_t);
 template hipError_t attn_combine<bf16_t>(const AttnArgs&, bf16_t*, hipStream_t);
 
 }  // namespace rgd

@@ -18,11 +18,15 @@ constexpr int kWave = 64;
 
 RGD_DEV float bf16_to_f32(bf16_t b) { return __uint_as_float(uint32_t(b) << 16); }
 
-// round-to-nearest-even float -> bf16 (inputs are finite by construction)
-RGD_DEV bf16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return bf16_t(u >> 16);
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// round-to-nearest-even float -> bf16 (v_cvt_pk_bf16_f32 on gfx950)
+RGD_DEV bf16_t f32_to_bf16(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
+
+// two floats -> packed bf16 pair (lo in bits 0..15)
+RGD_DEV uint32_t pack_bf16x2(float lo, float hi) {
+  const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 template <typename T> RGD_DEV float load_f(const T* p);

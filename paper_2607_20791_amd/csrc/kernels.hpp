@@ -99,6 +99,9 @@ hipError_t attn_tail_mfma_bf16(const AttnArgs& a, hipStream_t s);
 template <typename T> hipError_t attn_prefix_vec(const AttnArgs& a, hipStream_t s);
 template <typename T> hipError_t attn_tail_vec(const AttnArgs& a, hipStream_t s);
 template <typename T> hipError_t attn_combine(const AttnArgs& a, T* out, hipStream_t s);
+// attends each row's tail (vector units) and merges it with the prefix-split
+// partials 0 .. splits-1 into the final output
+template <typename T> hipError_t attn_tail_combine(const AttnArgs& a, T* out, hipStream_t s);
 
 // ---------------------------------------------------------------- sampler ----
 hipError_t fill_u32(uint32_t* p, uint32_t v, long long n, hipStream_t s);

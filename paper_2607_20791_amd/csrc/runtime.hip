@@ -287,15 +287,15 @@ int run_attention(rgd_model* m, const KVLayout& kvl, const Rows& rows, const Hos
   a.nrblocks = (int)h.blocks.size();
   a.tail_len = tail_len;
   a.tail_chunk = kTailChunk;
-  a.tail_chunks = (int)cdiv(tail_len, kTailChunk);
+  a.tail_chunks = 0;  // tails are attended inside the merge kernel
   const int R = rows.R;
   const int cap = (int)std::min<long long>(kMaxParts, (long long)kMaxParts * m->max_rows / std::max(R, 1));
   if (m->bf16) {
     int S = force_splits;
     if (S <= 0) S = (int)cdiv(512, (long long)c.n_kv_heads * a.nrblocks);
-    S = (int)std::max<long long>(1, std::min<long long>(S, cdiv(std::max(h.maxplen, 1), 32)));
+    S = (int)std::max<long long>(1, std::min<long long>(S, cdiv(std::max(h.maxplen, 1), 64)));
     S = std::min(S, cap - a.tail_chunks);
-    a.split_len = (int)cdiv(cdiv(std::max(h.maxplen, 1), S), 32) * 32;
+    a.split_len = (int)cdiv(cdiv(std::max(h.maxplen, 1), S), 64) * 64;
     a.splits = (int)cdiv(std::max(h.maxplen, 1), a.split_len);
   } else {
     a.split_len = 256;
@@ -310,12 +310,10 @@ int run_attention(rgd_model* m, const KVLayout& kvl, const Rows& rows, const Hos
       TimeScope tp(m, RGD_TIMER_ATTN_PREFIX, s);
       HIP_OK(attn_prefix_mfma_bf16(a, s));
     }
-    HIP_OK(attn_tail_mfma_bf16(a, s));
-    HIP_OK(attn_combine<bf16_t>(a, (bf16_t*)out, s));
+    HIP_OK(attn_tail_combine<bf16_t>(a, (bf16_t*)out, s));
   } else {
     HIP_OK(attn_prefix_vec<float>(a, s));
-    HIP_OK(attn_tail_vec<float>(a, s));
-    HIP_OK(attn_combine<float>(a, (float*)out, s));
+    HIP_OK(attn_tail_combine<float>(a, (float*)out, s));
   }
   return RGD_OK;
 }
@@ -539,8 +537,8 @@ bool valid_dtype_shapes(const rgd_model_config& c, std::string& why) {
     why = "n_heads must be a multiple of n_kv_heads";
     return false;
   }
-  if (c.head_dim % 2 || c.head_dim > 256) {
-    why = "head_dim must be even and <= 256";
+  if (c.head_dim < 8 || c.head_dim > 128 || 256 % c.head_dim) {
+    why = "head_dim must be 8, 16, 32, 64 or 128";
     return false;
   }
   if (c.vocab % 4) {
