@@ -116,13 +116,14 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
 void rgd_model_destroy(rgd_model* m);
 
 /* KV state for up to max_prompts prompts of up to max_prefix positions each.
- * Keys are stored position-major, values head-dim-major (transposed per KV
- * head), with VP = max_prefix rounded up to a multiple of 16:
- *  prefix_k: dev [n_layers][max_prompts][max_prefix][Hkv][D]
- *  prefix_v: dev [n_layers][max_prompts][Hkv][D][VP]
+ * All caches are KV-head-major, so the positions of one head form contiguous
+ * runs; values are stored transposed (head dim before position) in blocks of
+ * 64 positions.  VP = max_prefix rounded up to a multiple of 64:
+ *  prefix_k: dev [n_layers][max_prompts][Hkv][max_prefix][D]
+ *  prefix_v: dev [n_layers][max_prompts][Hkv][VP/64][D][64]
  *    - the shared prompt KV (rotated keys), written only by rgd_prefill_kv
  *    or by the caller, read in place by every probe and branch, never copied.
- *  pool_k: dev [n_layers][n_pages][page_size][Hkv][D]
+ *  pool_k: dev [n_layers][n_pages][Hkv][page_size][D]
  *  pool_v: dev [n_layers][n_pages][Hkv][D][page_size]
  *    - pages of the per-row tails (probe positions, branch positions).
  * bf16 models need page_size % 16 == 0.  The handle keeps per-prompt prefix

@@ -1,19 +1,21 @@
 // Decode attention over a shared prompt KV plus per-row tails.
 //
 // The prompt KV of one prompt is read by every row (probe or branch) of that
-// prompt.  The shared part is split over (prefix split, KV head, row block):
-// a workgroup loads each 32-position K/V tile of its split once into LDS and
-// all query vectors of the row block (rows x the G query heads of the KV head,
-// up to 64) consume it with MFMA.  Scores are computed transposed,
-// S^T = K Q^T, so that each lane ends up holding eight probabilities of one
-// query vector; those feed O^T += V^T P^T directly as the B operand.  The V
-// cache is kept head-dim-major (transposed per KV head), so the V^T tile is a
-// plain copy into LDS.  The next tile is fetched into registers while the
-// current one is consumed.  Online softmax runs in the exp2 domain with the
-// row statistics reduced by lane shuffles across the four lane groups.
+// prompt.  bf16 path: the shared part is split over (prefix split, KV head,
+// row block); a workgroup streams 64-position K/V tiles of its split through
+// LDS once and all query vectors of the row block (rows x the G query heads of
+// the KV head, up to 256) consume them with MFMA.  Scores are computed
+// transposed, S^T = K Q^T, with the K rows gathered so that each lane ends up
+// holding eight consecutive positions of one query vector; those feed
+// O^T += V^T P^T directly as the B operand, and the V cache is kept
+// head-dim-major (transposed per KV head) so that V^T fragments are plain
+// 16-byte reads.  Online softmax runs in the exp2 domain with a lazily moved
+// exponent reference.  A second kernel attends each row's own paged tail (also
+// on MFMA) and merges it with the prefix-split (o, log-sum-exp) partials in a
+// fixed order.
 //
-// Each row's own tail (paged) is handled by a vector kernel, and a combine
-// kernel merges the (o, log-sum-exp) partials in a fixed order.
+// fp32 path: vector kernels of the same structure (prefix splits, then tail
+// plus merge).
 #include "kernels.hpp"
 
 namespace rgd {
@@ -30,205 +32,291 @@ RGD_DEV f32x4 mfma16x16x32(const u32x4& a, const u32x4& b, f32x4 c) {
 
 RGD_DEV uint32_t pack2(float lo, float hi) { return pack_bf16x2(lo, hi); }
 
-// NWAVE waves; PAGED selects the row's paged tail (one row per workgroup)
-// instead of the shared prompt prefix (a block of rows of one prompt).
-// Tiles hold TP = 64 positions; the next tile is fetched into registers while
-// the current one is consumed from LDS.
-template <int NWAVE, bool PAGED>
-__global__ __launch_bounds__(NWAVE * 64) void attn_mfma_kernel(AttnArgs a) {
-  constexpr int D = 128, NT = NWAVE * 64, TP = 64;
-  constexpr int KSEG = TP * 16 / NT, VSEG = D * (TP / 8) / NT;  // 16-byte segments per thread
+// 2^x on the hardware unit, without the denormal range fix-up of exp2f:
+// results below 2^-126 flush to zero, far below what a softmax weight in
+// bf16 or an fp32 sum of them can resolve.
+RGD_DEV float exp2_raw(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Exponent headroom of the lazy softmax rescale (log2 units).
+constexpr float kLazy = 8.f;
+
+#ifndef RGD_ATTN_NW
+#define RGD_ATTN_NW 8
+#endif
+
+// K tiles sit in LDS as unpadded 256-byte rows whose 16-byte chunks are
+// XOR-swizzled: chunk c of row r is stored at chunk c ^ kswz(r).  A fragment
+// read touches rows {0..3, 8..11, 16..19, 24..27} (+ a multiple of 4) of a
+// 32-row half, and kswz maps those to distinct chunk positions, so the reads
+// are free of bank conflicts.
+RGD_DEV int kswz(int r) { return (r & 3) | ((r >> 1) & 12); }
+
+// Row of a 64-position tile that lane l16 supplies as the A operand of score
+// block (h, e).  With this order the score MFMA leaves lane (q, grp) holding
+// positions h*32 + grp*8 + e*4 + {0..3}, i.e. eight consecutive positions per
+// 32-position half: exactly the B operand layout of the P V product, and the
+// matching V^T fragment is one contiguous 16-byte read.
+RGD_DEV int k_gather_row(int h, int e, int l16) { return h * 32 + (l16 >> 2) * 8 + e * 4 + (l16 & 3); }
+
+// Shared-prefix attention: one workgroup per (prefix split, KV head, block of
+// up to 256 query vectors of one prompt).  NW waves each own NQ MFMA column
+// tiles of 16 query vectors, so each K / V^T fragment read from LDS feeds NQ
+// MFMAs and each 64-position tile is fetched from HBM once for all rows of the
+// prompt.  The tile loop is software-pipelined: tiles are fetched into
+// registers one tile ahead and stored into a ring of three LDS buffers, and
+// the scores of tile t+1 are computed (MFMA) while the softmax of tile t runs
+// on the vector units.  One barrier per tile.
+template <int NW, int NQ>
+__global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
+  constexpr int D = 128, TP = 64, NT = NW * 64, NB = 3;
+  static_assert(NW * NQ * 16 == 256, "a workgroup covers 256 query vectors");
   const int s = blockIdx.x, g = blockIdx.y;
-  int r0, nr, b, maxlen, lo, hi, part;
-  if (PAGED) {
-    r0 = blockIdx.z;
-    nr = 1;
-    b = 0;
-    maxlen = a.tail_len;
-    lo = s * a.tail_chunk;
-    hi = min(lo + a.tail_chunk, maxlen);
-    part = a.splits + s;
-  } else {
-    const int4 rb = a.rblocks[blockIdx.z];
-    r0 = rb.x;
-    nr = rb.y;
-    b = rb.z;
-    maxlen = rb.w;
-    lo = s * a.split_len;
-    hi = min(lo + a.split_len, maxlen);
-    part = s;
-  }
+  const int4 rb = a.rblocks[blockIdx.z];
+  const int r0 = rb.x, nr = rb.y, b = rb.z, maxplen = rb.w;
+  const int lo = s * a.split_len;
+  const int hi = min(lo + a.split_len, maxplen);
   const int G = a.Hq / a.Hkv;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int l16 = lane & 15, grp = lane >> 4;
   const int nq = nr * G;
-  const int v = wave * 16 + l16;
-  const bool vok = v < nq;
-  const bool wave_active = wave * 16 < nq;
-  const int row = r0 + (vok ? v / G : 0);
-  const int head = g * G + (vok ? v % G : 0);
-  const int my_end = PAGED ? hi : (vok ? min(a.rows.plen[row], hi) : lo);
 
-  u32x4 qf[4];
-  {
-    const bf16_t* qp = (const bf16_t*)a.q + ((long long)row * a.Hq + head) * D + grp * 8;
+  // B operand of the score MFMA: lane (q, grp) holds dims ks*32 + grp*8 + {0..7}
+  u32x4 qf[NQ][4];
+  bool vok[NQ];
+  int vrow[NQ], vhead[NQ], vend[NQ];
+#pragma unroll
+  for (int nt = 0; nt < NQ; ++nt) {
+    const int v = wave * NQ * 16 + nt * 16 + l16;
+    vok[nt] = v < nq;
+    vrow[nt] = r0 + (vok[nt] ? v / G : 0);
+    vhead[nt] = g * G + (vok[nt] ? v % G : 0);
+    vend[nt] = vok[nt] ? min(a.rows.plen[vrow[nt]], hi) : lo;
+    const bf16_t* qp = (const bf16_t*)a.q + ((long long)vrow[nt] * a.Hq + vhead[nt]) * D + grp * 8;
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks)
-      qf[ks] = vok ? *(const u32x4*)(qp + ks * 32) : u32x4{0u, 0u, 0u, 0u};
+      qf[nt][ks] = vok[nt] ? *(const u32x4*)(qp + ks * 32) : u32x4{0u, 0u, 0u, 0u};
   }
+  const bool wave_active = (wave * NQ * 16) < nq;
 
-  __shared__ __attribute__((aligned(16))) bf16_t ks_lds[TP][136];
-  __shared__ __attribute__((aligned(16))) bf16_t vt_lds[D][TP + 8];
+  __shared__ __attribute__((aligned(16))) bf16_t k_lds[NB][TP * D];
+  __shared__ __attribute__((aligned(16))) bf16_t v_lds[NB][D][TP + 8];
 
-  const long long pstride = (long long)a.Hkv * D;
-  const int ps = a.kv.page_size;
-  const bf16_t* kbase;
-  const bf16_t* vbase;
-  if (PAGED) {
-    kbase = (const bf16_t*)a.kv.pool_k + g * D;
-    vbase = (const bf16_t*)a.kv.pool_v + (long long)g * D * ps;
-  } else {
-    kbase = (const bf16_t*)a.kv.prefix_k + (long long)b * a.kv.P * pstride + g * D;
-    vbase = (const bf16_t*)a.kv.prefix_v + ((long long)b * a.Hkv + g) * D * a.kv.VP;
-  }
-  const int* pages = PAGED ? a.rows.pages + (long long)r0 * a.rows.max_pages : nullptr;
+  // this (prompt, KV head): K rows [P][D]; V in 64-position blocks [VP/64][D][64]
+  const long long bg = (long long)b * a.Hkv + g;
+  const bf16_t* kbase = (const bf16_t*)a.kv.prefix_k + bg * a.kv.P * D;
+  const bf16_t* vbase = (const bf16_t*)a.kv.prefix_v + bg * a.kv.VP * D;
   const float scale = rsqrtf(float(D)) * kLog2e;
 
-  float m = -INFINITY, lsum = 0.f;
-  f32x4 o[8];
+  float m[NQ], lsum[NQ];
+  f32x4 o[8][NQ];
 #pragma unroll
-  for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int nt = 0; nt < NQ; ++nt) {
+    m[nt] = -INFINITY;
+    lsum[nt] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) o[dt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
 
-  constexpr int NSET = 1;  // tile sets in registers (one tile in flight while one is consumed)
-  u32x4 kreg[NSET][KSEG], vreg[NSET][VSEG];
-  auto load_tile = [&](int t0, int set) {
+  // Register staging of the next tile.  Nothing reads these registers before
+  // store_tile, so the loads stay in flight through a whole tile of compute;
+  // zeroing of V past the range (whose cache contents are arbitrary) is done
+  // at the store.
+  constexpr int KSEG = TP * 16 / NT, VSEG = D * (TP / 8) / NT;  // 16-byte segments per thread
+  u32x4 kreg[KSEG], vreg[VSEG];
+  int vt0 = 0;
+  auto load_tile = [&](int t0) {
+    vt0 = t0;
 #pragma unroll
     for (int i = 0; i < KSEG; ++i) {
       const int seg = threadIdx.x + i * NT;
-      const int pos = t0 + (seg >> 4), pc = (seg & 15) * 8;
-      u32x4 kk = {0u, 0u, 0u, 0u};
-      if (pos < hi) {
-        const long long ro = PAGED ? ((long long)pages[pos / ps] * ps + pos % ps) * pstride : (long long)pos * pstride;
-        kk = *(const u32x4*)(kbase + ro + pc);
-      }
-      kreg[set][i] = kk;
+      const int pos = t0 + (seg >> 4);
+      kreg[i] = pos < hi ? *(const u32x4*)(kbase + (long long)pos * D + (seg & 15) * 8) : u32x4{0u, 0u, 0u, 0u};
     }
 #pragma unroll
     for (int i = 0; i < VSEG; ++i) {
       const int seg = threadIdx.x + i * NT;
       const int d = seg >> 3, p0 = t0 + (seg & 7) * 8;
-      const int nv = hi - p0;
-      u32x4 vv = {0u, 0u, 0u, 0u};
-      if (nv > 0) {
-        const long long vo = PAGED ? ((long long)pages[p0 / ps] * a.Hkv * D + d) * ps + p0 % ps
-                                   : (long long)d * a.kv.VP + p0;
-        vv = *(const u32x4*)(vbase + vo);
-        if (nv < 8) {  // positions past the range read as 0
-#pragma unroll
-          for (int w = 0; w < 4; ++w) {
-            if (2 * w >= nv) vv[w] = 0u;
-            else if (2 * w + 1 >= nv) vv[w] &= 0xFFFFu;
-          }
-        }
-      }
-      vreg[set][i] = vv;
+      vreg[i] = p0 < hi ? *(const u32x4*)(vbase + ((long long)(t0 / TP) * D + d) * TP + (seg & 7) * 8)
+                        : u32x4{0u, 0u, 0u, 0u};
     }
   };
-
-  auto consume = [&](int t0, int set) {
-    __syncthreads();
+  auto store_tile = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < KSEG; ++i) {
       const int seg = threadIdx.x + i * NT;
-      *(u32x4*)&ks_lds[seg >> 4][(seg & 15) * 8] = kreg[set][i];
+      const int row = seg >> 4;
+      *(u32x4*)&k_lds[buf][row * D + (((seg & 15) ^ kswz(row)) * 8)] = kreg[i];
     }
 #pragma unroll
     for (int i = 0; i < VSEG; ++i) {
       const int seg = threadIdx.x + i * NT;
-      *(u32x4*)&vt_lds[seg >> 3][(seg & 7) * 8] = vreg[set][i];
-    }
-    if (t0 + NSET * TP < hi) load_tile(t0 + NSET * TP, set);
-    __syncthreads();
-    if (!wave_active) return;
-    // S^T = K Q^T: 4 position blocks of 16; lane holds positions 16*mt + 4*grp + i
-    f32x4 sc[4];
+      const int nv = hi - (vt0 + (seg & 7) * 8);  // valid positions of this segment
+      u32x4 vv = vreg[i];
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
-      sc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int w = 0; w < 4; ++w) vv[w] &= nv >= 2 * w + 2 ? 0xFFFFFFFFu : (nv == 2 * w + 1 ? 0xFFFFu : 0u);
+      *(u32x4*)&v_lds[buf][seg >> 3][(seg & 7) * 8] = vv;
+    }
+  };
+
+  // The tile loop works on 32-position halves.  Scores of half hh of the tile
+  // in buffer buf: sc[e][nt][i] is position hh*32 + grp*8 + e*4 + i.
+  auto k_frag = [&](int buf, int hh, int e, int ks) -> u32x4 {
+    const int row = k_gather_row(hh, e, l16);
+    return *(const u32x4*)&k_lds[buf][row * D + (((ks * 4 + grp) ^ kswz(row)) * 8)];
+  };
+  // V^T fragment: lane (l16, grp) reads row dt*16 + l16 at positions hh*32 + grp*8 + {0..7}
+  auto v_frag = [&](int buf, int dt, int hh) -> u32x4 {
+    return *(const u32x4*)&v_lds[buf][dt * 16 + l16][hh * 32 + grp * 8];
+  };
+  auto scores = [&](int buf, int hh, f32x4 (&sc)[2][NQ]) {
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+#pragma unroll
+      for (int nt = 0; nt < NQ; ++nt) sc[e][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
-        const u32x4 ka = *(const u32x4*)&ks_lds[mt * 16 + l16][ks * 32 + grp * 8];
-        sc[mt] = mfma16x16x32(ka, qf[ks], sc[mt]);
-      }
-    }
-    float tmax = -INFINITY;
-    const bool full = t0 + TP <= my_end;
+        const u32x4 ka = k_frag(buf, hh, e, ks);
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float val = sc[mt][i] * scale;
-        if (!full && t0 + mt * 16 + grp * 4 + i >= my_end) val = -INFINITY;
-        sc[mt][i] = val;
-        tmax = fmaxf(tmax, val);
-      }
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    const float mnew = fmaxf(m, tmax);
-    // a query with nothing visible yet (only possible past a causal end) keeps
-    // m = -inf: its probabilities are 0 and its state is left unscaled
-    const bool none = mnew == -INFINITY;
-    const float alpha = none ? 1.f : exp2f(m - mnew);
-    const float msub = none ? 0.f : mnew;
-    m = mnew;
-    float ps_ = 0.f;
-    u32x4 pb[2];
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      float p[8];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        p[i] = exp2f(sc[2 * h][i] - msub);
-        p[4 + i] = exp2f(sc[2 * h + 1][i] - msub);
-      }
-#pragma unroll
-      for (int i = 0; i < 8; ++i) ps_ += p[i];
-      pb[h] = u32x4{pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]), pack2(p[6], p[7])};
-    }
-    lsum = lsum * alpha + ps_;
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt) {
-      o[dt] *= alpha;
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const bf16_t* vr = &vt_lds[dt * 16 + l16][h * 32 + grp * 4];
-        const u32x2 a0 = *(const u32x2*)vr;
-        const u32x2 a1 = *(const u32x2*)(vr + 16);
-        o[dt] = mfma16x16x32(u32x4{a0.x, a0.y, a1.x, a1.y}, pb[h], o[dt]);
+        for (int nt = 0; nt < NQ; ++nt) sc[e][nt] = mfma16x16x32(ka, qf[nt][ks], sc[e][nt]);
       }
     }
   };
 
+  // Masking and the exponent reference of a half starting at position p0.
+  // Positions past a query vector's end are masked (skipped when the half is
+  // visible to every query vector of the wave).  Lazy rescaling: the
+  // reference m of a query vector only moves when some score exceeds it by
+  // more than kLazy, so probabilities stay below 2^kLazy and the accumulators
+  // are rescaled on few halves.  The common path needs no cross-lane
+  // reduction: each lane tests its own scores, and only when some lane of the
+  // wave fails are the maxima reduced over the four lane groups that share a
+  // query vector.
+  auto prepare = [&](int p0, f32x4 (&sc)[2][NQ]) {
+    bool full = true;
 #pragma unroll
-  for (int k = 0; k < NSET; ++k)
-    if (lo + k * TP < hi) load_tile(lo + k * TP, k);
-  for (int t0 = lo; t0 < hi; t0 += NSET * TP) {
+    for (int nt = 0; nt < NQ; ++nt) full &= p0 + 32 <= vend[nt];
+    if (!__all(full)) {
 #pragma unroll
-    for (int k = 0; k < NSET; ++k)
-      if (t0 + k * TP < hi) consume(t0 + k * TP, k);
+      for (int nt = 0; nt < NQ; ++nt)
+#pragma unroll
+        for (int e = 0; e < 2; ++e)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (p0 + grp * 8 + e * 4 + i >= vend[nt]) sc[e][nt][i] = -INFINITY;
+    }
+    float lmax[NQ];
+    bool grow = false;
+#pragma unroll
+    for (int nt = 0; nt < NQ; ++nt) {
+      const float x = fmaxf(fmaxf(fmaxf(sc[0][nt][0], sc[0][nt][1]), fmaxf(sc[0][nt][2], sc[0][nt][3])),
+                            fmaxf(fmaxf(sc[1][nt][0], sc[1][nt][1]), fmaxf(sc[1][nt][2], sc[1][nt][3])));
+      lmax[nt] = x * scale;
+      grow |= lmax[nt] > m[nt] + kLazy;
+    }
+    if (__any(grow)) {
+#pragma unroll
+      for (int nt = 0; nt < NQ; ++nt) {
+        float x = lmax[nt];
+        x = fmaxf(x, __shfl_xor(x, 16, 64));
+        x = fmaxf(x, __shfl_xor(x, 32, 64));
+        if (x > m[nt]) {
+          const float alpha = exp2_raw(m[nt] - x);  // 0 on the first visible half
+          lsum[nt] *= alpha;
+#pragma unroll
+          for (int dt = 0; dt < 8; ++dt) o[dt][nt] *= alpha;
+          m[nt] = x;
+        }
+      }
+    }
+  };
+
+  // One straight-line stream per half: the scores of the following half
+  // (buffer kb, half kh, into nxt), the exponentials of this half (cur)
+  // interleaved with them, then this half's P V product (buffer vb, half vh).
+  // 16 fragment reads go through a 3-slot register ring, NQ MFMAs each.  After
+  // the last half kb holds stale data and nxt is simply not used.
+  auto stream = [&](int kb, int kh, int vb, int vh, f32x4 (&cur)[2][NQ], f32x4 (&nxt)[2][NQ]) {
+    float msub[NQ];
+#pragma unroll
+    for (int nt = 0; nt < NQ; ++nt) msub[nt] = m[nt] == -INFINITY ? INFINITY : m[nt];  // nothing visible: p = 0
+    auto frag = [&](int f) -> u32x4 { return f < 8 ? k_frag(kb, kh, f >> 2, f & 3) : v_frag(vb, f - 8, vh); };
+    u32x4 ring[3];
+    ring[0] = frag(0);
+    ring[1] = frag(1);
+    float ps[NQ], plo[NQ];
+    uint32_t pw[NQ][4];  // packed probabilities, word 2e + (i >> 1)
+#pragma unroll
+    for (int nt = 0; nt < NQ; ++nt) ps[nt] = 0.f;
+#pragma unroll
+    for (int f = 0; f < 16; ++f) {
+      if (f + 2 < 16) ring[(f + 2) % 3] = frag(f + 2);
+      if (f < 8) {
+        const int e = f >> 2, ks = f & 3;
+        if (ks == 0) {
+#pragma unroll
+          for (int nt = 0; nt < NQ; ++nt) nxt[e][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int nt = 0; nt < NQ; ++nt) nxt[e][nt] = mfma16x16x32(ring[f % 3], qf[nt][ks], nxt[e][nt]);
+        // step f handles value i = f & 3 of block e = f >> 2; pairs are packed
+        // to bf16 as soon as both halves exist
+#pragma unroll
+        for (int nt = 0; nt < NQ; ++nt) {
+          const float x = exp2_raw(fmaf(cur[e][nt][ks], scale, -msub[nt]));
+          ps[nt] += x;
+          if (ks & 1) pw[nt][e * 2 + (ks >> 1)] = pack2(plo[nt], x);
+          else plo[nt] = x;
+        }
+      } else {
+        const int dt = f - 8;
+#pragma unroll
+        for (int nt = 0; nt < NQ; ++nt)
+          o[dt][nt] = mfma16x16x32(ring[f % 3], u32x4{pw[nt][0], pw[nt][1], pw[nt][2], pw[nt][3]}, o[dt][nt]);
+      }
+    }
+#pragma unroll
+    for (int nt = 0; nt < NQ; ++nt) lsum[nt] += ps[nt];
+  };
+
+  const int ntile = hi > lo ? (hi - lo + TP - 1) / TP : 0;
+  // The loop is reached only through the prologue, whose first store waits for
+  // every earlier load (the Q fragments included), so no wait for them is
+  // needed inside the loop.
+  if (ntile > 0) {
+    load_tile(lo);
+    store_tile(0);
+    if (ntile > 1) load_tile(lo + TP);
+    __syncthreads();
+    f32x4 sa[2][NQ], sb[2][NQ];
+    if (wave_active) scores(0, 0, sa);
+    for (int t = 0; t < ntile; ++t) {
+      const int t0 = lo + t * TP, cb = t % NB, nb = (t + 1) % NB;
+      if (t + 1 < ntile) {  // publish tile t+1
+        store_tile(nb);
+        if (t + 2 < ntile) load_tile(t0 + 2 * TP);
+      }
+      __syncthreads();
+      if (wave_active) {
+        prepare(t0, sa);
+        stream(cb, 1, cb, 0, sa, sb);
+        prepare(t0 + 32, sb);
+        stream(nb, 0, cb, 1, sb, sa);
+      }
+    }
   }
 
-  float lt = lsum + __shfl_xor(lsum, 16, 64);
-  lt += __shfl_xor(lt, 32, 64);
-  if (vok) {
-    const long long idx = ((long long)part * a.rows.R + row) * a.Hq + head;
-    float* po = a.part_o + idx * D;
-    const float inv = lt > 0.f ? 1.0f / lt : 0.f;
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt)
+  for (int nt = 0; nt < NQ; ++nt) {
+    float lt = lsum[nt] + __shfl_xor(lsum[nt], 16, 64);
+    lt += __shfl_xor(lt, 32, 64);
+    if (vok[nt]) {
+      const long long idx = ((long long)s * a.rows.R + vrow[nt]) * a.Hq + vhead[nt];
+      float* po = a.part_o + idx * D;
+      const float inv = lt > 0.f ? 1.0f / lt : 0.f;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) po[dt * 16 + grp * 4 + i] = o[dt][i] * inv;
-    if (grp == 0) a.part_lse[idx] = lt > 0.f ? (m + __log2f(lt)) * kLn2 : -INFINITY;
+      for (int dt = 0; dt < 8; ++dt) *(f32x4*)(po + dt * 16 + grp * 4) = o[dt][nt] * inv;
+      if (grp == 0) a.part_lse[idx] = lt > 0.f ? (m[nt] + __log2f(lt)) * kLn2 : -INFINITY;
+    }
   }
 }
 
@@ -253,14 +341,16 @@ __global__ __launch_bounds__(256) void attn_vec_kernel(AttnArgs a) {
     qs[i / D][i % D] = load_f((const T*)a.q + ((long long)r * a.Hq + g * G) * D + i);
   __syncthreads();
 
+  const long long bg = (long long)a.rows.prompt[r] * a.Hkv + g;
   auto k_row = [&](int pos) -> const T* {
-    if (PREFIX) return (const T*)a.kv.prefix_k + ((long long)a.rows.prompt[r] * a.kv.P + pos) * pstride + g * D;
-    const int page = a.rows.pages[(long long)r * a.rows.max_pages + pos / a.kv.page_size];
-    return (const T*)a.kv.pool_k + ((long long)page * a.kv.page_size + pos % a.kv.page_size) * pstride + g * D;
+    if (PREFIX) return (const T*)a.kv.prefix_k + (bg * a.kv.P + pos) * D;
+    const int ps = a.kv.page_size;
+    const int page = a.rows.pages[(long long)r * a.rows.max_pages + pos / ps];
+    return (const T*)a.kv.pool_k + (((long long)page * a.Hkv + g) * ps + pos % ps) * D;
   };
   auto v_at = [&](int pos, int d) -> float {
     if (PREFIX)
-      return load_f((const T*)a.kv.prefix_v + (((long long)a.rows.prompt[r] * a.Hkv + g) * D + d) * a.kv.VP + pos);
+      return load_f((const T*)a.kv.prefix_v + ((bg * (a.kv.VP / 64) + pos / 64) * D + d) * 64 + pos % 64);
     const int ps = a.kv.page_size;
     const int page = a.rows.pages[(long long)r * a.rows.max_pages + pos / ps];
     return load_f((const T*)a.kv.pool_v + (((long long)page * a.Hkv + g) * D + d) * ps + pos % ps);
@@ -374,7 +464,7 @@ __global__ __launch_bounds__(256) void attn_tail_combine_kernel(AttnArgs a, T* o
     float dot[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     if (j < n) {
       const int pos = c0 + j;
-      const T* kr = (const T*)a.kv.pool_k + ((long long)pages[pos / ps] * ps + pos % ps) * pstride + g * D;
+      const T* kr = (const T*)a.kv.pool_k + (((long long)pages[pos / ps] * a.Hkv + g) * ps + pos % ps) * D;
       for (int e0 = 0; e0 < D; e0 += 8) {
         float kv[8];
         load8(kr + e0, kv);
@@ -474,39 +564,202 @@ __global__ __launch_bounds__(256) void attn_tail_combine_kernel(AttnArgs a, T* o
   }
 }
 
-template <typename T>
-__global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a, T* out) {
-  const int r = blockIdx.x, h = blockIdx.y;
-  const int D = a.D;
+// Tail attention fused with the merge, bf16 caches: one workgroup of four
+// waves per (row, KV head).  Each wave attends 32-position tiles of the row's
+// paged tail (tiles wave, wave+4, ...) with MFMA: the G query heads of the KV
+// head form one 16-column tile, K and V^T fragments are loaded straight from
+// the pages (K rows in the gathered order of the prefix kernel, so every lane
+// ends up with eight consecutive positions).  The four waves' tail states are
+// merged through LDS, then wave h merges query head h's prefix-split partials
+// with its tail in log-sum-exp form (split order fixed) and writes the output.
+constexpr int kMergeMaxSplits = 64;
+
+__global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t* out) {
+  constexpr int D = 128, TT = 32;
+  const int r = blockIdx.x, g = blockIdx.y;
+  const int G = a.Hq / a.Hkv;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int l16 = lane & 15, grp = lane >> 4;
   const long long R = a.rows.R;
-  float m = -INFINITY;
-  for (int p = 0; p < a.nparts; ++p) m = fmaxf(m, a.part_lse[(p * R + r) * a.Hq + h]);
-  for (int d = threadIdx.x; d < D; d += blockDim.x) {
-    float num = 0.f, den = 0.f;
-    for (int p = 0; p < a.nparts; ++p) {
-      const float l = a.part_lse[(p * R + r) * a.Hq + h];
-      if (l == -INFINITY) continue;
-      const float w = __expf(l - m);
-      num += w * a.part_o[((p * R + r) * a.Hq + h) * D + d];
-      den += w;
-    }
-    store_f(out + ((long long)r * a.Hq + h) * D + d, den > 0.f ? num / den : 0.f);
+  const int ps = a.kv.page_size;
+  const float scale = rsqrtf(float(D)) * kLog2e;
+
+  __shared__ float w_m[4][16], w_l[4][16];
+  __shared__ __attribute__((aligned(16))) float w_o[4][16][D + 4];  // [wave][query][dim]
+
+  // The prefix-split partials and log-sum-exps do not depend on the tail:
+  // request those of this wave's first head now so their latency overlaps the
+  // tail attention (splits beyond kPrefetch are loaded in the merge).
+  const int S = a.splits;
+  constexpr int kPrefetch = 16;
+  const long long pstep = R * a.Hq * D;
+  float2 pre[kPrefetch];
+  float pre_lse = -INFINITY;
+  if (wave < G) {
+    const int head = g * G + wave;
+    const float* po = a.part_o + ((long long)r * a.Hq + head) * D + 2 * lane;
+#pragma unroll
+    for (int k = 0; k < kPrefetch; ++k) pre[k] = k < S ? *(const float2*)(po + k * pstep) : float2{0.f, 0.f};
+    if (lane < S) pre_lse = a.part_lse[((long long)lane * R + r) * a.Hq + head];
   }
+
+  u32x4 qf[4];
+  {
+    const bool ok = l16 < G;
+    const bf16_t* qp = (const bf16_t*)a.q + ((long long)r * a.Hq + g * G + (ok ? l16 : 0)) * D + grp * 8;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) qf[ks] = ok ? *(const u32x4*)(qp + ks * 32) : u32x4{0u, 0u, 0u, 0u};
+  }
+  float m = -INFINITY, lsum = 0.f;
+  f32x4 o[8];
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int n = a.tail_len;
+  const int* pages = n > 0 ? a.rows.pages + (long long)r * a.rows.max_pages : nullptr;
+  for (int tb = wave * TT; tb < n; tb += 4 * TT) {
+    u32x4 ka[2][4], va[8];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int pos = tb + k_gather_row(0, e, l16);
+      const bool ok = pos < n;
+      const int pp = ok ? pos : 0;
+      const bf16_t* kr = (const bf16_t*)a.kv.pool_k +
+                         (((long long)pages[pp / ps] * a.Hkv + g) * ps + pp % ps) * D + grp * 8;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) ka[e][ks] = ok ? *(const u32x4*)(kr + ks * 32) : u32x4{0u, 0u, 0u, 0u};
+    }
+    const int p0 = tb + grp * 8;  // this lane's eight positions p0 .. p0+7 (one page: ps % 8 == 0)
+    const int nv = n - p0;
+    {
+      const int pp = nv > 0 ? p0 : 0;
+      const bf16_t* vr = (const bf16_t*)a.kv.pool_v +
+                         (((long long)pages[pp / ps] * a.Hkv + g) * D + l16) * ps + pp % ps;
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) va[dt] = nv > 0 ? *(const u32x4*)(vr + (long long)dt * 16 * ps) : u32x4{0u, 0u, 0u, 0u};
+    }
+    f32x4 sc[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      sc[e] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) sc[e] = mfma16x16x32(ka[e][ks], qf[ks], sc[e]);
+    }
+    float x = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (p0 + e * 4 + i >= n) sc[e][i] = -INFINITY;
+        x = fmaxf(x, sc[e][i]);
+      }
+    x = fmaxf(x, __shfl_xor(x, 16, 64));
+    x = fmaxf(x, __shfl_xor(x, 32, 64));
+    x *= scale;
+    if (x > m) {
+      const float alpha = exp2_raw(m - x);
+      lsum *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) o[dt] *= alpha;
+      m = x;
+    }
+    const float msub = m == -INFINITY ? INFINITY : m;
+    float p[8];
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) p[e * 4 + i] = exp2_raw(fmaf(sc[e][i], scale, -msub));
+#pragma unroll
+    for (int i = 0; i < 8; ++i) lsum += p[i];
+    const u32x4 pb = {pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]), pack2(p[6], p[7])};
+    if (nv < 8) {  // V past the tail end is arbitrary (unwritten page slots): zero it
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          if (2 * w >= nv) va[dt][w] = 0u;
+          else if (2 * w + 1 >= nv) va[dt][w] &= 0xFFFFu;
+        }
+    }
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) o[dt] = mfma16x16x32(va[dt], pb, o[dt]);
+  }
+  // per-wave tail states -> LDS (query q = l16, dims dt*16 + grp*4 + i)
+  lsum += __shfl_xor(lsum, 16, 64);
+  lsum += __shfl_xor(lsum, 32, 64);
+  if (grp == 0) {
+    w_m[wave][l16] = m;
+    w_l[wave][l16] = lsum;
+  }
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) *(f32x4*)&w_o[wave][l16][dt * 16 + grp * 4] = o[dt];
+  __syncthreads();
+
+  // merge: wave h handles query heads h, h+4, ...; lane holds dims 2*lane, 2*lane+1
+  auto finish = [&](int h, bool first) {
+    const int head = g * G + h;
+    // tail state of this head (exp2 domain) from the four waves
+    float tm = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) tm = fmaxf(tm, w_m[w][h]);
+    float tl = 0.f, to0 = 0.f, to1 = 0.f;
+    if (tm != -INFINITY) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float f = exp2_raw(w_m[w][h] - tm);
+        tl += f * w_l[w][h];
+        to0 += f * w_o[w][h][2 * lane];
+        to1 += f * w_o[w][h][2 * lane + 1];
+      }
+    }
+    const float tail_lse = tl > 0.f ? (tm + __log2f(tl)) * kLn2 : -INFINITY;
+    // split log-sum-exps: lane sp holds split sp's
+    const float ls = first ? pre_lse : (lane < S ? a.part_lse[((long long)lane * R + r) * a.Hq + head] : -INFINITY);
+    float mx = fmaxf(ls, tail_lse);
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+    const float w = ls == -INFINITY ? 0.f : __expf(ls - mx);
+    const float wt = tail_lse == -INFINITY ? 0.f : __expf(tail_lse - mx);
+    float den = w;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) den += __shfl_xor(den, off, 64);
+    den += wt;
+    const float inv = den > 0.f ? 1.f / den : 0.f;
+    const float ft = tl > 0.f ? wt * inv / tl : 0.f;  // applied to the unnormalised tail sum
+    float o0 = ft * to0, o1 = ft * to1;
+    const float* po = a.part_o + ((long long)r * a.Hq + head) * D + 2 * lane;
+    // weight of split sp sits in lane sp; fixed split order
+#pragma unroll
+    for (int k = 0; k < kPrefetch; ++k) {
+      if (k < S) {
+        const float2 v = first ? pre[k] : *(const float2*)(po + k * pstep);
+        const float wk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), k)) * inv;
+        o0 += wk * v.x;
+        o1 += wk * v.y;
+      }
+    }
+#pragma unroll
+    for (int k = kPrefetch; k < kMergeMaxSplits; ++k) {
+      if (k < S) {
+        const float2 v = *(const float2*)(po + k * pstep);
+        const float wk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), k)) * inv;
+        o0 += wk * v.x;
+        o1 += wk * v.y;
+      }
+    }
+    *(uint32_t*)(out + ((long long)r * a.Hq + head) * D + 2 * lane) = pack_bf16x2(o0, o1);
+  };
+  // the first head of the wave uses the prefetched partials
+  if (wave < G) finish(wave, true);
+  for (int h = wave + 4; h < G; h += 4) finish(h, false);
 }
 
 }  // namespace
 
-hipError_t attn_prefix_mfma_bf16(const AttnArgs& a, hipStream_t s) {
-  if (a.D != 128 || a.Hq / a.Hkv > 64 || a.split_len % 64 || a.kv.VP % 16) return hipErrorInvalidValue;
+hipError_t attn_prefix_bf16(const AttnArgs& a, hipStream_t s) {
+  if (a.D != 128 || a.Hq / a.Hkv > 256 || a.split_len % 64 || a.kv.VP % 64) return hipErrorInvalidValue;
   if (a.splits <= 0 || a.nrblocks <= 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_mfma_kernel<4, false>), dim3(a.splits, a.Hkv, a.nrblocks), dim3(256), 0, s, a);
-  return hipGetLastError();
-}
-
-hipError_t attn_tail_mfma_bf16(const AttnArgs& a, hipStream_t s) {
-  if (a.D != 128 || a.Hq / a.Hkv > 16 || a.tail_chunk % 64 || a.kv.page_size % 16) return hipErrorInvalidValue;
-  if (a.tail_chunks <= 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_mfma_kernel<1, true>), dim3(a.tail_chunks, a.Hkv, a.rows.R), dim3(64), 0, s, a);
+  hipLaunchKernelGGL((attn_prefix_kernel<RGD_ATTN_NW, 16 / RGD_ATTN_NW>), dim3(a.splits, a.Hkv, a.nrblocks),
+                     dim3(RGD_ATTN_NW * 64), 0, s, a);
   return hipGetLastError();
 }
 
@@ -519,14 +772,6 @@ hipError_t attn_prefix_vec(const AttnArgs& a, hipStream_t s) {
 }
 
 template <typename T>
-hipError_t attn_tail_vec(const AttnArgs& a, hipStream_t s) {
-  if (a.D > 256 || a.Hq / a.Hkv > 8 || a.tail_chunk > kChunk) return hipErrorInvalidValue;
-  if (a.tail_chunks <= 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_vec_kernel<T, false>), dim3(a.tail_chunks, a.Hkv, a.rows.R), dim3(256), 0, s, a);
-  return hipGetLastError();
-}
-
-template <typename T>
 hipError_t attn_tail_combine(const AttnArgs& a, T* out, hipStream_t s) {
   if (a.D > 128 || a.D < 8 || 256 % a.D || a.Hq / a.Hkv > 8 || (a.tail_len > 0 && !a.rows.pages) ||
       (a.tail_len > 0 && a.kv.page_size % 8) || a.splits > kMaxSplits)
@@ -535,19 +780,16 @@ hipError_t attn_tail_combine(const AttnArgs& a, T* out, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <typename T>
-hipError_t attn_combine(const AttnArgs& a, T* out, hipStream_t s) {
-  hipLaunchKernelGGL(attn_combine_kernel<T>, dim3(a.rows.R, a.Hq), dim3(128), 0, s, a, out);
+hipError_t attn_tail_merge_bf16(const AttnArgs& a, bf16_t* out, hipStream_t s) {
+  if (a.D != 128 || a.Hq / a.Hkv > 16 || a.splits > kMergeMaxSplits || a.splits < 1 ||
+      (a.tail_len > 0 && (!a.rows.pages || a.kv.page_size % 8)))
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(attn_tail_merge_kernel, dim3(a.rows.R, a.Hkv), dim3(256), 0, s, a, out);
   return hipGetLastError();
 }
 
 template hipError_t attn_prefix_vec<float>(const AttnArgs&, hipStream_t);
 template hipError_t attn_prefix_vec<bf16_t>(const AttnArgs&, hipStream_t);
-template hipError_t attn_tail_vec<float>(const AttnArgs&, hipStream_t);
-template hipError_t attn_tail_vec<bf16_t>(const AttnArgs&, hipStream_t);
-template hipError_t attn_combine<float>(const AttnArgs&, float*, hipStream_t);
 template hipError_t attn_tail_combine<float>(const AttnArgs&, float*, hipStream_t);
-template hipError_t attn_tail_combine<bf16_t>(const AttnArgs&, bf16_t*, hipStream_t);
-template hipError_t attn_combine<bf16_t>(const AttnArgs&, bf16_t*, hipStream_t);
 
 }  // namespace rgd

@@ -107,21 +107,26 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* parts, int n
     return v;
   };
   const int b = rows.prompt[r];
-  long long kv_off;  // K row of this position
+  // destinations: K of head h at kd + h * kstride; V of head h, dim d at
+  // vd + h * vhstride + d * vdstride
   T* kd;
-  T* vd;             // V of head h, dim d at vd[(h * D + d) * vstride]
-  long long vstride;
+  T* vd;
+  long long kstride, vhstride, vdstride;
   if (rows.prefill) {
-    kv_off = ((long long)b * kv.P + pos) * Hkv * D;
-    kd = (T*)kv.prefix_k;
-    vd = (T*)kv.prefix_v + (long long)b * Hkv * D * kv.VP + pos;
-    vstride = kv.VP;
+    kd = (T*)kv.prefix_k + ((long long)b * Hkv * kv.P + pos) * D;
+    kstride = (long long)kv.P * D;
+    vd = (T*)kv.prefix_v + ((long long)b * Hkv * (kv.VP / 64) + pos / 64) * D * 64 + pos % 64;
+    vhstride = (long long)kv.VP * D;
+    vdstride = 64;
   } else {
-    const int page = rows.pages[(long long)r * rows.max_pages + rows.t / kv.page_size];
-    kv_off = ((long long)page * kv.page_size + rows.t % kv.page_size) * Hkv * D;
-    kd = (T*)kv.pool_k;
-    vd = (T*)kv.pool_v + (long long)page * Hkv * D * kv.page_size + rows.t % kv.page_size;
-    vstride = kv.page_size;
+    const int ps = kv.page_size;
+    const int page = rows.pages[(long long)r * rows.max_pages + rows.t / ps];
+    const int slot = rows.t % ps;
+    kd = (T*)kv.pool_k + ((long long)page * Hkv * ps + slot) * D;
+    kstride = (long long)ps * D;
+    vd = (T*)kv.pool_v + (long long)page * Hkv * D * ps + slot;
+    vhstride = (long long)D * ps;
+    vdstride = ps;
   }
   const int nh = h1 - h0;
   for (int i = threadIdx.x; i < nh * half; i += 256) {
@@ -131,13 +136,13 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* parts, int n
       const float x1 = col(base + j), x2 = col(base + j + half);
       const float y1 = x1 * cs[j] - x2 * sn[j];
       const float y2 = x2 * cs[j] + x1 * sn[j];
-      T* dst = h < Hq ? q + ((long long)r * Hq + h) * D : kd + kv_off + (long long)(h - Hq) * D;
+      T* dst = h < Hq ? q + ((long long)r * Hq + h) * D : kd + (long long)(h - Hq) * kstride;
       store_f(dst + j, y1);
       store_f(dst + j + half, y2);
     } else {             // v: dims j and j + D/2 of head h - Hq - Hkv
       const int hv = h - Hq - Hkv;
-      store_f(vd + ((long long)hv * D + j) * vstride, col(base + j));
-      store_f(vd + ((long long)hv * D + j + half) * vstride, col(base + j + half));
+      store_f(vd + hv * vhstride + (long long)j * vdstride, col(base + j));
+      store_f(vd + hv * vhstride + (long long)(j + half) * vdstride, col(base + j + half));
     }
   }
 }

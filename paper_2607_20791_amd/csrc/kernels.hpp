@@ -49,19 +49,20 @@ struct Rows {
   int prefill;          // 1: K/V go to the prefix at base_pos; no tail
 };
 
-// K is stored position-major and V head-dim-major (transposed per KV head) so
-// that both MFMA operand tiles of attention are plain row copies.
+// Caches are KV-head-major so that a tile of consecutive positions of one head
+// is one contiguous run; V is stored transposed (head dim before position) in
+// blocks of 64 positions so that attention's V^T operand tile is a plain copy.
 struct KVLayout {
-  void* prefix_k;  // this layer: [B][P][Hkv][D]
-  void* prefix_v;  // this layer: [B][Hkv][D][VP]
-  void* pool_k;    // this layer: [pages][page_size][Hkv][D]
+  void* prefix_k;  // this layer: [B][Hkv][P][D]
+  void* prefix_v;  // this layer: [B][Hkv][VP/64][D][64]
+  void* pool_k;    // this layer: [pages][Hkv][page_size][D]
   void* pool_v;    // this layer: [pages][Hkv][D][page_size]
   int P;           // prefix capacity per prompt
-  int VP;          // V row stride: P rounded up to a multiple of 16
+  int VP;          // P rounded up to a multiple of 64
   int page_size;
 };
 
-inline int v_stride(int P) { return (P + 15) / 16 * 16; }
+inline int v_stride(int P) { return (P + 63) / 64 * 64; }
 
 // ------------------------------------------------------------ elementwise ----
 // x[r] = E[tok[r * tok_stride]] (ids clamped to [0, V)); xn[r] = rmsnorm(x[r]) * g
@@ -94,13 +95,15 @@ struct AttnArgs {
   int tail_len;             // visible tail positions (decode), 0 for prefill
   int tail_chunk; int tail_chunks;    // part index splits .. splits+tail_chunks-1
 };
-hipError_t attn_prefix_mfma_bf16(const AttnArgs& a, hipStream_t s);
-hipError_t attn_tail_mfma_bf16(const AttnArgs& a, hipStream_t s);
+// bf16, head_dim 128: prefix-split partials 0 .. splits-1 on MFMA, row blocks
+// of up to 256 query vectors of one prompt
+hipError_t attn_prefix_bf16(const AttnArgs& a, hipStream_t s);
+// bf16, head_dim 128, G <= 16: each row's paged tail on MFMA, merged with the
+// prefix-split partials into the final output
+hipError_t attn_tail_merge_bf16(const AttnArgs& a, bf16_t* out, hipStream_t s);
 template <typename T> hipError_t attn_prefix_vec(const AttnArgs& a, hipStream_t s);
-template <typename T> hipError_t attn_tail_vec(const AttnArgs& a, hipStream_t s);
-template <typename T> hipError_t attn_combine(const AttnArgs& a, T* out, hipStream_t s);
-// attends each row's tail (vector units) and merges it with the prefix-split
-// partials 0 .. splits-1 into the final output
+// fp32: attends each row's tail (vector units) and merges it with the
+// prefix-split partials 0 .. splits-1 into the final output
 template <typename T> hipError_t attn_tail_combine(const AttnArgs& a, T* out, hipStream_t s);
 
 // ---------------------------------------------------------------- sampler ----

@@ -221,9 +221,11 @@ struct HostRows {
   int maxplen = 0;
 };
 
+// Row blocks of one prompt for the shared-prefix attention kernel: up to 256
+// query vectors (rows x G query heads) per block.
 void build_blocks(const rgd_model* m, HostRows& h) {
   const int G = m->cfg.n_heads / m->cfg.n_kv_heads;
-  const int per = std::max(1, 64 / G);
+  const int per = std::max(1, (m->bf16 ? 256 : 64) / G);
   h.blocks.clear();
   h.maxplen = 0;
   const int R = (int)h.prompt.size();
@@ -292,7 +294,7 @@ int run_attention(rgd_model* m, const KVLayout& kvl, const Rows& rows, const Hos
   const int cap = (int)std::min<long long>(kMaxParts, (long long)kMaxParts * m->max_rows / std::max(R, 1));
   if (m->bf16) {
     int S = force_splits;
-    if (S <= 0) S = (int)cdiv(512, (long long)c.n_kv_heads * a.nrblocks);
+    if (S <= 0) S = (int)cdiv(256, (long long)c.n_kv_heads * a.nrblocks);
     S = (int)std::max<long long>(1, std::min<long long>(S, cdiv(std::max(h.maxplen, 1), 64)));
     S = std::min(S, cap - a.tail_chunks);
     a.split_len = (int)cdiv(cdiv(std::max(h.maxplen, 1), S), 64) * 64;
@@ -308,9 +310,9 @@ int run_attention(rgd_model* m, const KVLayout& kvl, const Rows& rows, const Hos
   if (m->bf16) {
     {
       TimeScope tp(m, RGD_TIMER_ATTN_PREFIX, s);
-      HIP_OK(attn_prefix_mfma_bf16(a, s));
+      HIP_OK(attn_prefix_bf16(a, s));
     }
-    HIP_OK(attn_tail_combine<bf16_t>(a, (bf16_t*)out, s));
+    HIP_OK(attn_tail_merge_bf16(a, (bf16_t*)out, s));
   } else {
     HIP_OK(attn_prefix_vec<float>(a, s));
     HIP_OK(attn_tail_combine<float>(a, (float*)out, s));
@@ -558,8 +560,8 @@ bool valid_dtype_shapes(const rgd_model_config& c, std::string& why) {
       why = "projection widths must be multiples of 64";
       return false;
     }
-    if (c.n_heads / c.n_kv_heads > 64) {
-      why = "at most 64 query heads per KV head";
+    if (c.n_heads / c.n_kv_heads > 16) {
+      why = "bf16 models support at most 16 query heads per KV head";
       return false;
     }
   } else if (c.dtype == RGD_DTYPE_F32) {

@@ -49,10 +49,11 @@ def alloc_kv(model: Model, w, max_prompts: int, max_prefix: int, n_pages: int,
              page_size: int = 16) -> KV:
     torch = _torch()
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
-    pre_k = (w.n_layers, max_prompts, max_prefix, w.n_kv_heads, w.head_dim)
-    pre_v = (w.n_layers, max_prompts, w.n_kv_heads, w.head_dim, v_stride(max_prefix))
-    pool_k = (w.n_layers, max(n_pages, 1), page_size, w.n_kv_heads, w.head_dim)
-    pool_v = (w.n_layers, max(n_pages, 1), w.n_kv_heads, w.head_dim, page_size)
+    H, D = w.n_kv_heads, w.head_dim
+    pre_k = (w.n_layers, max_prompts, H, max_prefix, D)
+    pre_v = (w.n_layers, max_prompts, H, v_stride(max_prefix) // 64, D, 64)
+    pool_k = (w.n_layers, max(n_pages, 1), H, page_size, D)
+    pool_v = (w.n_layers, max(n_pages, 1), H, D, page_size)
     pk = torch.zeros(pre_k, dtype=dt, device="cuda")
     pv = torch.zeros(pre_v, dtype=dt, device="cuda")
     qk = torch.zeros(pool_k, dtype=dt, device="cuda")
@@ -61,13 +62,30 @@ def alloc_kv(model: Model, w, max_prompts: int, max_prefix: int, n_pages: int,
 
 
 def v_stride(max_prefix: int) -> int:
-    """Row stride of the head-dim-major V cache: max_prefix rounded up to 16."""
-    return (max_prefix + 15) // 16 * 16
+    """Positions per prompt and head in the V cache: max_prefix rounded up to 64."""
+    return (max_prefix + 63) // 64 * 64
+
+
+def k_cache_layout(k: np.ndarray) -> np.ndarray:
+    """[B][P][Hkv][D] -> the K cache layout [B][Hkv][P][D]."""
+    return np.ascontiguousarray(k.transpose(0, 2, 1, 3))
+
+
+def v_cache_layout(v: np.ndarray, VP: int) -> np.ndarray:
+    """[B][P][Hkv][D] -> the V cache layout [B][Hkv][VP/64][D][64] (zero padded)."""
+    B, P, H, D = v.shape
+    out = np.zeros((B, H, VP // 64, D, 64), v.dtype)
+    vt = v.transpose(0, 2, 3, 1)                 # [B][H][D][P]
+    for blk in range((P + 63) // 64):
+        n = min(64, P - blk * 64)
+        out[:, :, blk, :, :n] = vt[:, :, :, blk * 64:blk * 64 + n]
+    return out
 
 
 def fill_prefix(kv: KV, layer: int, k: np.ndarray, v: np.ndarray):
-    """Writes caller-generated prefix K/V [B][P][Hkv][D] into positions [0, P)
-    (V goes to the head-dim-major layout)."""
+    """Writes caller-generated prefix K/V [B][P][Hkv][D] into positions [0, P)."""
     B, P = k.shape[:2]
-    kv.prefix_k[layer, :B, :P].copy_(to_device(k))
-    kv.prefix_v[layer, :B, :, :, :P].copy_(to_device(np.ascontiguousarray(v.transpose(0, 2, 3, 1))))
+    kv.prefix_k[layer, :B, :, :P].copy_(to_device(k_cache_layout(k)))
+    VP = kv.prefix_v.shape[2] * 64
+    vv = v_cache_layout(v, VP)
+    kv.prefix_v[layer, :B].copy_(to_device(vv))

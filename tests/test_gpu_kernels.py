@@ -79,13 +79,15 @@ def _attn_case(rgd, w, m, R_per_prompt, prompts, P, tail, plens=None, splits=0, 
     plen = np.full(R, P, np.int32) if plens is None else np.asarray(plens, np.int32)
     out = t.empty(R, Hq * D, dtype=t.bfloat16 if w.dtype == "bf16" else t.float32, device="cuda")
     dev = session.to_device
-    # V caches are head-dim-major: prefix [prompts][Hkv][D][VP], pages [page][Hkv][D][ps]
+    # cache layouts: prefix K [prompts][Hkv][P][D], V [prompts][Hkv][VP/64][D][64];
+    # pages K [page][Hkv][ps][D], V [page][Hkv][D][ps]
     VP = session.v_stride(P)
-    vp_t = np.zeros((prompts, Hkv, D, VP), vp.dtype)
-    vp_t[..., :P] = vp.transpose(0, 2, 3, 1)
-    pool_v_t = np.ascontiguousarray(pool_v.transpose(0, 2, 3, 1))
-    rgd.kernel_attention(m, dev(q), row_prompt, plen, dev(kp), dev(vp_t), prompts, P, dev(pool_k),
-                         dev(pool_v_t), ps, dev(perm), perm.shape[1], tail, out, splits=splits)
+    kp_c = session.k_cache_layout(kp)
+    vp_c = session.v_cache_layout(vp, VP)
+    pool_k_c = np.ascontiguousarray(pool_k.transpose(0, 2, 1, 3))
+    pool_v_c = np.ascontiguousarray(pool_v.transpose(0, 2, 3, 1))
+    rgd.kernel_attention(m, dev(q), row_prompt, plen, dev(kp_c), dev(vp_c), prompts, P, dev(pool_k_c),
+                         dev(pool_v_c), ps, dev(perm), perm.shape[1], tail, out, splits=splits)
     t.cuda.synchronize()
     got = (bf16_to_f64(out) if w.dtype == "bf16" else out.cpu().numpy()).reshape(R, Hq, D)
     W = om.widen
