@@ -30,6 +30,15 @@ DTYPE_F32, DTYPE_BF16 = 0, 1
 EVENT_INCOMPAT, EVENT_STOP, EVENT_MAXLEN = 0, 1, 2
 STATUS = {0: "OK", 1: "INVALID_ARG", 2: "OOM", 3: "HIP", 4: "UNSUPPORTED", 5: "NONFINITE", 6: "STATE"}
 
+# PyTorch ships its own HIP runtime (same soname as the system one).  Loading it
+# first makes librgd bind to that instance; loading librgd first would bring in
+# the system runtime and leave the process with two HIP/HSA runtimes, of which
+# the second sees no device.
+try:
+    import torch  # noqa: F401
+except ImportError:  # CPU-only use of the binding (export checks) needs no torch
+    pass
+
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with paper_2607_20791_amd/build.py "
                       "(there is no fallback path)")

@@ -129,7 +129,9 @@ struct rgd_model {
   int alloc(P** out, size_t bytes) {
     void* p = nullptr;
     hipError_t e = hipMalloc(&p, std::max<size_t>(bytes, 256));
-    if (e != hipSuccess) return fail(RGD_E_OOM, "workspace allocation of %zu bytes failed", bytes);
+    if (e != hipSuccess)
+      return fail(e == hipErrorOutOfMemory ? RGD_E_OOM : RGD_E_HIP, "workspace allocation of %zu bytes failed: %s",
+                  bytes, hipGetErrorString(e));
     allocs.push_back(p);
     *out = (P*)p;
     return RGD_OK;

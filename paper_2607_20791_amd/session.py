@@ -86,6 +86,6 @@ def fill_prefix(kv: KV, layer: int, k: np.ndarray, v: np.ndarray):
     """Writes caller-generated prefix K/V [B][P][Hkv][D] into positions [0, P)."""
     B, P = k.shape[:2]
     kv.prefix_k[layer, :B, :, :P].copy_(to_device(k_cache_layout(k)))
-    VP = kv.prefix_v.shape[2] * 64
+    VP = kv.prefix_v.shape[3] * 64  # [L][B][Hkv][VP/64][D][64]
     vv = v_cache_layout(v, VP)
     kv.prefix_v[layer, :B].copy_(to_device(vv))

@@ -13,6 +13,9 @@ pytestmark = pytest.mark.gpu
 # the kernel under test does not depend on them
 ATTN_BF16 = synth.scaled(synth.C2, name="attn-bf16", d_model=512, ffn=512, vocab=1024)
 ATTN_F32 = synth.scaled(synth.C0, name="attn-f32", vocab=1024)
+# 8 and 16 query heads per KV head (the tail merge loops over heads per wave)
+ATTN_G8 = synth.scaled(synth.C2, name="attn-g8", n_kv_heads=4, d_model=512, ffn=512, vocab=1024)
+ATTN_G16 = synth.scaled(synth.C2, name="attn-g16", n_kv_heads=2, d_model=512, ffn=512, vocab=1024)
 
 
 @pytest.fixture(scope="module")
@@ -121,6 +124,39 @@ def test_attention_bf16_causal_rows_and_forced_splits(rgd, mb):
     err1 = _attn_case(rgd, ATTN_BF16, mb, 4, 1, 4000, 20, splits=1, seed=6)
     err9 = _attn_case(rgd, ATTN_BF16, mb, 4, 1, 4000, 20, splits=9, seed=6)
     assert err1.max() <= 2e-2 and err9.max() <= 2e-2
+
+
+def test_attention_bf16_long_tail_and_many_splits(rgd, mb):
+    # tail of 300 positions: each wave of the merge kernel attends several tiles
+    err = _attn_case(rgd, ATTN_BF16, mb, 4, 1, 700, 300, seed=11)
+    assert err.max() <= 2e-2
+    # 33 prefix splits: more than the merge kernel prefetches
+    err = _attn_case(rgd, ATTN_BF16, mb, 4, 1, 8193, 5, splits=40, seed=12)
+    assert err.max() <= 2e-2
+
+
+@pytest.mark.parametrize("w", [ATTN_G8, ATTN_G16], ids=["G8", "G16"])
+def test_attention_bf16_wide_groups(rgd, w):
+    m = _model(rgd, w, max_rows=64)
+    for R, prompts, P, tail in [(32, 1, 1000, 40), (3, 2, 200, 7)]:
+        err = _attn_case(rgd, w, m, R, prompts, P, tail, seed=R + P)
+        assert err.max() <= 2e-2, (R, prompts, P, tail, err.max())
+
+
+def test_fill_prefix_round_trip(rgd, mb):
+    from paper_2607_20791_amd import session
+    t = torch()
+    w = ATTN_BF16
+    kv = session.alloc_kv(mb, w, max_prompts=2, max_prefix=100, n_pages=4)
+    g = np.random.default_rng(3)
+    k = synth.to_bf16_bits(g.normal(size=(2, 90, w.n_kv_heads, w.head_dim)).astype(np.float32))
+    v = synth.to_bf16_bits(g.normal(size=(2, 90, w.n_kv_heads, w.head_dim)).astype(np.float32))
+    session.fill_prefix(kv, 0, k, v)
+    t.cuda.synchronize()
+    pk = kv.prefix_k[0].view(t.int16).cpu().numpy().view(np.uint16)
+    pv = kv.prefix_v[0].view(t.int16).cpu().numpy().view(np.uint16)
+    assert np.array_equal(pk[:, :, :90], session.k_cache_layout(k))
+    assert np.array_equal(pv, session.v_cache_layout(v, session.v_stride(100)))
 
 
 @pytest.fixture(scope="module")
