@@ -56,12 +56,12 @@ __global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(float* x
     const float* pr = parts + (long long)r * d;
     for (int i = threadIdx.x * 4; i < d; i += blockDim.x * 4) {
       float4 v = *(float4*)(xr + i);
-      float4 q[8];
+      float4 q[kMaxSplitK];
 #pragma unroll
-      for (int p = 0; p < 8; ++p)
+      for (int p = 0; p < kMaxSplitK; ++p)
         if (p < nparts) q[p] = *(const float4*)(pr + p * part_stride + i);
 #pragma unroll
-      for (int p = 0; p < 8; ++p)
+      for (int p = 0; p < kMaxSplitK; ++p)
         if (p < nparts) {
           v.x += q[p].x;
           v.y += q[p].y;
@@ -102,7 +102,7 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* parts, int n
   auto col = [&](int c) {
     float v = pr[c];
 #pragma unroll
-    for (int p = 1; p < 8; ++p)
+    for (int p = 1; p < kMaxSplitK; ++p)
       if (p < nparts) v += pr[p * part_stride + c];
     return v;
   };
@@ -161,7 +161,7 @@ hipError_t embed_rmsnorm(const int* tok, int tok_stride, int R, const T* E, int 
 template <typename T>
 hipError_t residual_rmsnorm(float* x, const float* parts, int nparts, long long part_stride, const float* g,
                             float eps, int R, int d, T* xn, hipStream_t s) {
-  if (d % 4 || nparts < 0 || nparts > 8) return hipErrorInvalidValue;
+  if (d % 4 || nparts < 0 || nparts > kMaxSplitK) return hipErrorInvalidValue;
   hipLaunchKernelGGL(residual_rmsnorm_kernel<T>, dim3(R), dim3(kNormThreads), 0, s, x, parts, nparts, part_stride,
                      g, eps, d, xn);
   return hipGetLastError();
@@ -170,7 +170,7 @@ hipError_t residual_rmsnorm(float* x, const float* parts, int nparts, long long 
 template <typename T>
 hipError_t qkv_rope_store(const float* parts, int nparts, long long part_stride, const Rows& rows, int Hq,
                           int Hkv, int D, float theta, T* q, const KVLayout& kv, hipStream_t s) {
-  if (D > 256 || (D & 1) || nparts < 1 || nparts > 8) return hipErrorInvalidValue;
+  if (D > 256 || (D & 1) || nparts < 1 || nparts > kMaxSplitK) return hipErrorInvalidValue;
   hipLaunchKernelGGL(qkv_rope_kernel<T>, dim3(rows.R, (Hq + 2 * Hkv + 7) / 8), dim3(256), 0, s, parts, nparts,
                      part_stride, rows, Hq, Hkv, D, theta, q, kv);
   return hipGetLastError();

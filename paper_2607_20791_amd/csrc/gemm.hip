@@ -3,11 +3,12 @@
 //
 // At decode sizes every GEMM is bound by streaming W from HBM.  Weights are
 // repacked once, at model creation, into 16-row panels: panel p holds rows
-// [16p, 16p+16) as consecutive 2 KiB blocks of 64 k values, each block laid
-// out in the order the MFMA B operand is loaded (lane l = 16q + r reads 32
-// contiguous bytes: row r, k values [16q, 16q+16) of the block).  A wave
-// reading its panels therefore streams long contiguous runs, which keeps the
-// DRAM pages open.
+// [16p, 16p+16) as consecutive 2 KiB blocks of 64 k values.  A block is two
+// dense 1 KiB halves, one per MFMA of the 64-k step, each in the order the
+// MFMA B operand is loaded: lane l = 16q + r reads 16 contiguous bytes, row r,
+// k values 16q + 8h + {0..7} of the block (h = half).  Every weight load
+// instruction of a wave is thus one dense 1 KiB read, and a wave streaming its
+// panels reads long contiguous runs.
 //
 // A workgroup owns NW*NT panels (waves split N; for SwiGLU the first half of
 // the waves computes the gate panels and the second half the matching up
@@ -32,26 +33,20 @@ RGD_DEV float silu(float g) { return g / (1.0f + __expf(-g)); }
 
 constexpr int kStep = 64;  // k values per pipeline step
 
-// W [N][K] row-major -> panels [ceil(N/16)][K/64][64 lanes][16], rows past N
-// are zero.
+// W [N][K] row-major -> panels [ceil(N/16)][K/64][2 halves][64 lanes][8];
+// rows past N are zero.  One thread per 16-byte output chunk.
 __global__ void pack_panels_kernel(const bf16_t* __restrict__ w, int N, int K, bf16_t* __restrict__ out) {
   const long long nst = K / kStep;
-  const long long total = (long long)((N + 15) / 16) * nst * 64;  // 32-byte lane chunks
+  const long long total = (long long)((N + 15) / 16) * nst * 128;  // 16-byte chunks
   for (long long c = blockIdx.x * 256ll + threadIdx.x; c < total; c += 256ll * gridDim.x) {
-    const int lane = int(c & 63);
-    const long long blk = c >> 6;
+    const int lane = int(c & 63), h = int((c >> 6) & 1);
+    const long long blk = c >> 7;
     const long long st = blk % nst, p = blk / nst;
     const int r = lane & 15, q = lane >> 4;
     const long long row = p * 16 + r;
-    u32x4 v0 = {0u, 0u, 0u, 0u}, v1 = {0u, 0u, 0u, 0u};
-    if (row < N) {
-      const u32x4* src = (const u32x4*)(w + row * K + st * kStep + q * 16);
-      v0 = src[0];
-      v1 = src[1];
-    }
-    u32x4* dst = (u32x4*)(out + c * 16);
-    dst[0] = v0;
-    dst[1] = v1;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (row < N) v = *(const u32x4*)(w + row * K + st * kStep + q * 16 + h * 8);
+    *(u32x4*)(out + c * 8) = v;
   }
 }
 
@@ -81,7 +76,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
       if (a.nseg > 2 && p * 16 >= a.seg[2].n0) si = 2;
     }
     const int lp = min(p - a.seg[si].n0 / 16, (a.seg[si].n + 15) / 16 - 1);  // panel within the segment
-    wp[j] = (const bf16_t*)a.seg[si].w + ((long long)lp * nst) * 1024 + lane * 16;
+    wp[j] = (const bf16_t*)a.seg[si].w + ((long long)lp * nst) * 1024 + lane * 8;
     ncol[j] = p * 16 + col16;
   }
 
@@ -96,9 +91,9 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
   auto loadw = [&](int st, int slot) {
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
-      const u32x4* p = (const u32x4*)(wp[j] + (long long)st * 1024);
-      wb[slot][j][0] = __builtin_nontemporal_load(p);
-      wb[slot][j][1] = __builtin_nontemporal_load(p + 1);
+      const bf16_t* p = wp[j] + (long long)st * 1024;
+      wb[slot][j][0] = __builtin_nontemporal_load((const u32x4*)p);
+      wb[slot][j][1] = __builtin_nontemporal_load((const u32x4*)(p + 512));
     }
   };
   const bf16_t* X = (const bf16_t*)a.x;
@@ -275,7 +270,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 
 hipError_t pack_panels(const void* w, int N, int K, void* out, hipStream_t s) {
   if (K % kStep) return hipErrorInvalidValue;
-  const long long chunks = (long long)((N + 15) / 16) * (K / kStep) * 64;
+  const long long chunks = (long long)((N + 15) / 16) * (K / kStep) * 128;
   const int blocks = int(std::min<long long>(8192, (chunks + 255) / 256));
   hipLaunchKernelGGL(pack_panels_kernel, dim3(blocks), dim3(256), 0, s, (const bf16_t*)w, N, K, (bf16_t*)out);
   return hipGetLastError();

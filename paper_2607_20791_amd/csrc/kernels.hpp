@@ -69,7 +69,9 @@ inline int v_stride(int P) { return (P + 63) / 64 * 64; }
 template <typename T>
 hipError_t embed_rmsnorm(const int* tok, int tok_stride, int R, const T* E, int d, int V, float* x,
                          const float* g, float eps, T* xn, hipStream_t s);
-// x[r] += sum_p parts[p][r] (nparts <= 8); xn[r] = rmsnorm(x[r]) * g
+// split-K partial outputs a consumer kernel sums (at most)
+constexpr int kMaxSplitK = 16;
+// x[r] += sum_p parts[p][r] (nparts <= kMaxSplitK); xn[r] = rmsnorm(x[r]) * g
 template <typename T>
 hipError_t residual_rmsnorm(float* x, const float* parts, int nparts, long long part_stride, const float* g,
                             float eps, int R, int d, T* xn, hipStream_t s);

@@ -266,9 +266,11 @@ Rows device_rows(const rgd_model* m, const rgd_kv* kv, int R, int t, bool prefil
   return r;
 }
 
+// split-K factor of a decode GEMM: enough workgroups (about three per CU) to
+// keep the weight stream saturated, at least 4 steps of 64 k per split
 int pick_splits(int groups, int mblocks, int K, int R, int cap_rows) {
-  int ks = (int)cdiv(512, (long long)groups * mblocks);
-  ks = std::min(ks, 8);
+  int ks = (int)cdiv(768, (long long)groups * mblocks);
+  ks = std::min(ks, kMaxSplitK);
   ks = std::min(ks, std::max(1, K / 64 / 4));
   ks = std::min(ks, std::max(1, cap_rows / std::max(R, 1)));
   return std::max(ks, 1);
@@ -613,7 +615,7 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
   m->lm_head = w->lm_head;
   m->layers.assign(w->layers, w->layers + cfg->n_layers);
   m->max_rows = max_rows;
-  m->part_rows = std::max(max_rows, 512);
+  m->part_rows = std::max(max_rows, 16 * 64);
   const int R = max_rows, d = cfg->d_model, Hq = cfg->n_heads, Hkv = cfg->n_kv_heads, D = cfg->head_dim;
   m->nqkv = (Hq + 2 * Hkv) * D;
   m->ntiles = m->bf16 ? gemm_groups(GEMM_LOGITS, cfg->vocab) : (int)cdiv(cfg->vocab, 64);
