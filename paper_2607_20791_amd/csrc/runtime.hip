@@ -1090,7 +1090,9 @@ int32_t rgd_timing_enable(rgd_model* m, int32_t enable) {
   if (enable && m->tev[0].empty()) {
     for (int u = 0; u < RGD_TIMER_COUNT; ++u) {
       m->tev[u].resize(2 * kTimerPairs);
-      for (auto& e : m->tev[u]) HIP_OK(hipEventCreate(&e));
+      // timing-only events: no system-scope fence (no cache writeback and invalidate
+      // between the timed kernels)
+      for (auto& e : m->tev[u]) HIP_OK(hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
     }
   }
   m->timing = enable != 0;
