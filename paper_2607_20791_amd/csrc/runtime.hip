@@ -172,7 +172,7 @@ struct rgd_kv {
 namespace {
 
 // ------------------------------------------------------------ timing hooks --
-constexpr int kTimerPairs = 65536;
+constexpr int kTimerPairs = 8192;  // timed launches kept per unit between reads
 
 struct TimeScope {
   rgd_model* m;
