@@ -221,11 +221,14 @@ enum rgd_timer {
   RGD_TIMER_COUNT = 5
 };
 
-/* enable != 0: from now on the model records HIP events on the work stream
- * around each timed unit (at most 65536 launches per unit between reads; later
- * launches are not timed).  enable == 0 stops recording.  Events are created
- * here, not on the decode path. */
-int32_t rgd_timing_enable(rgd_model* m, int32_t enable);
+/* period >= 1: from now on the model records HIP events on the work stream
+ * around every period-th launch of each timed unit (at most 8192 timed
+ * launches per unit between reads; later launches are not timed).  A period
+ * above 1 keeps most launches free of event records, which otherwise leave
+ * small idle gaps on the stream.  period == 0 stops recording; negative is
+ * RGD_E_INVALID_ARG.  Events are created on the first enable, not on the
+ * decode path. */
+int32_t rgd_timing_enable(rgd_model* m, int32_t period);
 
 /* Waits for the recorded events and returns, per timed unit, the summed
  * duration in milliseconds (ms[RGD_TIMER_COUNT]) and the number of launches

@@ -256,8 +256,9 @@ def kernel_lm_head(model, h, logits):
     _check(lib.rgd_kernel_lm_head(model.h, _ptr(h), h.shape[0], _ptr(logits), _stream()))
 
 
-def timing_enable(model, on=True):
-    _check(lib.rgd_timing_enable(model.h, 1 if on else 0))
+def timing_enable(model, period=1):
+    """period >= 1 times every period-th launch of each unit; 0 (or False) stops."""
+    _check(lib.rgd_timing_enable(model.h, int(period)))
 
 
 def timing_read(model):

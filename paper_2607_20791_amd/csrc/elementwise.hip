@@ -75,28 +75,18 @@ __global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(float* x
   norm_store(xr, d, g, eps, xn + (long long)r * d);
 }
 
-// One workgroup per (row, group of 8 heads of the fused q|k|v output).
+// One workgroup per (row, group of 8 heads of the fused q|k|v output).  The
+// rotation of position pos, pair j is (cos, sin) = rope_cs[pos][j] (a table
+// computed once on the host in fp64).
 template <typename T>
 __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* parts, int nparts, long long part_stride,
-                                                       Rows rows, int Hq, int Hkv, int D, float theta, T* q,
-                                                       KVLayout kv) {
-  __shared__ float cs[128], sn[128];
+                                                       Rows rows, int Hq, int Hkv, int D, const float2* rope_cs,
+                                                       int max_pos, T* q, KVLayout kv) {
   const int r = blockIdx.x;
   const int h0 = blockIdx.y * 8, h1 = min(h0 + 8, Hq + 2 * Hkv);
   const int half = D / 2;
-  const int pos = rows.prefill ? rows.base_pos[r] : rows.base_pos[r] + rows.t;
-  if (h0 < Hq + Hkv) {
-    for (int j = threadIdx.x; j < half; j += 256) {
-      // angle in fp64: pos * theta^(-2j/D), reduced mod 2*pi before sin/cos
-      const double ang = double(pos) * pow(double(theta), -2.0 * double(j) / double(D));
-      const double red = ang - 6.283185307179586 * floor(ang / 6.283185307179586);
-      double sv, cv;
-      sincos(red, &sv, &cv);
-      cs[j] = float(cv);
-      sn[j] = float(sv);
-    }
-  }
-  __syncthreads();
+  const int pos = min(rows.prefill ? rows.base_pos[r] : rows.base_pos[r] + rows.t, max_pos);
+  const float2* cs = rope_cs + (long long)pos * half;
   const int nqkv = (Hq + 2 * Hkv) * D;
   const float* pr = parts + (long long)r * nqkv;
   auto col = [&](int c) {
@@ -134,8 +124,9 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* parts, int n
     const int base = h * D;
     if (h < Hq + Hkv) {  // rotated q or k pair (j, j + D/2)
       const float x1 = col(base + j), x2 = col(base + j + half);
-      const float y1 = x1 * cs[j] - x2 * sn[j];
-      const float y2 = x2 * cs[j] + x1 * sn[j];
+      const float2 cj = cs[j];
+      const float y1 = x1 * cj.x - x2 * cj.y;
+      const float y2 = x2 * cj.x + x1 * cj.y;
       T* dst = h < Hq ? q + ((long long)r * Hq + h) * D : kd + (long long)(h - Hq) * kstride;
       store_f(dst + j, y1);
       store_f(dst + j + half, y2);
@@ -169,10 +160,11 @@ hipError_t residual_rmsnorm(float* x, const float* parts, int nparts, long long 
 
 template <typename T>
 hipError_t qkv_rope_store(const float* parts, int nparts, long long part_stride, const Rows& rows, int Hq,
-                          int Hkv, int D, float theta, T* q, const KVLayout& kv, hipStream_t s) {
+                          int Hkv, int D, const float* rope_cs, int max_pos, T* q, const KVLayout& kv,
+                          hipStream_t s) {
   if (D > 256 || (D & 1) || nparts < 1 || nparts > kMaxSplitK) return hipErrorInvalidValue;
   hipLaunchKernelGGL(qkv_rope_kernel<T>, dim3(rows.R, (Hq + 2 * Hkv + 7) / 8), dim3(256), 0, s, parts, nparts,
-                     part_stride, rows, Hq, Hkv, D, theta, q, kv);
+                     part_stride, rows, Hq, Hkv, D, (const float2*)rope_cs, max_pos, q, kv);
   return hipGetLastError();
 }
 
@@ -184,9 +176,9 @@ template hipError_t residual_rmsnorm<float>(float*, const float*, int, long long
                                             float*, hipStream_t);
 template hipError_t residual_rmsnorm<bf16_t>(float*, const float*, int, long long, const float*, float, int, int,
                                              bf16_t*, hipStream_t);
-template hipError_t qkv_rope_store<float>(const float*, int, long long, const Rows&, int, int, int, float, float*,
+template hipError_t qkv_rope_store<float>(const float*, int, long long, const Rows&, int, int, int, const float*, int, float*,
                                           const KVLayout&, hipStream_t);
-template hipError_t qkv_rope_store<bf16_t>(const float*, int, long long, const Rows&, int, int, int, float,
+template hipError_t qkv_rope_store<bf16_t>(const float*, int, long long, const Rows&, int, int, int, const float*, int,
                                            bf16_t*, const KVLayout&, hipStream_t);
 
 }  // namespace rgd

@@ -76,10 +76,11 @@ template <typename T>
 hipError_t residual_rmsnorm(float* x, const float* parts, int nparts, long long part_stride, const float* g,
                             float eps, int R, int d, T* xn, hipStream_t s);
 // q/k/v = sum of nparts split partials [R][(Hq+2Hkv)D] fp32 -> RoPE -> q (T),
-// k/v appended to the cache
+// k/v appended to the cache.  rope_cs: [max_pos + 1][D/2] (cos, sin) pairs.
 template <typename T>
 hipError_t qkv_rope_store(const float* parts, int nparts, long long part_stride, const Rows& rows, int Hq,
-                          int Hkv, int D, float theta, T* q, const KVLayout& kv, hipStream_t s);
+                          int Hkv, int D, const float* rope_cs, int max_pos, T* q, const KVLayout& kv,
+                          hipStream_t s);
 
 // -------------------------------------------------------------- attention ----
 struct AttnArgs {

@@ -2,6 +2,7 @@
 // per-row tails, the decode step, and the probe, gate and sampling loops of
 // refusal-gated decoding (Algorithm 1).
 #include <algorithm>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -94,6 +95,7 @@ struct rgd_model {
   void* q = nullptr;
   float* part_o = nullptr;
   float* part_lse = nullptr;
+  float* rope_cs = nullptr;  // [max_pos + 1][head_dim / 2] (cos, sin)
   void* attn_out = nullptr;
   float* o_part = nullptr;
   void* act = nullptr;
@@ -118,6 +120,8 @@ struct rgd_model {
   bool timing = false;
   std::vector<hipEvent_t> tev[RGD_TIMER_COUNT];
   int tused[RGD_TIMER_COUNT] = {0};
+  long long tcount[RGD_TIMER_COUNT] = {0};  // launches seen while timing (every tperiod-th is timed)
+  int tperiod = 1;
   ~rgd_model() {
     for (auto& v : tev)
       for (hipEvent_t e : v) (void)hipEventDestroy(e);
@@ -180,7 +184,7 @@ struct TimeScope {
   hipStream_t s;
   bool on;
   TimeScope(rgd_model* m_, int unit_, hipStream_t s_) : m(m_), unit(unit_), s(s_) {
-    on = m->timing && m->tused[unit] < (int)m->tev[unit].size() / 2;
+    on = m->timing && m->tcount[unit]++ % m->tperiod == 0 && m->tused[unit] < (int)m->tev[unit].size() / 2;
     if (on) (void)hipEventRecord(m->tev[unit][2 * m->tused[unit]], s);
   }
   ~TimeScope() {
@@ -400,10 +404,10 @@ int forward_rows(rgd_model* m, rgd_kv* kv, const Rows& rows, const HostRows& h, 
     g.mode = GEMM_STORE;
     RGD_TRY(gemm(m, g, s));
     if (bf)
-      HIP_OK(qkv_rope_store<bf16_t>(m->qkv_part, g.splits, g.split_stride, rows, Hq, Hkv, D, c.rope_theta,
+      HIP_OK(qkv_rope_store<bf16_t>(m->qkv_part, g.splits, g.split_stride, rows, Hq, Hkv, D, m->rope_cs, c.max_pos,
                                     (bf16_t*)m->q, kvl, s));
     else
-      HIP_OK(qkv_rope_store<float>(m->qkv_part, g.splits, g.split_stride, rows, Hq, Hkv, D, c.rope_theta,
+      HIP_OK(qkv_rope_store<float>(m->qkv_part, g.splits, g.split_stride, rows, Hq, Hkv, D, m->rope_cs, c.max_pos,
                                    (float*)m->q, kvl, s));
     RGD_TRY(run_attention(m, kvl, rows, h, rows.prefill ? 0 : rows.t + 1, 0, m->attn_out, s));
     // output projection: partials added to the residual stream by the FFN norm
@@ -648,6 +652,23 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
   A(&m->d_base, (size_t)R * 4);
   A(&m->d_plen, (size_t)R * 4);
   A(&m->d_rblocks, (size_t)R * 16);
+  // RoPE rotations: angle pos * theta^(-2j/D) in fp64, rounded to fp32 once
+  const int half = D / 2;
+  const size_t ncs = ((size_t)cfg->max_pos + 1) * half;
+  A(&m->rope_cs, ncs * 2 * sizeof(float));
+  if (rc == RGD_OK) {
+    std::vector<float> cs(ncs * 2);
+    for (int j = 0; j < half; ++j) {
+      const double f = std::pow((double)cfg->rope_theta, -2.0 * j / D);
+      for (int pos = 0; pos <= cfg->max_pos; ++pos) {
+        const double a = pos * f;
+        cs[((size_t)pos * half + j) * 2] = (float)std::cos(a);
+        cs[((size_t)pos * half + j) * 2 + 1] = (float)std::sin(a);
+      }
+    }
+    if (hipMemcpy(m->rope_cs, cs.data(), cs.size() * sizeof(float), hipMemcpyHostToDevice) != hipSuccess)
+      rc = fail(RGD_E_HIP, "RoPE table upload failed");
+  }
   // bf16: repack every matrix into the GEMM panel layout
   if (rc == RGD_OK && m->bf16) {
     auto pack = [&](const void* src, int N, int K, void** dst) {
@@ -1084,10 +1105,11 @@ int32_t rgd_check_status(rgd_model* m, rgd_stream stream) {
   return RGD_OK;
 }
 
-int32_t rgd_timing_enable(rgd_model* m, int32_t enable) {
+int32_t rgd_timing_enable(rgd_model* m, int32_t period) {
   g_err.clear();
   if (!m) return fail(RGD_E_INVALID_ARG, "null model");
-  if (enable && m->tev[0].empty()) {
+  if (period < 0) return fail(RGD_E_INVALID_ARG, "timing period must be >= 0");
+  if (period && m->tev[0].empty()) {
     for (int u = 0; u < RGD_TIMER_COUNT; ++u) {
       m->tev[u].resize(2 * kTimerPairs);
       // timing-only events: no system-scope fence (no cache writeback and invalidate
@@ -1095,7 +1117,9 @@ int32_t rgd_timing_enable(rgd_model* m, int32_t enable) {
       for (auto& e : m->tev[u]) HIP_OK(hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
     }
   }
-  m->timing = enable != 0;
+  m->timing = period != 0;
+  m->tperiod = std::max(period, 1);
+  for (auto& c : m->tcount) c = 0;  // the first launch after an enable is timed
   return RGD_OK;
 }
 

@@ -2,13 +2,13 @@
 //
 // min-p sampling (temperature first): with m the row maximum, a token is kept
 // when w_i = exp2((z_i - m) * log2(e) / T) >= p_min, and the draw returns the
-// smallest kept id whose running kept-weight sum exceeds u * W.  Each row is
-// split into chunks handled by independent workgroups; every chunk's kept sum
-// goes to global memory, and the last workgroup of a row to finish (found with
-// a device-scope counter, no spinning) forms the chunk prefix in chunk order,
-// locates u * W and rescans that one chunk with a block-wide prefix scan.
-// Logits are therefore read once per draw from HBM; the row maximum comes in as
-// partial maxima (from the LM-head epilogue or a chunk-max pass).
+// smallest kept id whose running kept-weight sum exceeds u * W.  Two kernels:
+// the first has one workgroup per (row, chunk of logits) and writes the
+// chunk's kept-weight sum; the second has one workgroup per row, forms the
+// chunk prefix in chunk order, locates u * W and rescans that one chunk with a
+// block-wide prefix scan.  Logits are read once per draw from HBM (plus the
+// one rescanned chunk); the row maximum comes in as partial maxima (from the
+// LM-head epilogue or a chunk-max pass).  No cross-workgroup synchronisation.
 #include "kernels.hpp"
 #include "philox.hpp"
 
@@ -17,6 +17,14 @@ namespace rgd {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+
+// Kept-weight of one logit.  The hardware 2^x (no denormal range fix-up: a
+// weight below 2^-126 flushes to 0); the chunk sums and the rescan use this
+// same expression so both see the same kept set.
+RGD_DEV float kept_weight(float z, float mx, float kT, float p_min) {
+  const float w = __builtin_amdgcn_exp2f((z - mx) * kT);
+  return w >= p_min ? w : -1.f;  // -1 marks a dropped token
+}
 
 __global__ void fill_u32_kernel(uint32_t* p, uint32_t v, long long n) {
   for (long long i = blockIdx.x * 256ll + threadIdx.x; i < n; i += 256ll * gridDim.x) p[i] = v;
@@ -95,9 +103,10 @@ RGD_DEV float block_inclusive_scan(float v, float* wsum) {
   return v + off;
 }
 
-// Selects the token of row r for target u (in [0,1)) given the chunk sums.
-// Returns the token id (valid in every thread).
-RGD_DEV int select_token(const SampleArgs& a, int r, float mx, float u) {
+// Selects the token of row r for target u (in [0,1)); `mine` is chunk
+// threadIdx.x's kept sum (0 past the last chunk).  Returns the token id (valid
+// in every thread).
+RGD_DEV int select_token(const SampleArgs& a, int r, float mx, float u, float mine) {
   __shared__ float csum[256];
   __shared__ int sh_chunk, sh_last_nz;
   __shared__ float sh_base, sh_target;
@@ -106,7 +115,6 @@ RGD_DEV int select_token(const SampleArgs& a, int r, float mx, float u) {
   const float kT = kLog2e / a.T;
   // running sum over chunks in chunk order (one chunk per thread)
   const int c = threadIdx.x;
-  const float mine = c < a.nchunks ? a.chunk_sums[(long long)r * a.nchunks + c] : 0.f;
   const float incl_c = block_inclusive_scan(mine, wsum);
   csum[c] = incl_c;
   if (c == 0) {
@@ -128,24 +136,24 @@ RGD_DEV int select_token(const SampleArgs& a, int r, float mx, float u) {
     sh_target = target;
   }
   __syncthreads();
+  // rescan of the chosen chunk: thread t owns `per` consecutive logits
+  // (per = chunk / 256 <= 16, a multiple of 4; V is a multiple of 4)
   const int lo = sh_chunk * a.chunk, hi = min(a.V, lo + a.chunk);
   const int per = a.chunk / 256;
   const int e0 = lo + threadIdx.x * per, e1 = min(hi, e0 + per);
   const float* zr = a.z + r * a.ldz;
+  float4 zv[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+    zv[k] = (4 * k < per && e0 + 4 * k < e1) ? *(const float4*)(zr + e0 + 4 * k) : float4{0.f, 0.f, 0.f, 0.f};
   float wv[16];
   float ts = 0.f;
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
-    const int e = e0 + i;
-    float w = 0.f;
-    if (i < per && e < e1) {
-      w = exp2f((zr[e] - mx) * kT);
-      w = w >= a.p_min ? w : -1.f;   // -1 marks a dropped token
-    } else {
-      w = -1.f;
-    }
+    const float zi = i % 4 == 0 ? zv[i / 4].x : i % 4 == 1 ? zv[i / 4].y : i % 4 == 2 ? zv[i / 4].z : zv[i / 4].w;
+    const float w = (i < per && e0 + i < e1) ? kept_weight(zi, mx, kT, a.p_min) : -1.f;
     wv[i] = w;
-    ts += w > 0.f ? w : (w == 0.f ? 0.f : 0.f);
+    ts += w > 0.f ? w : 0.f;
   }
   const float incl = block_inclusive_scan(ts, wsum);
   float run = sh_base + (incl - ts);
@@ -181,18 +189,24 @@ RGD_DEV int select_token(const SampleArgs& a, int r, float mx, float u) {
 __global__ __launch_bounds__(256) void minp_sum_kernel(SampleArgs a) {
   __shared__ float red[4];
   const int c = blockIdx.x, r = blockIdx.y;
-  const float mx = row_max_from_partials(a.pmax, a.npmax, r, red);
-  const float kT = kLog2e / a.T;
   const float* zr = a.z + r * a.ldz;
   const int lo = c * a.chunk, hi = min(a.V, lo + a.chunk);
+  // the chunk's logits (chunk <= 4096: at most 4 float4 per thread) are
+  // requested before the row maximum is formed, so the two latencies overlap
+  float4 v[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int i = lo + (threadIdx.x + k * 256) * 4;  // V and chunk are multiples of 4
+    v[k] = i < hi ? *(const float4*)(zr + i) : float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+  }
+  const float mx = row_max_from_partials(a.pmax, a.npmax, r, red);
+  const float kT = kLog2e / a.T;
   float sum = 0.f;
-#pragma unroll 4
-  for (int i = lo + threadIdx.x * 4; i < hi; i += 1024) {
-    const float4 v = *(const float4*)(zr + i);  // V and chunk are multiples of 4
-    const float w0 = exp2f((v.x - mx) * kT), w1 = exp2f((v.y - mx) * kT);
-    const float w2 = exp2f((v.z - mx) * kT), w3 = exp2f((v.w - mx) * kT);
-    sum += (w0 >= a.p_min ? w0 : 0.f) + (w1 >= a.p_min ? w1 : 0.f) + (w2 >= a.p_min ? w2 : 0.f) +
-           (w3 >= a.p_min ? w3 : 0.f);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const float w0 = kept_weight(v[k].x, mx, kT, a.p_min), w1 = kept_weight(v[k].y, mx, kT, a.p_min);
+    const float w2 = kept_weight(v[k].z, mx, kT, a.p_min), w3 = kept_weight(v[k].w, mx, kT, a.p_min);
+    sum += (w0 > 0.f ? w0 : 0.f) + (w1 > 0.f ? w1 : 0.f) + (w2 > 0.f ? w2 : 0.f) + (w3 > 0.f ? w3 : 0.f);
   }
   sum = block_sum(sum, red);
   if (threadIdx.x == 0) {
@@ -204,9 +218,11 @@ __global__ __launch_bounds__(256) void minp_sum_kernel(SampleArgs a) {
 __global__ __launch_bounds__(256) void minp_select_kernel(SampleArgs a) {
   __shared__ float red[4];
   const int r = blockIdx.x;
+  // chunk sums and partial maxima are requested together
+  const float mine = (int)threadIdx.x < a.nchunks ? a.chunk_sums[(long long)r * a.nchunks + threadIdx.x] : 0.f;
   const float mx = row_max_from_partials(a.pmax, a.npmax, r, red);
   const float u = philox_uniform(a.seeds[r], a.ctr, a.stream);
-  const int tok = select_token(a, r, mx, u);
+  const int tok = select_token(a, r, mx, u, mine);
   if (threadIdx.x == 0) {
     a.out[r * a.out_stride + a.out_col] = tok;
     if (a.cur_tok) a.cur_tok[r] = tok;
@@ -217,9 +233,10 @@ __global__ __launch_bounds__(256) void minp_multi_kernel(SampleArgs a, unsigned 
                                                          int* out) {
   __shared__ float red[4];
   const int d = blockIdx.x, r = blockIdx.y;
+  const float mine = (int)threadIdx.x < a.nchunks ? a.chunk_sums[(long long)r * a.nchunks + threadIdx.x] : 0.f;
   const float mx = row_max_from_partials(a.pmax, a.npmax, r, red);
   const float u = philox_uniform(a.seeds[r], a.ctr, stream0 + unsigned(d));
-  const int tok = select_token(a, r, mx, u);
+  const int tok = select_token(a, r, mx, u, mine);
   if (threadIdx.x == 0) out[(long long)r * draws + d] = tok;
 }
 
