@@ -50,9 +50,11 @@ __global__ void pack_panels_kernel(const bf16_t* __restrict__ w, int N, int K, b
   }
 }
 
-template <int MT, int NT, int NW, int SW, int MODE>
+// XS: 64-k steps of X staged per LDS slot (one barrier per XS steps).
+template <int MT, int NT, int NW, int SW, int MODE, int XS>
 __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
-  constexpr int NTH = NW * 64, XSEG = MT * 16 * 8, XPT = (XSEG + NTH - 1) / NTH;
+  constexpr int NTH = NW * 64, XSEG = MT * 16 * 8 * XS, XPT = (XSEG + NTH - 1) / NTH;
+  static_assert(XS % SW == 0 || SW % XS == 0, "ring slots must stay static within an X stage");
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, col16 = lane & 15;
   const int m0 = blockIdx.y * (MT * 16);
   const int split = blockIdx.z;
@@ -80,7 +82,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
     ncol[j] = p * 16 + col16;
   }
 
-  __shared__ __attribute__((aligned(16))) bf16_t xs[2][MT * 16][72];
+  __shared__ __attribute__((aligned(16))) bf16_t xs[2][MT * 16][XS * kStep + 8];
   f32x4 acc[MT][NT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
@@ -97,21 +99,23 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
     }
   };
   const bf16_t* X = (const bf16_t*)a.x;
-  auto loadx = [&](int st) {
+  // X rows of the stage starting at step c0: XS * 8 16-byte segments per row
+  auto loadx = [&](int c0) {
 #pragma unroll
     for (int i = 0; i < XPT; ++i) {
       const int seg = threadIdx.x + i * NTH;
-      const int r = seg >> 3, c = (seg & 7) * 8;
+      const int r = seg / (8 * XS), c = (seg % (8 * XS)) * 8;
       const int m = m0 + r;
-      xr[i] = (seg < XSEG && m < a.M) ? *(const u32x4*)(X + (long long)m * a.ldx + st * kStep + c)
-                                       : u32x4{0u, 0u, 0u, 0u};
+      const int k = c0 * kStep + c;
+      xr[i] = (seg < XSEG && m < a.M && k < st1 * kStep) ? *(const u32x4*)(X + (long long)m * a.ldx + k)
+                                                          : u32x4{0u, 0u, 0u, 0u};
     }
   };
   auto storex = [&](int slot) {
 #pragma unroll
     for (int i = 0; i < XPT; ++i) {
       const int seg = threadIdx.x + i * NTH;
-      if (seg < XSEG) *(u32x4*)&xs[slot][seg >> 3][(seg & 7) * 8] = xr[i];
+      if (seg < XSEG) *(u32x4*)&xs[slot][seg / (8 * XS)][(seg % (8 * XS)) * 8] = xr[i];
     }
   };
 
@@ -120,24 +124,30 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
     if (st0 + j < st1) loadw(st0 + j, j);
   if (st0 < st1) loadx(st0);
   const int kq = (lane >> 4) * 16;
-  for (int sb = st0; sb < st1; sb += SW) {
+  // W ring: step st lives in slot (st - st0) % SW; X stage g covers steps
+  // [st0 + g*XS, st0 + (g+1)*XS)
+  constexpr int UN = XS > SW ? XS : SW;  // steps per unrolled block
+  for (int sb = st0; sb < st1; sb += UN) {
 #pragma unroll
-    for (int j = 0; j < SW; ++j) {
+    for (int j = 0; j < UN; ++j) {
       const int st = sb + j;
       if (st < st1) {
-        const int xsl = (st - st0) & 1;
-        storex(xsl);
-        if (st + 1 < st1) loadx(st + 1);
-        __syncthreads();
+        const int g = (st - st0) / XS, kk = ((st - st0) % XS) * kStep;
+        const int xsl = g & 1;
+        if (kk == 0) {  // first step of a stage: publish it, fetch the next
+          storex(xsl);
+          if (st + XS < st1) loadx(st + XS);
+          __syncthreads();
+        }
 #pragma unroll
         for (int h = 0; h < 2; ++h)
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) {
-            const u32x4 av = *(const u32x4*)&xs[xsl][mt * 16 + col16][kq + h * 8];
+            const u32x4 av = *(const u32x4*)&xs[xsl][mt * 16 + col16][kk + kq + h * 8];
 #pragma unroll
-            for (int jj = 0; jj < NT; ++jj) acc[mt][jj] = mfma16x16x32(av, wb[j][jj][h], acc[mt][jj]);
+            for (int jj = 0; jj < NT; ++jj) acc[mt][jj] = mfma16x16x32(av, wb[j % SW][jj][h], acc[mt][jj]);
           }
-        if (st + SW < st1) loadw(st + SW, j);
+        if (st + SW < st1) loadw(st + SW, j % SW);
       }
     }
   }
@@ -213,17 +223,17 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
   }
 }
 
-template <int NT, int NW, int SW, int MODE>
+template <int NT, int NW, int SW, int MODE, int XS>
 hipError_t launch_bf16(const GemmArgs& a, int ngroups, hipStream_t s) {
   const int splits = a.splits;
   if (a.M <= 16) {
-    hipLaunchKernelGGL((gemm_bf16_kernel<1, NT, NW, SW, MODE>), dim3(ngroups, 1, splits), dim3(NW * 64), 0, s,
-                       a);
+    hipLaunchKernelGGL((gemm_bf16_kernel<1, NT, NW, SW, MODE, XS>), dim3(ngroups, 1, splits), dim3(NW * 64), 0,
+                       s, a);
   } else if (a.M <= 32) {
-    hipLaunchKernelGGL((gemm_bf16_kernel<2, NT, NW, SW, MODE>), dim3(ngroups, 1, splits), dim3(NW * 64), 0, s,
-                       a);
+    hipLaunchKernelGGL((gemm_bf16_kernel<2, NT, NW, SW, MODE, XS>), dim3(ngroups, 1, splits), dim3(NW * 64), 0,
+                       s, a);
   } else {
-    hipLaunchKernelGGL((gemm_bf16_kernel<4, NT, NW, SW, MODE>), dim3(ngroups, (a.M + 63) / 64, splits),
+    hipLaunchKernelGGL((gemm_bf16_kernel<4, NT, NW, SW, MODE, XS>), dim3(ngroups, (a.M + 63) / 64, splits),
                        dim3(NW * 64), 0, s, a);
   }
   return hipGetLastError();
@@ -282,24 +292,27 @@ int gemm_groups(int mode, int N) {
   switch (mode) {
     case GEMM_SILU: return (N + 31) / 32;     // 2 gate + 2 up panels of 16 features
     case GEMM_LOGITS: return (N + 255) / 256;  // 8 waves x 2 panels
-    default: return (N + 63) / 64;            // 4 waves x 1 panel
+    default: return (N + 127) / 128;          // 8 waves x 1 panel
   }
 }
 
+// Launch shapes (panels per wave, waves, weight steps in flight, X steps per
+// LDS stage), chosen by measurement at the decode shapes of an 8B-class layer:
+// split-K projections <1, 8, 4, 2>, SwiGLU <1, 4, 4, 4>, LM head <2, 8, 2, 1>.
 hipError_t gemm_bf16(const GemmArgs& a, hipStream_t s) {
   if (a.K % kStep != 0 || a.M < 1 || a.splits < 1 || a.splits > a.K / kStep) return hipErrorInvalidValue;
   const int g = gemm_groups(a.mode, a.N);
   switch (a.mode) {
     case GEMM_STORE:
       for (int i = 1; i < a.nseg; ++i)
-        if (a.seg[i].n0 % 64) return hipErrorInvalidValue;  // a workgroup never straddles segments
-      return launch_bf16<1, 4, 4, GEMM_STORE>(a, g, s);
+        if (a.seg[i].n0 % 128) return hipErrorInvalidValue;  // a workgroup never straddles segments
+      return launch_bf16<1, 8, 4, GEMM_STORE, 2>(a, g, s);
     case GEMM_SILU:
       if (a.splits != 1) return hipErrorInvalidValue;
-      return launch_bf16<1, 4, 4, GEMM_SILU>(a, g, s);
+      return launch_bf16<1, 4, 4, GEMM_SILU, 4>(a, g, s);
     case GEMM_LOGITS:
       if (a.splits != 1 || a.ntiles != g) return hipErrorInvalidValue;
-      return launch_bf16<2, 8, 2, GEMM_LOGITS>(a, g, s);
+      return launch_bf16<2, 8, 2, GEMM_LOGITS, 1>(a, g, s);
     default:
       return hipErrorInvalidValue;
   }

@@ -270,14 +270,14 @@ Rows device_rows(const rgd_model* m, const rgd_kv* kv, int R, int t, bool prefil
   return r;
 }
 
-// split-K factor of a decode GEMM: enough workgroups (about three per CU) to
-// keep the weight stream saturated, at least 4 steps of 64 k per split
+// split-K factor of a decode GEMM: the smallest power of two that gives at
+// least one workgroup per CU (equal splits measured best), at most
+// kMaxSplitK, at least 4 steps of 64 k per split, within the partial buffers
 int pick_splits(int groups, int mblocks, int K, int R, int cap_rows) {
-  int ks = (int)cdiv(768, (long long)groups * mblocks);
-  ks = std::min(ks, kMaxSplitK);
-  ks = std::min(ks, std::max(1, K / 64 / 4));
-  ks = std::min(ks, std::max(1, cap_rows / std::max(R, 1)));
-  return std::max(ks, 1);
+  int ks = 1;
+  while (ks < kMaxSplitK && (long long)groups * mblocks * ks < 256) ks *= 2;
+  while (ks > 1 && (K / 64 / ks < 4 || ks * std::max(R, 1) > cap_rows)) ks /= 2;
+  return ks;
 }
 
 // -------------------------------------------------------------- attention --
