@@ -66,6 +66,46 @@ def algorithmic(w, R, P, tails):
     return lm_bytes, lm_flops, att_bytes, att_flops, samp_bytes
 
 
+def sampler_sweep(rgd, torch, reps=10):
+    """The standalone min-p sampler on the sampler-sweep workload (256 rows of
+    152064 Zipf-biased logits) at every (T, p_min) grid point, plus T = 0
+    (argmax): average time per call over `reps` calls, events on the launch
+    stream.  Algorithmic bytes per call: the logits once plus the tokens."""
+    import synth
+    s = synth.C3
+    z = torch.from_numpy(synth.sweep_logits(s)).cuda()
+    R, V = z.shape
+    ws = torch.empty(rgd.sampler_workspace_bytes(R, V), dtype=torch.uint8, device="cuda")
+    out = torch.empty(R, 1, dtype=torch.int32, device="cuda")
+    seeds = torch.arange(R, dtype=torch.int64, device="cuda")
+    nbytes = R * V * 4 + R * 4
+
+    def timed(f):
+        for _ in range(2):
+            f()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            f()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps
+
+    pts = []
+    for T in s.temperatures:
+        for pm in s.min_ps:
+            us = timed(lambda: rgd.kernel_sample(z, T, pm, seeds, 0, 0, 1, ws, out))
+            pts.append({"T": T, "min_p": pm, "us": round(us, 2)})
+    am = timed(lambda: rgd.kernel_argmax(z, ws, out[:, 0]))
+    us_all = sorted(p["us"] for p in pts)
+    med = us_all[len(us_all) // 2]
+    return {"workload": s.name, "rows": R, "vocab": V, "bytes_per_call": nbytes, "points": pts,
+            "median_us": med, "median_gbs": round(nbytes / (med * 1e-6) / 1e9, 1),
+            "median_frac": round(nbytes / (med * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+            "argmax_us": round(am, 2)}
+
+
 def cpu_baseline(weights, w, P, last_tok, kp, vp, budget_s=15.0):
     """The oracle on the host: prefill of the last prompt token, then one
     branch's draws and decode steps until the time budget is spent."""
@@ -272,6 +312,8 @@ def main():
         "wall_ms_per_step_with_prefill": round(elapsed / args.steps * 1e3, 3),
     }
     line.update(res)
+    log("sampler sweep ...")
+    line["sampler_sweep"] = sampler_sweep(rgd, torch)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle ...")
         line["cpu_baseline"] = cpu_baseline(weights, w, P, last_tok, kp, vp)

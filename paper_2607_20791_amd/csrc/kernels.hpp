@@ -121,7 +121,6 @@ struct SampleArgs {
   float T; float p_min;
   int chunk; int nchunks;
   float* chunk_sums;              // [R][nchunks]
-  unsigned int* counters;         // [R] zero on entry, left zero
   const unsigned long long* seeds;  // [R]
   unsigned int ctr; unsigned int stream;
   int* out; long long out_stride; int out_col;   // token of row r -> out[r*out_stride + out_col]

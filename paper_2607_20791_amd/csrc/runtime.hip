@@ -103,7 +103,6 @@ struct rgd_model {
   float* logits = nullptr;
   float* tilemax = nullptr;
   float* chunk_sums = nullptr;
-  unsigned* counters = nullptr;
   unsigned long long* best = nullptr;
   int* cur_tok = nullptr;
   int* status = nullptr;
@@ -476,7 +475,6 @@ SampleArgs sample_args(rgd_model* m, const float* z, long long ldz, int R, int V
   a.chunk = kSampleChunk;
   a.nchunks = (int)cdiv(V, kSampleChunk);
   a.chunk_sums = m->chunk_sums;
-  a.counters = m->counters;
   a.seeds = seeds;
   a.ctr = ctr;
   a.stream = 0;
@@ -643,7 +641,6 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
   A(&m->logits, (size_t)R * cfg->vocab * 4);
   A(&m->tilemax, (size_t)R * m->ntiles * 4);
   A(&m->chunk_sums, (size_t)R * m->nchunks * 4);
-  A(&m->counters, (size_t)R * 4);
   A(&m->best, (size_t)R * 8);
   A(&m->cur_tok, (size_t)R * 4);
   A(&m->status, 4);
@@ -702,8 +699,8 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
     delete m;
     return fail(RGD_E_HIP, "pinned staging allocation failed");
   }
-  // counters / maxima start cleared
-  if (hipMemset(m->counters, 0, (size_t)R * 4) != hipSuccess || hipMemset(m->best, 0, (size_t)R * 8) != hipSuccess ||
+  // argmax keys start cleared
+  if (hipMemset(m->best, 0, (size_t)R * 8) != hipSuccess ||
       hipMemset(m->status, 0, 4) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
     delete m;
     return fail(RGD_E_HIP, "workspace initialisation failed");
@@ -1200,8 +1197,8 @@ int32_t rgd_kernel_lm_head(rgd_model* m, const void* hvec, int32_t R, float* log
 uint64_t rgd_sampler_workspace_bytes(int32_t R, int32_t V) {
   if (R < 1 || V < 1) return 0;
   const long long nch = cdiv(V, kSampleChunk);
-  // best u64 [R], counters u32 [R], chunk maxima f32 [R][nch], chunk sums f32 [R][nch]
-  return (uint64_t)(8LL * R + 4LL * R + 8LL * R * nch + 256);
+  // best u64 [R], chunk maxima f32 [R][nch], chunk sums f32 [R][nch]
+  return (uint64_t)(8LL * R + 8LL * R * nch + 256);
 }
 
 int32_t rgd_kernel_argmax(const float* z, int32_t R, int32_t V, void* workspace, int32_t* out, rgd_stream stream) {
@@ -1231,10 +1228,8 @@ int32_t rgd_kernel_sample(const float* z, int32_t R, int32_t V, float T, float m
   hipStream_t s = (hipStream_t)stream;
   const int nch = (int)cdiv(V, kSampleChunk);
   char* w = (char*)workspace;
-  unsigned* counters = (unsigned*)(w + 8LL * R);
-  float* cmax = (float*)(w + 12LL * R);
+  float* cmax = (float*)(w + 8LL * R);
   float* csum = cmax + (long long)R * nch;
-  HIP_OK(fill_u32(counters, 0u, R, s));
   HIP_OK(chunk_max(z, V, R, V, kSampleChunk, cmax, s));
   SampleArgs a{};
   a.z = z;
@@ -1248,7 +1243,6 @@ int32_t rgd_kernel_sample(const float* z, int32_t R, int32_t V, float T, float m
   a.chunk = kSampleChunk;
   a.nchunks = nch;
   a.chunk_sums = csum;
-  a.counters = counters;
   a.seeds = (const unsigned long long*)seeds;
   a.ctr = ctr;
   a.stream = stream0;

@@ -30,6 +30,8 @@ __global__ void fill_u32_kernel(uint32_t* p, uint32_t v, long long n) {
   for (long long i = blockIdx.x * 256ll + threadIdx.x; i < n; i += 256ll * gridDim.x) p[i] = v;
 }
 
+// Per-chunk maxima; chunk is a multiple of 1024 (4 float4 per thread per
+// 1024 logits) and V a multiple of 4.
 __global__ __launch_bounds__(256) void chunk_max_kernel(const float* z, long long ldz, int V, int chunk,
                                                         float* cmax) {
   __shared__ float red[4];
@@ -37,7 +39,16 @@ __global__ __launch_bounds__(256) void chunk_max_kernel(const float* z, long lon
   const float* zr = z + r * ldz;
   const int lo = c * chunk, hi = min(V, lo + chunk);
   float mx = -INFINITY;
-  for (int i = lo + threadIdx.x; i < hi; i += 256) mx = fmaxf(mx, zr[i]);
+  for (int i0 = lo; i0 < hi; i0 += 4096) {
+    float4 v[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int i = i0 + (threadIdx.x + k * 256) * 4;
+      v[k] = i < hi ? *(const float4*)(zr + i) : float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) mx = fmaxf(mx, fmaxf(fmaxf(v[k].x, v[k].y), fmaxf(v[k].z, v[k].w)));
+  }
   mx = block_max(mx, red);
   if (threadIdx.x == 0) cmax[(long long)r * gridDim.x + c] = mx;
 }
@@ -46,6 +57,9 @@ RGD_DEV unsigned long long pack_key(float v, int idx) {
   return ((unsigned long long)ordered_u32(v) << 32) | (unsigned long long)(0xFFFFFFFFu - uint32_t(idx));
 }
 
+// VEC: float4 loads (V and ldz multiples of 4, rows 16-byte aligned);
+// otherwise one logit per thread and step.
+template <bool VEC>
 __global__ __launch_bounds__(256) void argmax_kernel(const float* z, long long ldz, int V, int chunk,
                                                      unsigned long long* best) {
   __shared__ unsigned long long red[4];
@@ -53,9 +67,34 @@ __global__ __launch_bounds__(256) void argmax_kernel(const float* z, long long l
   const float* zr = z + r * ldz;
   const int lo = c * chunk, hi = min(V, lo + chunk);
   unsigned long long k = 0;
-  for (int i = lo + threadIdx.x; i < hi; i += 256) {
-    const unsigned long long ki = pack_key(zr[i], i);
-    k = ki > k ? ki : k;
+  if (VEC) {
+    for (int i0 = lo; i0 < hi; i0 += 4096) {
+      float4 v[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int i = i0 + (threadIdx.x + j * 256) * 4;
+        v[j] = i < hi ? *(const float4*)(zr + i) : float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int i = i0 + (threadIdx.x + j * 256) * 4;
+        if (i < hi) {
+          unsigned long long t = pack_key(v[j].x, i);
+          k = t > k ? t : k;
+          t = pack_key(v[j].y, i + 1);
+          k = t > k ? t : k;
+          t = pack_key(v[j].z, i + 2);
+          k = t > k ? t : k;
+          t = pack_key(v[j].w, i + 3);
+          k = t > k ? t : k;
+        }
+      }
+    }
+  } else {
+    for (int i = lo + threadIdx.x; i < hi; i += 256) {
+      const unsigned long long t = pack_key(zr[i], i);
+      k = t > k ? t : k;
+    }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -291,6 +330,7 @@ hipError_t fill_u32(uint32_t* p, uint32_t v, long long n, hipStream_t s) {
 }
 
 hipError_t chunk_max(const float* z, long long ldz, int R, int V, int chunk, float* cmax, hipStream_t s) {
+  if (chunk % 1024 || V % 4 || ldz % 4) return hipErrorInvalidValue;
   hipLaunchKernelGGL(chunk_max_kernel, dim3((V + chunk - 1) / chunk, R), dim3(256), 0, s, z, ldz, V, chunk,
                      cmax);
   return hipGetLastError();
@@ -299,8 +339,11 @@ hipError_t chunk_max(const float* z, long long ldz, int R, int V, int chunk, flo
 hipError_t argmax_rows(const float* z, long long ldz, int R, int V, unsigned long long* best,
                        hipStream_t s) {
   const int chunk = 4096;
-  hipLaunchKernelGGL(argmax_kernel, dim3((V + chunk - 1) / chunk, R), dim3(256), 0, s, z, ldz, V, chunk,
-                     best);
+  const dim3 grid((V + chunk - 1) / chunk, R);
+  if (V % 4 == 0 && ldz % 4 == 0 && (uintptr_t)z % 16 == 0)
+    hipLaunchKernelGGL(argmax_kernel<true>, grid, dim3(256), 0, s, z, ldz, V, chunk, best);
+  else
+    hipLaunchKernelGGL(argmax_kernel<false>, grid, dim3(256), 0, s, z, ldz, V, chunk, best);
   return hipGetLastError();
 }
 

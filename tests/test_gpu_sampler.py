@@ -38,6 +38,20 @@ def test_argmax_ties_lowest_index(rgd):
     assert list(got) == [0, 100, 4095, 3, 10]
 
 
+@pytest.mark.parametrize("V", [1, 5, 1003, 4097, 8193])
+def test_argmax_any_vocab(rgd, V):
+    """Vocabularies that are not a multiple of 4 (unaligned rows) take the
+    scalar path; the last position and ties across chunk edges included."""
+    g = np.random.default_rng(V)
+    z = g.normal(size=(3, V)).astype(np.float32)
+    z[1, V - 1] = 40.0
+    if V > 4096:
+        z[2, 4095] = z[2, 4096] = 41.0
+    got = argmax_gpu(rgd, z)
+    want = np.array([sampler.argmax(r) for r in z])
+    assert np.array_equal(got, want)
+
+
 def _check_rows(z, T, pmin, got, seeds, ctr, stream):
     counts = {"exact": 0, "margin-equal": 0, "margin-diff": 0}
     for r in range(got.shape[0]):
