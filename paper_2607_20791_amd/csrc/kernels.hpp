@@ -128,6 +128,10 @@ struct SampleArgs {
   int* status;                    // device flag: set to 1 on a non-finite row maximum
 };
 hipError_t minp_sample(const SampleArgs& a, hipStream_t s);
+// rows without producer maxima: chunk maxima into cmax [R][nchunks] and the
+// chunk sums in one read of the logits (plus rereads of chunks whose maximum
+// is within the min-p window of the row maximum), then the draw
+hipError_t minp_sample_standalone(const SampleArgs& a, float* cmax, hipStream_t s);
 // many draws per row from precomputed chunk sums (counter (ctr, stream0 + d))
 hipError_t minp_multi_draw(const SampleArgs& a, int draws, unsigned int stream0, int* out,
                            hipStream_t s);

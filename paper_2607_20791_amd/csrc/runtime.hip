@@ -1230,7 +1230,6 @@ int32_t rgd_kernel_sample(const float* z, int32_t R, int32_t V, float T, float m
   char* w = (char*)workspace;
   float* cmax = (float*)(w + 8LL * R);
   float* csum = cmax + (long long)R * nch;
-  HIP_OK(chunk_max(z, V, R, V, kSampleChunk, cmax, s));
   SampleArgs a{};
   a.z = z;
   a.ldz = V;
@@ -1251,7 +1250,7 @@ int32_t rgd_kernel_sample(const float* z, int32_t R, int32_t V, float T, float m
   a.out_col = 0;
   a.cur_tok = nullptr;
   a.status = nullptr;
-  HIP_OK(minp_sample(a, s));
+  HIP_OK(minp_sample_standalone(a, cmax, s));
   if (draws > 1) HIP_OK(minp_multi_draw(a, draws, stream0, out, s));
   return RGD_OK;
 }

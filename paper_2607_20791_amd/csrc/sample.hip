@@ -254,6 +254,70 @@ __global__ __launch_bounds__(256) void minp_sum_kernel(SampleArgs a) {
   }
 }
 
+// Standalone rows (no partial maxima from a producer): one read of the
+// logits.  Pass 1 writes each chunk's maximum m_c and its kept sum relative
+// to m_c.  With m the row maximum, a chunk whose m_c == m has the exact sum,
+// a chunk whose best weight exp2((m_c - m) kT) is below p_min keeps nothing,
+// and only the chunks in between are read again (pass 2) to sum the weights
+// relative to m.
+__global__ __launch_bounds__(256) void minp_cand_kernel(SampleArgs a, float* cmax) {
+  __shared__ float red[4];
+  const int c = blockIdx.x, r = blockIdx.y;
+  const float* zr = a.z + r * a.ldz;
+  const int lo = c * a.chunk, hi = min(a.V, lo + a.chunk);
+  float4 v[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int i = lo + (threadIdx.x + k * 256) * 4;
+    v[k] = i < hi ? *(const float4*)(zr + i) : float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+  }
+  float mc = -INFINITY;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) mc = fmaxf(mc, fmaxf(fmaxf(v[k].x, v[k].y), fmaxf(v[k].z, v[k].w)));
+  mc = block_max(mc, red);
+  const float kT = kLog2e / a.T;
+  float sum = 0.f;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const float w0 = kept_weight(v[k].x, mc, kT, a.p_min), w1 = kept_weight(v[k].y, mc, kT, a.p_min);
+    const float w2 = kept_weight(v[k].z, mc, kT, a.p_min), w3 = kept_weight(v[k].w, mc, kT, a.p_min);
+    sum += (w0 > 0.f ? w0 : 0.f) + (w1 > 0.f ? w1 : 0.f) + (w2 > 0.f ? w2 : 0.f) + (w3 > 0.f ? w3 : 0.f);
+  }
+  sum = block_sum(sum, red);
+  if (threadIdx.x == 0) {
+    cmax[(long long)r * a.nchunks + c] = mc;
+    a.chunk_sums[(long long)r * a.nchunks + c] = sum;
+  }
+}
+
+__global__ __launch_bounds__(256) void minp_fix_kernel(SampleArgs a) {
+  __shared__ float red[4];
+  const int c = blockIdx.x, r = blockIdx.y;
+  const float mx = row_max_from_partials(a.pmax, a.npmax, r, red);
+  const float mc = a.pmax[(long long)r * a.npmax + c];
+  const float kT = kLog2e / a.T;
+  if (mc == mx) return;                         // exact already
+  if (kept_weight(mc, mx, kT, a.p_min) < 0.f) {  // nothing of this chunk is kept
+    if (threadIdx.x == 0) a.chunk_sums[(long long)r * a.nchunks + c] = 0.f;
+    return;
+  }
+  const float* zr = a.z + r * a.ldz;
+  const int lo = c * a.chunk, hi = min(a.V, lo + a.chunk);
+  float sum = 0.f;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int i = lo + (threadIdx.x + k * 256) * 4;
+    if (i < hi) {
+      const float4 v = *(const float4*)(zr + i);
+      const float w0 = kept_weight(v.x, mx, kT, a.p_min), w1 = kept_weight(v.y, mx, kT, a.p_min);
+      const float w2 = kept_weight(v.z, mx, kT, a.p_min), w3 = kept_weight(v.w, mx, kT, a.p_min);
+      sum += (w0 > 0.f ? w0 : 0.f) + (w1 > 0.f ? w1 : 0.f) + (w2 > 0.f ? w2 : 0.f) + (w3 > 0.f ? w3 : 0.f);
+    }
+  }
+  sum = block_sum(sum, red);
+  if (threadIdx.x == 0) a.chunk_sums[(long long)r * a.nchunks + c] = sum;
+}
+
 __global__ __launch_bounds__(256) void minp_select_kernel(SampleArgs a) {
   __shared__ float red[4];
   const int r = blockIdx.x;
@@ -352,6 +416,19 @@ hipError_t minp_sample(const SampleArgs& a, hipStream_t s) {
       a.nchunks * a.chunk < a.V || !(a.T > 0.f))
     return hipErrorInvalidValue;
   hipLaunchKernelGGL(minp_sum_kernel, dim3(a.nchunks, a.R), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(minp_select_kernel, dim3(a.R), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t minp_sample_standalone(const SampleArgs& a0, float* cmax, hipStream_t s) {
+  if (a0.chunk != 4096 || a0.V % 4 || a0.ldz % 4 || a0.nchunks > 256 || a0.nchunks * a0.chunk < a0.V ||
+      !(a0.T > 0.f))
+    return hipErrorInvalidValue;
+  SampleArgs a = a0;
+  a.pmax = cmax;
+  a.npmax = a.nchunks;
+  hipLaunchKernelGGL(minp_cand_kernel, dim3(a.nchunks, a.R), dim3(256), 0, s, a, cmax);
+  hipLaunchKernelGGL(minp_fix_kernel, dim3(a.nchunks, a.R), dim3(256), 0, s, a);
   hipLaunchKernelGGL(minp_select_kernel, dim3(a.R), dim3(256), 0, s, a);
   return hipGetLastError();
 }
