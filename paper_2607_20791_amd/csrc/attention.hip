@@ -219,7 +219,10 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
         float x = lmax[nt];
         x = fmaxf(x, __shfl_xor(x, 16, 64));
         x = fmaxf(x, __shfl_xor(x, 32, 64));
-        if (x > m[nt]) {
+        // only a query vector whose own maximum passed its reference by more
+        // than kLazy moves: its arithmetic never depends on the other query
+        // vectors of the wave (rows batched together give the same results)
+        if (x > m[nt] + kLazy) {
           const float alpha = exp2_raw(m[nt] - x);  // 0 on the first visible half
           lsum[nt] *= alpha;
 #pragma unroll

@@ -60,6 +60,7 @@ struct KVLayout {
   int P;           // prefix capacity per prompt
   int VP;          // P rounded up to a multiple of 64
   int page_size;
+  int split_len;   // positions per prefix split of the bf16 attention (fixed per KV state)
 };
 
 inline int v_stride(int P) { return (P + 63) / 64 * 64; }

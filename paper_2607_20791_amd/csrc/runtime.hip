@@ -43,6 +43,16 @@ int fail(int code, const char* fmt, ...) {
 
 inline long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
 
+// Positions per prefix split of the bf16 attention: a function of the KV
+// state's shape only (prompt capacity, prompts, KV heads), never of the rows
+// of a step, so the split boundaries a row sees do not depend on the other
+// rows.  Enough splits that the prompts' (split, KV head) pairs fill the
+// chip (about 256 workgroups), a multiple of 64 positions.
+int prefix_split_len(int P, int prompts, int Hkv) {
+  const long long S = std::max<long long>(1, cdiv(256, (long long)std::max(prompts, 1) * Hkv));
+  return (int)std::max<long long>(64, cdiv(cdiv(std::max(P, 1), S), 64) * 64);
+}
+
 constexpr int kMaxParts = 40;      // attention partials per row (prefix splits + tail chunks)
 constexpr int kSampleChunk = 4096; // logits per sampler workgroup
 constexpr int kTailChunk = 256;
@@ -167,6 +177,7 @@ struct rgd_kv {
     k.pool_v = (char*)pool_v + l * pool;
     k.P = max_prefix;
     k.VP = v_stride(max_prefix);
+    k.split_len = prefix_split_len(max_prefix, max_prompts, m->cfg.n_kv_heads);
     k.page_size = page_size;
     return k;
   }
@@ -219,6 +230,7 @@ int upload(rgd_model* m, const std::vector<Upload>& ups, hipStream_t s) {
   return RGD_OK;
 }
 
+
 // Host description of the rows of one step.
 struct HostRows {
   std::vector<int> prompt, base, plen;
@@ -269,15 +281,18 @@ Rows device_rows(const rgd_model* m, const rgd_kv* kv, int R, int t, bool prefil
   return r;
 }
 
-// split-K factor of a decode GEMM: the smallest power of two that gives at
-// least one workgroup per CU (equal splits measured best), at most
-// kMaxSplitK, at least 4 steps of 64 k per split, within the partial buffers
-int pick_splits(int groups, int mblocks, int K, int R, int cap_rows) {
+// split-K factor of a bf16 GEMM: a function of its shape only (never of the
+// number of rows), so that a row's arithmetic does not depend on which other
+// rows share the launch.  The smallest power of two that gives at least one
+// workgroup per CU for one 64-row block (equal splits measured best), at most
+// kMaxSplitK, with at least 4 steps of 64 k per split.
+int pick_splits(int groups, int K) {
   int ks = 1;
-  while (ks < kMaxSplitK && (long long)groups * mblocks * ks < 256) ks *= 2;
-  while (ks > 1 && (K / 64 / ks < 4 || ks * std::max(R, 1) > cap_rows)) ks /= 2;
+  while (ks < kMaxSplitK && (long long)groups * ks < 256) ks *= 2;
+  while (ks > 1 && K / 64 / ks < 4) ks /= 2;
   return ks;
 }
+
 
 // -------------------------------------------------------------- attention --
 int run_attention(rgd_model* m, const KVLayout& kvl, const Rows& rows, const HostRows& h,
@@ -298,13 +313,14 @@ int run_attention(rgd_model* m, const KVLayout& kvl, const Rows& rows, const Hos
   a.tail_chunk = kTailChunk;
   a.tail_chunks = 0;  // tails are attended inside the merge kernel
   const int R = rows.R;
-  const int cap = (int)std::min<long long>(kMaxParts, (long long)kMaxParts * m->max_rows / std::max(R, 1));
+  const int cap = kMaxParts;  // the partial buffers hold kMaxParts x max_rows rows
   if (m->bf16) {
-    int S = force_splits;
-    if (S <= 0) S = (int)cdiv(256, (long long)c.n_kv_heads * a.nrblocks);
-    S = (int)std::max<long long>(1, std::min<long long>(S, cdiv(std::max(h.maxplen, 1), 64)));
-    S = std::min(S, cap - a.tail_chunks);
-    a.split_len = (int)cdiv(cdiv(std::max(h.maxplen, 1), S), 64) * 64;
+    if (force_splits > 0) {  // kernel-level entry point: an explicit split count
+      const int S = (int)std::max<long long>(1, std::min<long long>(force_splits, cdiv(std::max(h.maxplen, 1), 64)));
+      a.split_len = (int)cdiv(cdiv(std::max(h.maxplen, 1), S), 64) * 64;
+    } else {
+      a.split_len = kvl.split_len;
+    }
     a.splits = (int)cdiv(std::max(h.maxplen, 1), a.split_len);
   } else {
     a.split_len = 256;
@@ -376,9 +392,7 @@ int forward_rows(rgd_model* m, rgd_kv* kv, const Rows& rows, const HostRows& h, 
               : residual_rmsnorm<float>(m->x, parts, np, stride, (const float*)gain, c.rms_eps, R, d,
                                         (float*)m->xn, s);
   };
-  auto splits = [&](int mode, int N, int K) {
-    return bf ? pick_splits(gemm_groups(mode, N), mblocks, K, R, m->part_rows) : 1;
-  };
+  auto splits = [&](int mode, int N, int K) { return bf ? pick_splits(gemm_groups(mode, N), K) : 1; };
   for (int l = 0; l < c.n_layers; ++l) {
     const rgd_layer_weights& L = m->layers[l];
     const KVLayout kvl = kv->layer(l);
@@ -617,7 +631,15 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
   m->lm_head = w->lm_head;
   m->layers.assign(w->layers, w->layers + cfg->n_layers);
   m->max_rows = max_rows;
-  m->part_rows = std::max(max_rows, 16 * 64);
+  // split-K partials: every row of a step times the largest split factor of
+  // the model's projections
+  const int ksmax = cfg->dtype == RGD_DTYPE_BF16
+                        ? std::max({pick_splits(gemm_groups(GEMM_STORE, (cfg->n_heads + 2 * cfg->n_kv_heads) * cfg->head_dim),
+                                                cfg->d_model),
+                                    pick_splits(gemm_groups(GEMM_STORE, cfg->d_model), cfg->n_heads * cfg->head_dim),
+                                    pick_splits(gemm_groups(GEMM_STORE, cfg->d_model), cfg->ffn_dim)})
+                        : 1;
+  m->part_rows = max_rows * ksmax;
   const int R = max_rows, d = cfg->d_model, Hq = cfg->n_heads, Hkv = cfg->n_kv_heads, D = cfg->head_dim;
   m->nqkv = (Hq + 2 * Hkv) * D;
   m->ntiles = m->bf16 ? gemm_groups(GEMM_LOGITS, cfg->vocab) : (int)cdiv(cfg->vocab, 64);
@@ -1181,6 +1203,7 @@ int32_t rgd_kernel_attention(rgd_model* m, const void* q, int32_t R, const int32
   kvl.P = max_prefix;
   kvl.VP = v_stride(max_prefix);
   kvl.page_size = page_size;
+  kvl.split_len = prefix_split_len(max_prefix, max_prompts, m->cfg.n_kv_heads);
   // q is read from the model's q buffer: copy the caller's q there first
   const size_t qbytes = (size_t)R * m->cfg.n_heads * m->cfg.head_dim * m->esz;
   HIP_OK(hipMemcpyAsync(m->q, q, qbytes, hipMemcpyDeviceToDevice, s));

@@ -39,10 +39,10 @@ def head_model(rgd):
     mini = synth.scaled(w, name="lm-mini", ffn=128, n_heads=1, n_kv_heads=1)
     small = synth.model_weights(synth.scaled(mini, vocab=128))
     ws = synth.Weights(mini, small.embed, small.final_norm, head, small.layers)
-    return session.build_model(ws, max_rows=64, max_pos=64), head
+    return session.build_model(ws, max_rows=256, max_pos=64), head
 
 
-@pytest.mark.parametrize("R", [1, 16, 37, 64])
+@pytest.mark.parametrize("R", [1, 16, 37, 64, 100, 256])
 def test_lm_head_bf16_full_vocab(rgd, head_model, R):
     from paper_2607_20791_amd import session
     t = torch()
@@ -54,7 +54,7 @@ def test_lm_head_bf16_full_vocab(rgd, head_model, R):
     rgd.kernel_lm_head(m, session.to_device(h), logits)
     t.cuda.synchronize()
     got = logits.cpu().numpy()
-    rows = sorted({0, R // 2, R - 1})
+    rows = sorted({0, R // 2, R - 1} | ({63, 64, 127, 128, 200} & set(range(R))))
     want = om.linear(head, om.widen(h[rows]))
     err = rel_err(got[rows], want)
     print("lm head rel err", err.max())
