@@ -223,9 +223,10 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
   }
 }
 
-// Row tiles per workgroup follow M (16, 32, 64, 128 or 256 rows), so every
-// weight panel is streamed once for up to 256 rows; wider tiles stage X one
-// step at a time (LDS).  The tile height never changes a row's arithmetic.
+// Row tiles per workgroup follow M (16, 32, 64 or 128 rows; larger M takes
+// several 128-row blocks, whose weight reads then largely hit in L2); the
+// 128-row tile stages X one step at a time (LDS).  The tile height never
+// changes a row's arithmetic.
 template <int NT, int NW, int SW, int MODE, int XS>
 hipError_t launch_bf16(const GemmArgs& a, int ngroups, hipStream_t s) {
   const int splits = a.splits;
@@ -236,10 +237,8 @@ hipError_t launch_bf16(const GemmArgs& a, int ngroups, hipStream_t s) {
     hipLaunchKernelGGL((gemm_bf16_kernel<2, NT, NW, SW, MODE, XS>), dim3(ngroups, 1, splits), blk, 0, s, a);
   } else if (a.M <= 64) {
     hipLaunchKernelGGL((gemm_bf16_kernel<4, NT, NW, SW, MODE, XS>), dim3(ngroups, 1, splits), blk, 0, s, a);
-  } else if (a.M <= 128) {
-    hipLaunchKernelGGL((gemm_bf16_kernel<8, NT, NW, SW, MODE, 1>), dim3(ngroups, 1, splits), blk, 0, s, a);
   } else {
-    hipLaunchKernelGGL((gemm_bf16_kernel<16, NT, NW, SW, MODE, 1>), dim3(ngroups, (a.M + 255) / 256, splits), blk,
+    hipLaunchKernelGGL((gemm_bf16_kernel<8, NT, NW, SW, MODE, 1>), dim3(ngroups, (a.M + 127) / 128, splits), blk,
                        0, s, a);
   }
   return hipGetLastError();
