@@ -10,25 +10,39 @@ namespace {
 
 constexpr int kNormThreads = 1024;
 
-// Row RMSNorm over v[0..d) held as float4 chunks (thread i owns chunks
-// i, i + blockDim, ...); writes xn = v / sqrt(mean(v^2) + eps) * g.
+// Each thread owns up to kChunks float4 chunks of a row (chunk c of thread t
+// covers elements (t + c * blockDim) * 4 .. +3), keeps them in registers
+// through the residual update and the norm, and issues all its loads (x,
+// split partials, gain) before using any: one round trip to memory per row.
+constexpr int kChunks = 4;  // d <= kChunks * 4 * kNormThreads = 16384
+
+RGD_DEV float4 load4(const float* p) { return *(const float4*)p; }
+RGD_DEV float4 load4(const bf16_t* p) {
+  const uint2 u = *(const uint2*)p;
+  return float4{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u), __uint_as_float(u.y << 16),
+                __uint_as_float(u.y & 0xFFFF0000u)};
+}
+RGD_DEV void store4(float* p, float4 v) { *(float4*)p = v; }
+RGD_DEV void store4(bf16_t* p, float4 v) { *(uint2*)p = uint2{pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w)}; }
+
+// xn = v / sqrt(mean(v^2) + eps) * g for the chunks held in registers
 template <typename T>
-RGD_DEV void norm_store(const float* v, int d, const float* g, float eps, T* xn) {
+RGD_DEV void norm_store(const float4 (&v)[kChunks], const float4 (&gg)[kChunks], int d, float eps, T* xn) {
   __shared__ float red[16];
   float ss = 0.f;
-  for (int i = threadIdx.x * 4; i < d; i += blockDim.x * 4) {
-    const float4 a = *(const float4*)(v + i);
-    ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
+#pragma unroll
+  for (int c = 0; c < kChunks; ++c) {
+    const int i = (threadIdx.x + c * blockDim.x) * 4;
+    if (i < d) ss += v[c].x * v[c].x + v[c].y * v[c].y + v[c].z * v[c].z + v[c].w * v[c].w;
   }
   ss = block_sum(ss, red);
   const float inv = rsqrtf(ss / float(d) + eps);
-  for (int i = threadIdx.x * 4; i < d; i += blockDim.x * 4) {
-    const float4 a = *(const float4*)(v + i);
-    const float4 gg = *(const float4*)(g + i);
-    store_f(xn + i, a.x * inv * gg.x);
-    store_f(xn + i + 1, a.y * inv * gg.y);
-    store_f(xn + i + 2, a.z * inv * gg.z);
-    store_f(xn + i + 3, a.w * inv * gg.w);
+#pragma unroll
+  for (int c = 0; c < kChunks; ++c) {
+    const int i = (threadIdx.x + c * blockDim.x) * 4;
+    if (i < d)
+      store4(xn + i, float4{v[c].x * inv * gg[c].x, v[c].y * inv * gg[c].y, v[c].z * inv * gg[c].z,
+                            v[c].w * inv * gg[c].w});
   }
 }
 
@@ -41,9 +55,21 @@ __global__ __launch_bounds__(kNormThreads) void embed_rmsnorm_kernel(const int* 
   // outside the embedding table
   const long long t = min(max(tok[(long long)r * tok_stride], 0), V - 1);
   float* xr = x + (long long)r * d;
-  for (int i = threadIdx.x; i < d; i += blockDim.x) xr[i] = load_f(E + t * d + i);
-  __syncthreads();
-  norm_store(xr, d, g, eps, xn + (long long)r * d);
+  float4 v[kChunks], gg[kChunks];
+#pragma unroll
+  for (int c = 0; c < kChunks; ++c) {
+    const int i = (threadIdx.x + c * blockDim.x) * 4;
+    if (i < d) {
+      v[c] = load4(E + t * d + i);
+      gg[c] = load4(g + i);
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < kChunks; ++c) {
+    const int i = (threadIdx.x + c * blockDim.x) * 4;
+    if (i < d) store4(xr + i, v[c]);
+  }
+  norm_store(v, gg, d, eps, xn + (long long)r * d);
 }
 
 template <typename T>
@@ -52,34 +78,37 @@ __global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(float* x
                                                                       float eps, int d, T* xn) {
   const int r = blockIdx.x;
   float* xr = x + (long long)r * d;
-  if (nparts > 0) {
-    const float* pr = parts + (long long)r * d;
-    for (int i = threadIdx.x * 4; i < d; i += blockDim.x * 4) {
-      float4 v = *(float4*)(xr + i);
+  const float* pr = parts + (long long)r * d;
+  float4 v[kChunks], gg[kChunks];
+#pragma unroll
+  for (int c = 0; c < kChunks; ++c) {
+    const int i = (threadIdx.x + c * blockDim.x) * 4;
+    if (i < d) {
       float4 q[kMaxSplitK];
 #pragma unroll
       for (int p = 0; p < kMaxSplitK; ++p)
         if (p < nparts) q[p] = *(const float4*)(pr + p * part_stride + i);
+      v[c] = *(const float4*)(xr + i);
+      gg[c] = *(const float4*)(g + i);
 #pragma unroll
       for (int p = 0; p < kMaxSplitK; ++p)
         if (p < nparts) {
-          v.x += q[p].x;
-          v.y += q[p].y;
-          v.z += q[p].z;
-          v.w += q[p].w;
+          v[c].x += q[p].x;
+          v[c].y += q[p].y;
+          v[c].z += q[p].z;
+          v[c].w += q[p].w;
         }
-      *(float4*)(xr + i) = v;
+      if (nparts > 0) store4(xr + i, v[c]);
     }
-    __syncthreads();
   }
-  norm_store(xr, d, g, eps, xn + (long long)r * d);
+  norm_store(v, gg, d, eps, xn + (long long)r * d);
 }
 
 // One workgroup per (row, group of 8 heads of the fused q|k|v output).  The
 // rotation of position pos, pair j is (cos, sin) = rope_cs[pos][j] (a table
 // computed once on the host in fp64).
 template <typename T>
-__global__ __launch_bounds__(256) void qkv_rope_kernel(const float* parts, int nparts, long long part_stride,
+__global__ __launch_bounds__(1024) void qkv_rope_kernel(const float* parts, int nparts, long long part_stride,
                                                        Rows rows, int Hq, int Hkv, int D, const float2* rope_cs,
                                                        int max_pos, T* q, KVLayout kv) {
   const int r = blockIdx.x;
@@ -119,7 +148,7 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* parts, int n
     vdstride = ps;
   }
   const int nh = h1 - h0;
-  for (int i = threadIdx.x; i < nh * half; i += 256) {
+  for (int i = threadIdx.x; i < nh * half; i += blockDim.x) {
     const int h = h0 + i / half, j = i % half;
     const int base = h * D;
     if (h < Hq + Hkv) {  // rotated q or k pair (j, j + D/2)
@@ -143,7 +172,7 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* parts, int n
 template <typename T>
 hipError_t embed_rmsnorm(const int* tok, int tok_stride, int R, const T* E, int d, int V, float* x,
                          const float* g, float eps, T* xn, hipStream_t s) {
-  if (d % 4) return hipErrorInvalidValue;
+  if (d % 4 || d > kChunks * 4 * kNormThreads) return hipErrorInvalidValue;
   hipLaunchKernelGGL(embed_rmsnorm_kernel<T>, dim3(R), dim3(kNormThreads), 0, s, tok, tok_stride, E, d, V, x,
                      g, eps, xn);
   return hipGetLastError();
@@ -152,7 +181,7 @@ hipError_t embed_rmsnorm(const int* tok, int tok_stride, int R, const T* E, int 
 template <typename T>
 hipError_t residual_rmsnorm(float* x, const float* parts, int nparts, long long part_stride, const float* g,
                             float eps, int R, int d, T* xn, hipStream_t s) {
-  if (d % 4 || nparts < 0 || nparts > kMaxSplitK) return hipErrorInvalidValue;
+  if (d % 4 || d > kChunks * 4 * kNormThreads || nparts < 0 || nparts > kMaxSplitK) return hipErrorInvalidValue;
   hipLaunchKernelGGL(residual_rmsnorm_kernel<T>, dim3(R), dim3(kNormThreads), 0, s, x, parts, nparts, part_stride,
                      g, eps, d, xn);
   return hipGetLastError();
@@ -163,7 +192,9 @@ hipError_t qkv_rope_store(const float* parts, int nparts, long long part_stride,
                           int Hkv, int D, const float* rope_cs, int max_pos, T* q, const KVLayout& kv,
                           hipStream_t s) {
   if (D > 256 || (D & 1) || nparts < 1 || nparts > kMaxSplitK) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(qkv_rope_kernel<T>, dim3(rows.R, (Hq + 2 * Hkv + 7) / 8), dim3(256), 0, s, parts, nparts,
+  // one thread per (head of the group of 8, rotation pair)
+  const int threads = std::max(64, 8 * (D / 2));
+  hipLaunchKernelGGL(qkv_rope_kernel<T>, dim3(rows.R, (Hq + 2 * Hkv + 7) / 8), dim3(threads), 0, s, parts, nparts,
                      part_stride, rows, Hq, Hkv, D, (const float2*)rope_cs, max_pos, q, kv);
   return hipGetLastError();
 }
