@@ -28,9 +28,9 @@ sys.path.insert(0, ROOT)
 METRIC = "gated decode tokens/sec (probe+N branches) + % HBM roofline, attn & sampler"
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
-# the library times every TIMING_PERIOD-th launch of each unit (launch 0, P,
-# 2P, ... of each sampling call); the others run without event records
-TIMING_PERIOD = 4
+# the library times every unit of decode steps 1, 1+P, 1+2P, ... of each
+# sampling call (P = TIMING_PERIOD); the other steps run without event records
+TIMING_PERIOD = 8
 
 
 def log(*a):

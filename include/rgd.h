@@ -222,11 +222,13 @@ enum rgd_timer {
 };
 
 /* period >= 1: from now on the model records HIP events on the work stream
- * around every period-th launch of each timed unit (at most 8192 timed
- * launches per unit between reads; later launches are not timed).  A period
- * above 1 keeps most launches free of event records, which otherwise leave
- * small idle gaps on the stream.  period == 0 stops recording; negative is
- * RGD_E_INVALID_ARG.  Events are created on the first enable, not on the
+ * around each timed unit: inside rgd_sample_continuations, for every unit of
+ * decode steps 1, 1 + period, 1 + 2 period, ... (the draw from the prompt's
+ * logits is not timed when period > 1); elsewhere, every launch.  At most
+ * 8192 timed launches per unit between reads; later launches are not timed.
+ * A period above 1 keeps most steps free of event records, which otherwise
+ * leave small idle gaps on the stream.  period == 0 stops recording; negative
+ * is RGD_E_INVALID_ARG.  Events are created on the first enable, not on the
  * decode path. */
 int32_t rgd_timing_enable(rgd_model* m, int32_t period);
 

@@ -129,7 +129,10 @@ struct rgd_model {
   bool timing = false;
   std::vector<hipEvent_t> tev[RGD_TIMER_COUNT];
   int tused[RGD_TIMER_COUNT] = {0};
-  long long tcount[RGD_TIMER_COUNT] = {0};  // launches seen while timing (every tperiod-th is timed)
+  // steps of a sampling call are timed when tstep % tperiod == 0 (tstep = the
+  // decode step - 1; the draw from the prompt logits is never timed); outside
+  // the sampling loop tstep is 0 and every launch is timed
+  int tstep = 0;
   int tperiod = 1;
   ~rgd_model() {
     for (auto& v : tev)
@@ -194,7 +197,7 @@ struct TimeScope {
   hipStream_t s;
   bool on;
   TimeScope(rgd_model* m_, int unit_, hipStream_t s_) : m(m_), unit(unit_), s(s_) {
-    on = m->timing && m->tcount[unit]++ % m->tperiod == 0 && m->tused[unit] < (int)m->tev[unit].size() / 2;
+    on = m->timing && m->tstep % m->tperiod == 0 && m->tused[unit] < (int)m->tev[unit].size() / 2;
     if (on) (void)hipEventRecord(m->tev[unit][2 * m->tused[unit]], s);
   }
   ~TimeScope() {
@@ -1093,8 +1096,14 @@ int32_t rgd_sample_continuations(rgd_model* m, rgd_kv* kv, const float* last_log
                      m->row_map, V, z0);
   HIP_OK(hipGetLastError());
   if (T > 0.f) HIP_OK(chunk_max(z0, V, R, V, kSampleChunk, m->tilemax, s));
+  struct StepIndex {  // restores the timing step index on every exit
+    rgd_model* m;
+    ~StepIndex() { m->tstep = 0; }
+  } step_index{m};
+  m->tstep = -1;  // the first draw (prompt logits) is not timed
   RGD_TRY(select_tokens(m, z0, V, R, m->tilemax, m->nchunks, T, min_p, sd, 0u, out, steps, 0, m->cur_tok, s));
   for (int st = 1; st < steps; ++st) {
+    m->tstep = st - 1;
     TimeScope tstep(m, RGD_TIMER_STEP, s);
     Rows rows = device_rows(m, kv, R, st - 1, false);
     const int* feed = forced ? forced + (st - 1) : m->cur_tok;
@@ -1138,7 +1147,6 @@ int32_t rgd_timing_enable(rgd_model* m, int32_t period) {
   }
   m->timing = period != 0;
   m->tperiod = std::max(period, 1);
-  for (auto& c : m->tcount) c = 0;  // the first launch after an enable is timed
   return RGD_OK;
 }
 
