@@ -314,10 +314,14 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
     lt += __shfl_xor(lt, 32, 64);
     if (vok[nt]) {
       const long long idx = ((long long)s * a.rows.R + vrow[nt]) * a.Hq + vhead[nt];
-      float* po = a.part_o + idx * D;
+      // normalised partial output, stored in bf16 (bounded by max|V|; the
+      // merged output is bf16 as well)
+      bf16_t* po = (bf16_t*)a.part_o + idx * D;
       const float inv = lt > 0.f ? 1.0f / lt : 0.f;
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt) *(f32x4*)(po + dt * 16 + grp * 4) = o[dt][nt] * inv;
+      for (int dt = 0; dt < 8; ++dt)
+        *(u32x2*)(po + dt * 16 + grp * 4) = u32x2{pack2(o[dt][nt][0] * inv, o[dt][nt][1] * inv),
+                                                  pack2(o[dt][nt][2] * inv, o[dt][nt][3] * inv)};
       if (grp == 0) a.part_lse[idx] = lt > 0.f ? (m[nt] + __log2f(lt)) * kLn2 : -INFINITY;
     }
   }
@@ -594,15 +598,15 @@ __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t
   // request those of this wave's first head now so their latency overlaps the
   // tail attention (splits beyond kPrefetch are loaded in the merge).
   const int S = a.splits;
-  constexpr int kPrefetch = 16;
+  constexpr int kPrefetch = 32;
   const long long pstep = R * a.Hq * D;
-  float2 pre[kPrefetch];
+  uint32_t pre[kPrefetch];  // bf16 pairs
   float pre_lse = -INFINITY;
   if (wave < G) {
     const int head = g * G + wave;
-    const float* po = a.part_o + ((long long)r * a.Hq + head) * D + 2 * lane;
+    const bf16_t* po = (const bf16_t*)a.part_o + ((long long)r * a.Hq + head) * D + 2 * lane;
 #pragma unroll
-    for (int k = 0; k < kPrefetch; ++k) pre[k] = k < S ? *(const float2*)(po + k * pstep) : float2{0.f, 0.f};
+    for (int k = 0; k < kPrefetch; ++k) pre[k] = k < S ? *(const uint32_t*)(po + k * pstep) : 0u;
     if (lane < S) pre_lse = a.part_lse[((long long)lane * R + r) * a.Hq + head];
   }
 
@@ -729,24 +733,24 @@ __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t
     const float inv = den > 0.f ? 1.f / den : 0.f;
     const float ft = tl > 0.f ? wt * inv / tl : 0.f;  // applied to the unnormalised tail sum
     float o0 = ft * to0, o1 = ft * to1;
-    const float* po = a.part_o + ((long long)r * a.Hq + head) * D + 2 * lane;
+    const bf16_t* po = (const bf16_t*)a.part_o + ((long long)r * a.Hq + head) * D + 2 * lane;
     // weight of split sp sits in lane sp; fixed split order
 #pragma unroll
     for (int k = 0; k < kPrefetch; ++k) {
       if (k < S) {
-        const float2 v = first ? pre[k] : *(const float2*)(po + k * pstep);
+        const uint32_t v = first ? pre[k] : *(const uint32_t*)(po + k * pstep);
         const float wk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), k)) * inv;
-        o0 += wk * v.x;
-        o1 += wk * v.y;
+        o0 += wk * __uint_as_float(v << 16);
+        o1 += wk * __uint_as_float(v & 0xFFFF0000u);
       }
     }
 #pragma unroll
     for (int k = kPrefetch; k < kMergeMaxSplits; ++k) {
       if (k < S) {
-        const float2 v = *(const float2*)(po + k * pstep);
+        const uint32_t v = *(const uint32_t*)(po + k * pstep);
         const float wk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), k)) * inv;
-        o0 += wk * v.x;
-        o1 += wk * v.y;
+        o0 += wk * __uint_as_float(v << 16);
+        o1 += wk * __uint_as_float(v & 0xFFFF0000u);
       }
     }
     *(uint32_t*)(out + ((long long)r * a.Hq + head) * D + 2 * lane) = pack_bf16x2(o0, o1);

@@ -89,7 +89,7 @@ struct AttnArgs {
   Rows rows;
   KVLayout kv;
   int Hq, Hkv, D;
-  float* part_o;            // [nparts][R][Hq][D]
+  float* part_o;            // [nparts][R][Hq][D], fp32; the bf16 prefix path stores bf16 here
   float* part_lse;          // [nparts][R][Hq]
   int nparts;
   // prefix (shared) part
