@@ -39,6 +39,10 @@ RGD_DEV float exp2_raw(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // Exponent headroom of the lazy softmax rescale (log2 units).
 constexpr float kLazy = 8.f;
+// Exponent reference of a query vector with no visible position yet: finite,
+// so that s*scale - kNoRef is huge for a visible score and -inf (never NaN)
+// for a masked one.
+constexpr float kNoRef = -3.0e38f;
 
 #ifndef RGD_ATTN_NW
 #define RGD_ATTN_NW 8
@@ -71,7 +75,7 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
   constexpr int D = 128, TP = 64, NT = NW * 64, NB = 3;
   static_assert(NW * NQ * 16 == 256, "a workgroup covers 256 query vectors");
   const int s = blockIdx.x, g = blockIdx.y;
-  const int4 rb = a.rblocks[blockIdx.z];
+  const int4 rb = blockIdx.z == 0 ? a.rblock0 : a.rblocks[blockIdx.z];
   const int r0 = rb.x, nr = rb.y, b = rb.z, maxplen = rb.w;
   const int lo = s * a.split_len;
   const int hi = min(lo + a.split_len, maxplen);
@@ -107,15 +111,20 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
   const bf16_t* vbase = (const bf16_t*)a.kv.prefix_v + bg * a.kv.VP * D;
   const float scale = rsqrtf(float(D)) * kLog2e;
 
-  float m[NQ], lsum[NQ];
-  f32x4 o[8][NQ];
+  // m: exponent reference (log2 units) of a query vector; kNoRef until some
+  // position of it is visible.  lacc: running sum of its weights, produced by
+  // the P V MFMA against an all-ones A operand (every element holds the sum,
+  // taken over the same bf16 weights as the output).
+  float m[NQ];
+  f32x4 o[8][NQ], lacc[NQ];
 #pragma unroll
   for (int nt = 0; nt < NQ; ++nt) {
-    m[nt] = -INFINITY;
-    lsum[nt] = 0.f;
+    m[nt] = kNoRef;
+    lacc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) o[dt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
+  const u32x4 ones = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};  // bf16 1.0 x 8
 
   // Register staging of the next tile.  Nothing reads these registers before
   // store_tile, so the loads stay in flight through a whole tile of compute;
@@ -182,15 +191,18 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
     }
   };
 
-  // Masking and the exponent reference of a half starting at position p0.
+  // Masking, exponent arguments and the exponent reference of a half starting
+  // at position p0; on return sc holds the base-2 exponents s*scale - m.
   // Positions past a query vector's end are masked (skipped when the half is
   // visible to every query vector of the wave).  Lazy rescaling: the
   // reference m of a query vector only moves when some score exceeds it by
-  // more than kLazy, so probabilities stay below 2^kLazy and the accumulators
-  // are rescaled on few halves.  The common path needs no cross-lane
-  // reduction: each lane tests its own scores, and only when some lane of the
-  // wave fails are the maxima reduced over the four lane groups that share a
-  // query vector.
+  // more than kLazy, so weights stay below 2^kLazy and the accumulators are
+  // rescaled on few halves.  The common path needs no cross-lane reduction:
+  // each lane tests its own exponents (results of arithmetic, so their
+  // maximum needs no NaN quieting), and only when some lane of the wave fails
+  // are the raw maxima reduced over the four lane groups that share a query
+  // vector.  A vector with no visible position yet has m = kNoRef: its
+  // exponents are huge (a move) for visible scores and -inf for masked ones.
   auto prepare = [&](int p0, f32x4 (&sc)[2][NQ]) {
     bool full = true;
 #pragma unroll
@@ -204,32 +216,45 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
           for (int i = 0; i < 4; ++i)
             if (p0 + grp * 8 + e * 4 + i >= vend[nt]) sc[e][nt][i] = -INFINITY;
     }
-    float lmax[NQ];
+    f32x4 t[2][NQ];
     bool grow = false;
 #pragma unroll
     for (int nt = 0; nt < NQ; ++nt) {
-      const float x = fmaxf(fmaxf(fmaxf(sc[0][nt][0], sc[0][nt][1]), fmaxf(sc[0][nt][2], sc[0][nt][3])),
-                            fmaxf(fmaxf(sc[1][nt][0], sc[1][nt][1]), fmaxf(sc[1][nt][2], sc[1][nt][3])));
-      lmax[nt] = x * scale;
-      grow |= lmax[nt] > m[nt] + kLazy;
+#pragma unroll
+      for (int e = 0; e < 2; ++e)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) t[e][nt][i] = fmaf(sc[e][nt][i], scale, -m[nt]);
+      const float x = fmaxf(fmaxf(fmaxf(t[0][nt][0], t[0][nt][1]), fmaxf(t[0][nt][2], t[0][nt][3])),
+                            fmaxf(fmaxf(t[1][nt][0], t[1][nt][1]), fmaxf(t[1][nt][2], t[1][nt][3])));
+      grow |= x > kLazy;
     }
     if (__any(grow)) {
 #pragma unroll
       for (int nt = 0; nt < NQ; ++nt) {
-        float x = lmax[nt];
+        float x = fmaxf(fmaxf(fmaxf(sc[0][nt][0], sc[0][nt][1]), fmaxf(sc[0][nt][2], sc[0][nt][3])),
+                        fmaxf(fmaxf(sc[1][nt][0], sc[1][nt][1]), fmaxf(sc[1][nt][2], sc[1][nt][3]))) * scale;
         x = fmaxf(x, __shfl_xor(x, 16, 64));
         x = fmaxf(x, __shfl_xor(x, 32, 64));
         // only a query vector whose own maximum passed its reference by more
         // than kLazy moves: its arithmetic never depends on the other query
         // vectors of the wave (rows batched together give the same results)
         if (x > m[nt] + kLazy) {
-          const float alpha = exp2_raw(m[nt] - x);  // 0 on the first visible half
-          lsum[nt] *= alpha;
+          const float alpha = exp2_raw(m[nt] - x);  // 0 when moving from kNoRef
+          lacc[nt] *= alpha;
 #pragma unroll
           for (int dt = 0; dt < 8; ++dt) o[dt][nt] *= alpha;
           m[nt] = x;
+#pragma unroll
+          for (int e = 0; e < 2; ++e)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) t[e][nt][i] = fmaf(sc[e][nt][i], scale, -x);
         }
       }
+    }
+#pragma unroll
+    for (int nt = 0; nt < NQ; ++nt) {
+      sc[0][nt] = t[0][nt];
+      sc[1][nt] = t[1][nt];
     }
   };
 
@@ -239,17 +264,12 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
   // 16 fragment reads go through a 3-slot register ring, NQ MFMAs each.  After
   // the last half kb holds stale data and nxt is simply not used.
   auto stream = [&](int kb, int kh, int vb, int vh, f32x4 (&cur)[2][NQ], f32x4 (&nxt)[2][NQ]) {
-    float msub[NQ];
-#pragma unroll
-    for (int nt = 0; nt < NQ; ++nt) msub[nt] = m[nt] == -INFINITY ? INFINITY : m[nt];  // nothing visible: p = 0
     auto frag = [&](int f) -> u32x4 { return f < 8 ? k_frag(kb, kh, f >> 2, f & 3) : v_frag(vb, f - 8, vh); };
     u32x4 ring[3];
     ring[0] = frag(0);
     ring[1] = frag(1);
-    float ps[NQ], plo[NQ];
-    uint32_t pw[NQ][4];  // packed probabilities, word 2e + (i >> 1)
-#pragma unroll
-    for (int nt = 0; nt < NQ; ++nt) ps[nt] = 0.f;
+    float plo[NQ];
+    uint32_t pw[NQ][4];  // packed weights, word 2e + (i >> 1)
 #pragma unroll
     for (int f = 0; f < 16; ++f) {
       if (f + 2 < 16) ring[(f + 2) % 3] = frag(f + 2);
@@ -265,8 +285,7 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
         // to bf16 as soon as both halves exist
 #pragma unroll
         for (int nt = 0; nt < NQ; ++nt) {
-          const float x = exp2_raw(fmaf(cur[e][nt][ks], scale, -msub[nt]));
-          ps[nt] += x;
+          const float x = exp2_raw(cur[e][nt][ks]);
           if (ks & 1) pw[nt][e * 2 + (ks >> 1)] = pack2(plo[nt], x);
           else plo[nt] = x;
         }
@@ -275,10 +294,13 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
 #pragma unroll
         for (int nt = 0; nt < NQ; ++nt)
           o[dt][nt] = mfma16x16x32(ring[f % 3], u32x4{pw[nt][0], pw[nt][1], pw[nt][2], pw[nt][3]}, o[dt][nt]);
+        if (dt == 7) {
+#pragma unroll
+          for (int n2 = 0; n2 < NQ; ++n2)
+            lacc[n2] = mfma16x16x32(ones, u32x4{pw[n2][0], pw[n2][1], pw[n2][2], pw[n2][3]}, lacc[n2]);
+        }
       }
     }
-#pragma unroll
-    for (int nt = 0; nt < NQ; ++nt) lsum[nt] += ps[nt];
   };
 
   const int ntile = hi > lo ? (hi - lo + TP - 1) / TP : 0;
@@ -310,8 +332,7 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
 
 #pragma unroll
   for (int nt = 0; nt < NQ; ++nt) {
-    float lt = lsum[nt] + __shfl_xor(lsum[nt], 16, 64);
-    lt += __shfl_xor(lt, 32, 64);
+    const float lt = lacc[nt][0];
     if (vok[nt]) {
       const long long idx = ((long long)s * a.rows.R + vrow[nt]) * a.Hq + vhead[nt];
       // normalised partial output, stored in bf16 (bounded by max|V|; the

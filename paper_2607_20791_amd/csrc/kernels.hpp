@@ -94,6 +94,7 @@ struct AttnArgs {
   int nparts;
   // prefix (shared) part
   const int4* rblocks; int nrblocks;  // (r0, nr, prompt, maxplen) row blocks for the MFMA path
+  int4 rblock0;                       // rblocks[0], passed by value (no dependent load)
   int splits; int split_len;          // prefix splits (part index 0..splits-1)
   // tail part
   int tail_len;             // visible tail positions (decode), 0 for prefill

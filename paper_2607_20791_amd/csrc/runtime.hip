@@ -312,6 +312,7 @@ int run_attention(rgd_model* m, const KVLayout& kvl, const Rows& rows, const Hos
   a.part_lse = m->part_lse;
   a.rblocks = m->d_rblocks;
   a.nrblocks = (int)h.blocks.size();
+  if (!h.blocks.empty()) a.rblock0 = h.blocks[0];
   a.tail_len = tail_len;
   a.tail_chunk = kTailChunk;
   a.tail_chunks = 0;  // tails are attended inside the merge kernel
