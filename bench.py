@@ -57,7 +57,7 @@ def measured_traffic(name="lm_head_c2_traffic.md"):
 def algorithmic(w, R, P, tails):
     """Algorithmic bytes / flops per launch of the three named kernels."""
     d, V, Hq, Hkv, D = w.d_model, w.vocab, w.n_heads, w.n_kv_heads, w.head_dim
-    ntiles = (V + 255) // 256   # row maxima the LM head emits (one per 256-column group)
+    ntiles = (V + 511) // 512   # row maxima the LM head emits (one per 512-column group)
     lm_bytes = V * d * 2 + R * d * 2 + R * V * 4 + R * ntiles * 4
     lm_flops = 2.0 * R * d * V
     att_bytes = [2 * P * Hkv * D * 2 + R * 2 * t * Hkv * D * 2 + 2 * R * Hq * D * 2 for t in tails]

@@ -296,14 +296,15 @@ size_t packed_elems(int N, int K) { return (size_t)((N + 15) / 16) * 16 * K; }
 int gemm_groups(int mode, int N) {
   switch (mode) {
     case GEMM_SILU: return (N + 31) / 32;     // 2 gate + 2 up panels of 16 features
-    case GEMM_LOGITS: return (N + 255) / 256;  // 8 waves x 2 panels
+    case GEMM_LOGITS: return (N + 511) / 512;  // 8 waves x 4 panels
     default: return (N + 127) / 128;          // 8 waves x 1 panel
   }
 }
 
 // Launch shapes (panels per wave, waves, weight steps in flight, X steps per
 // LDS stage), chosen by measurement at the decode shapes of an 8B-class layer:
-// split-K projections <1, 8, 4, 2>, SwiGLU <1, 4, 4, 4>, LM head <2, 8, 2, 1>.
+// split-K projections <1, 8, 4, 2>, SwiGLU <1, 4, 4, 4>, LM head <4, 8, 2, 1> (512 columns per
+// workgroup: the X rows every workgroup streams through LDS cost half as much per weight byte).
 hipError_t gemm_bf16(const GemmArgs& a, hipStream_t s) {
   if (a.K % kStep != 0 || a.M < 1 || a.splits < 1 || a.splits > a.K / kStep) return hipErrorInvalidValue;
   const int g = gemm_groups(a.mode, a.N);
@@ -317,7 +318,7 @@ hipError_t gemm_bf16(const GemmArgs& a, hipStream_t s) {
       return launch_bf16<1, 4, 4, GEMM_SILU, 4>(a, g, s);
     case GEMM_LOGITS:
       if (a.splits != 1 || a.ntiles != g) return hipErrorInvalidValue;
-      return launch_bf16<2, 8, 2, GEMM_LOGITS, 1>(a, g, s);
+      return launch_bf16<4, 8, 2, GEMM_LOGITS, 1>(a, g, s);
     default:
       return hipErrorInvalidValue;
   }
