@@ -3,6 +3,7 @@
 // embedding, store of q, append of k/v to the shared prefix or to the row's
 // paged tail).
 #include "kernels.hpp"
+#include "rownorm.hpp"
 
 namespace rgd {
 
@@ -10,66 +11,12 @@ namespace {
 
 constexpr int kNormThreads = 1024;
 
-// Each thread owns up to kChunks float4 chunks of a row (chunk c of thread t
-// covers elements (t + c * blockDim) * 4 .. +3), keeps them in registers
-// through the residual update and the norm, and issues all its loads (x,
-// split partials, gain) before using any: one round trip to memory per row.
-constexpr int kChunks = 4;  // d <= kChunks * 4 * kNormThreads = 16384
-
-RGD_DEV float4 load4(const float* p) { return *(const float4*)p; }
-RGD_DEV float4 load4(const bf16_t* p) {
-  const uint2 u = *(const uint2*)p;
-  return float4{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u), __uint_as_float(u.y << 16),
-                __uint_as_float(u.y & 0xFFFF0000u)};
-}
-RGD_DEV void store4(float* p, float4 v) { *(float4*)p = v; }
-RGD_DEV void store4(bf16_t* p, float4 v) { *(uint2*)p = uint2{pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w)}; }
-
-// xn = v / sqrt(mean(v^2) + eps) * g for the chunks held in registers
-template <typename T>
-RGD_DEV void norm_store(const float4 (&v)[kChunks], const float4 (&gg)[kChunks], int d, float eps, T* xn) {
-  __shared__ float red[16];
-  float ss = 0.f;
-#pragma unroll
-  for (int c = 0; c < kChunks; ++c) {
-    const int i = (threadIdx.x + c * blockDim.x) * 4;
-    if (i < d) ss += v[c].x * v[c].x + v[c].y * v[c].y + v[c].z * v[c].z + v[c].w * v[c].w;
-  }
-  ss = block_sum(ss, red);
-  const float inv = rsqrtf(ss / float(d) + eps);
-#pragma unroll
-  for (int c = 0; c < kChunks; ++c) {
-    const int i = (threadIdx.x + c * blockDim.x) * 4;
-    if (i < d)
-      store4(xn + i, float4{v[c].x * inv * gg[c].x, v[c].y * inv * gg[c].y, v[c].z * inv * gg[c].z,
-                            v[c].w * inv * gg[c].w});
-  }
-}
-
 template <typename T>
 __global__ __launch_bounds__(kNormThreads) void embed_rmsnorm_kernel(const int* tok, int tok_stride, const T* E,
                                                                    int d, int V, float* x, const float* g,
                                                                    float eps, T* xn) {
   const int r = blockIdx.x;
-  // ids come from the sampler or the caller; clamp so that a bad id cannot read
-  // outside the embedding table
-  const long long t = min(max(tok[(long long)r * tok_stride], 0), V - 1);
-  float* xr = x + (long long)r * d;
-  float4 v[kChunks], gg[kChunks];
-#pragma unroll
-  for (int c = 0; c < kChunks; ++c) {
-    const int i = (threadIdx.x + c * blockDim.x) * 4;
-    if (i < d) {
-      v[c] = load4(E + t * d + i);
-      gg[c] = load4(g + i);
-    }
-  }
-#pragma unroll
-  for (int c = 0; c < kChunks; ++c) {
-    const int i = (threadIdx.x + c * blockDim.x) * 4;
-    if (i < d) store4(xr + i, v[c]);
-  }
-  norm_store(v, gg, d, eps, xn + (long long)r * d);
+  embed_norm_row(tok[(long long)r * tok_stride], E, d, V, g, eps, x + (long long)r * d, xn + (long long)r * d);
 }
 
 template <typename T>

@@ -128,6 +128,11 @@ struct SampleArgs {
   int* out; long long out_stride; int out_col;   // token of row r -> out[r*out_stride + out_col]
   int* cur_tok;                   // optional [R] copy of the token (next step's input)
   int* status;                    // device flag: set to 1 on a non-finite row maximum
+  // optional: the next decode step's input row of each drawn token, x = E[tok]
+  // (fp32 [R][d]) and xn = RMSNorm(x) * gain (model dtype), written by the
+  // selecting workgroup (null embed: not fused; needs d % 4 == 0, d <= 4096)
+  const void* embed; int embed_bf16; int d; int vocab;
+  const float* gain; float eps; float* x; void* xn;
 };
 hipError_t minp_sample(const SampleArgs& a, hipStream_t s);
 // rows without producer maxima: chunk maxima into cmax [R][nchunks] and the

@@ -374,19 +374,21 @@ int lm_head(rgd_model* m, const void* x, int ldx, int R, float* logits, hipStrea
 }
 
 // One forward pass of R rows through every layer.  feed: token of row r at
-// feed[r * feed_stride].  Leaves the final normalised hidden state in m->xn.
+// feed[r * feed_stride]; embedded: the input rows (m->x, m->xn) were already
+// written by the sampler for these tokens.  Leaves the final normalised hidden
+// state in m->xn.
 int forward_rows(rgd_model* m, rgd_kv* kv, const Rows& rows, const HostRows& h, const int* feed,
-                 int feed_stride, hipStream_t s) {
+                 int feed_stride, hipStream_t s, bool embedded = false) {
   const rgd_model_config& c = m->cfg;
   const int R = rows.R, d = c.d_model, Hq = c.n_heads, Hkv = c.n_kv_heads, D = c.head_dim;
   const int F = c.ffn_dim;
   const bool bf = m->bf16;
   const int mblocks = (int)cdiv(R, 64);
   const float* g0 = (const float*)m->layers[0].attn_norm;
-  if (bf)
+  if (!embedded && bf)
     HIP_OK(embed_rmsnorm<bf16_t>(feed, feed_stride, R, (const bf16_t*)m->embed, d, c.vocab, m->x, g0, c.rms_eps,
                                  (bf16_t*)m->xn, s));
-  else
+  else if (!embedded)
     HIP_OK(embed_rmsnorm<float>(feed, feed_stride, R, (const float*)m->embed, d, c.vocab, m->x, g0, c.rms_eps,
                                 (float*)m->xn, s));
   auto norm = [&](const float* parts, int np, const void* gain) -> hipError_t {
@@ -534,12 +536,15 @@ __global__ void probe_feed_kernel(const int* prompt, int R, const int* probe_tok
   if (r < R) cur[r] = probe_tokens[(long long)prompt[r] * k + j];
 }
 
-// Selects one token per row from logits z (ldz) with row indirection `map`
-// (null: identity).  T == 0: argmax.
+// Selects one token per row from logits z (ldz).  T == 0: argmax.  With
+// fuse_embed the sampling workgroups also write the next step's input rows
+// (embedding + first RMSNorm into m->x, m->xn) where the shapes allow it;
+// *embedded tells the caller whether they did.
 int select_tokens(rgd_model* m, const float* z, long long ldz, int R, const float* pmax, int npmax, float T,
                   float p_min, const unsigned long long* seeds, unsigned ctr, int* out, long long out_stride,
-                  int out_col, int* cur, hipStream_t s) {
+                  int out_col, int* cur, hipStream_t s, bool fuse_embed = false, bool* embedded = nullptr) {
   const int V = m->cfg.vocab;
+  if (embedded) *embedded = false;
   if (T == 0.f) {
     HIP_OK(argmax_rows(z, ldz, R, V, m->best, s));
     hipLaunchKernelGGL(argmax_finish_kernel, dim3((R + 255) / 256), dim3(256), 0, s, m->best, R, out,
@@ -548,6 +553,18 @@ int select_tokens(rgd_model* m, const float* z, long long ldz, int R, const floa
     return RGD_OK;
   }
   SampleArgs a = sample_args(m, z, ldz, R, V, T, p_min, pmax, npmax, seeds, ctr, out, out_stride, out_col, cur);
+  const int d = m->cfg.d_model;
+  if (fuse_embed && d % 4 == 0 && d <= 4096) {
+    a.embed = m->embed;
+    a.embed_bf16 = m->bf16;
+    a.d = d;
+    a.vocab = V;
+    a.gain = (const float*)m->layers[0].attn_norm;
+    a.eps = m->cfg.rms_eps;
+    a.x = m->x;
+    a.xn = m->xn;
+    if (embedded) *embedded = true;
+  }
   TimeScope ts(m, RGD_TIMER_SAMPLER, s);
   HIP_OK(minp_sample(a, s));
   return RGD_OK;
@@ -1102,18 +1119,22 @@ int32_t rgd_sample_continuations(rgd_model* m, rgd_kv* kv, const float* last_log
     ~StepIndex() { m->tstep = 0; }
   } step_index{m};
   m->tstep = -1;  // the first draw (prompt logits) is not timed
-  RGD_TRY(select_tokens(m, z0, V, R, m->tilemax, m->nchunks, T, min_p, sd, 0u, out, steps, 0, m->cur_tok, s));
+  // the sampler writes the next step's input rows itself unless tokens are
+  // forced (teacher forcing feeds other tokens) or no step follows
+  bool embedded = false;
+  RGD_TRY(select_tokens(m, z0, V, R, m->tilemax, m->nchunks, T, min_p, sd, 0u, out, steps, 0, m->cur_tok, s,
+                        !forced && steps > 1, &embedded));
   for (int st = 1; st < steps; ++st) {
     m->tstep = st - 1;
     TimeScope tstep(m, RGD_TIMER_STEP, s);
     Rows rows = device_rows(m, kv, R, st - 1, false);
     const int* feed = forced ? forced + (st - 1) : m->cur_tok;
     const int fstride = forced ? steps : 1;
-    RGD_TRY(forward_rows(m, kv, rows, h, feed, fstride, s));
+    RGD_TRY(forward_rows(m, kv, rows, h, feed, fstride, s, embedded));
     float* z = logits_tap ? logits_tap + (size_t)st * R * V : m->logits;
     RGD_TRY(lm_head(m, m->xn, m->cfg.d_model, R, z, s));
     RGD_TRY(select_tokens(m, z, V, R, m->tilemax, m->ntiles, T, min_p, sd, (unsigned)st, out, steps, st,
-                          m->cur_tok, s));
+                          m->cur_tok, s, !forced && st + 1 < steps, &embedded));
   }
   // pages are returned to the pool by `give` (work on them stays ordered on `s`)
   return RGD_OK;

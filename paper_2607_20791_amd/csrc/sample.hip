@@ -11,6 +11,7 @@
 // LM-head epilogue or a chunk-max pass).  No cross-workgroup synchronisation.
 #include "kernels.hpp"
 #include "philox.hpp"
+#include "rownorm.hpp"
 
 namespace rgd {
 
@@ -329,6 +330,14 @@ __global__ __launch_bounds__(256) void minp_select_kernel(SampleArgs a) {
   if (threadIdx.x == 0) {
     a.out[r * a.out_stride + a.out_col] = tok;
     if (a.cur_tok) a.cur_tok[r] = tok;
+  }
+  // the next step's first kernel (embedding gather + RMSNorm) for this row
+  if (a.embed) {
+    float* x = a.x + (long long)r * a.d;
+    if (a.embed_bf16)
+      embed_norm_row(tok, (const bf16_t*)a.embed, a.d, a.vocab, a.gain, a.eps, x, (bf16_t*)a.xn + (long long)r * a.d);
+    else
+      embed_norm_row(tok, (const float*)a.embed, a.d, a.vocab, a.gain, a.eps, x, (float*)a.xn + (long long)r * a.d);
   }
 }
 
