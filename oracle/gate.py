@@ -14,8 +14,18 @@ otherwise a stop token ends it with STOP and reaching k tokens with MAXLEN
 (both return the greedy probe).  Algorithm 1 splits the loop into a c-token
 gate and a post-cap probe B_M with the same three events; the decision does not
 depend on c.
+
+Soft variant (Appendix C): during the first c tokens, a greedy token that would
+make q incompatible is not final.  Among the K most probable next tokens, those
+that keep q compatible carry a probability mass m; if that set is not empty and
+m >= rho, its most probable token is appended instead and the probe goes on.
+After c tokens the hard rule applies (the post-cap probe B_M).
 """
 from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
 
 INCOMPAT, STOP, MAXLEN = 0, 1, 2
 
@@ -27,7 +37,10 @@ def is_prefix(a, b) -> bool:
 
 def compatible(q, table, min_match: int = 2) -> bool:
     """C(q, P) on token ids: q is a prefix of an entry, or an entry is a prefix
-    of q; entries shorter than min_match are ignored."""
+    of q; entries shorter than min_match are ignored.  table None: no refusal
+    set at all, the fixed-length probe of the ablations (every q passes)."""
+    if table is None:
+        return True
     q = [int(t) for t in q]
     for e in table:
         e = [int(t) for t in e]
@@ -58,6 +71,64 @@ def probe(first_logits, next_logits, table, k: int, eos: int = -1, min_match: in
         if not compatible(q, table, min_match):
             return q, INCOMPAT
         if eos >= 0 and y == eos:
+            return q, STOP
+        if len(q) >= k:
+            return q, MAXLEN
+        logits = next_logits(q)
+
+
+def top_k(z, K: int):
+    """The K most probable tokens of logits z, most probable first (equal logits:
+    lower id first), with their probabilities under softmax(z) over the whole
+    vocabulary (temperature 1: the model's own next-token distribution)."""
+    z = np.asarray(z, np.float64)
+    order = np.lexsort((np.arange(len(z)), -z))
+    w = np.exp(z - z.max())
+    p = w / w.sum()
+    return [(int(i), float(p[i])) for i in order[:K]]
+
+
+@dataclass
+class SoftStep:
+    """What a soft step decided, with the margins that make it fragile under
+    rounding: the gap between the K-th and (K+1)-th logit (top-K membership) and
+    |m - rho| (the mass test); None where the step did not use them."""
+    greedy: int
+    appended: int
+    mass: float | None = None
+    topk_gap: float | None = None
+    rho_margin: float | None = None
+
+
+def soft_probe(first_logits, next_logits, table, k: int, c: int, K: int, rho: float,
+               eos: int = -1, min_match: int = 2, steps: list | None = None):
+    """Probe with the soft compatibility gate (Appendix C, Algorithm 2): tokens
+    1..c are soft steps, later ones follow the hard rule.  Returns (q, event);
+    on INCOMPAT the last token of q is the greedy token that failed.  `steps`,
+    when given, collects one SoftStep per soft step that met an incompatible
+    greedy token."""
+    from .sampler import argmax
+    q = []
+    logits = first_logits
+    while True:
+        y = int(argmax(logits))
+        if compatible(q + [y], table, min_match):
+            q.append(y)
+        elif len(q) < c:
+            cand = top_k(logits, K)
+            alts = [(a, pa) for a, pa in cand if compatible(q + [a], table, min_match)]
+            mass = sum(pa for _, pa in alts)
+            zs = np.sort(np.asarray(logits, np.float64))[::-1]
+            gap = float(zs[K - 1] - zs[K]) if K < len(zs) else None
+            ok = bool(alts) and mass >= rho
+            if steps is not None:
+                steps.append(SoftStep(y, alts[0][0] if ok else y, mass, gap, abs(mass - rho)))
+            if not ok:
+                return q + [y], INCOMPAT
+            q.append(alts[0][0])  # the most probable compatible alternative
+        else:
+            return q + [y], INCOMPAT
+        if eos >= 0 and q[-1] == eos:
             return q, STOP
         if len(q) >= k:
             return q, MAXLEN

@@ -55,6 +55,18 @@ def greedy_probe(model: Decoder, prefix: KVCache, last_logits, table, k: int, eo
     return gate.probe(last_logits, nxt, table, k, eos, min_match)
 
 
+def soft_greedy_probe(model: Decoder, prefix: KVCache, last_logits, table, k: int, c: int, K: int,
+                      rho: float, eos: int = -1, min_match: int = 2, steps: list | None = None):
+    """The probe of the soft compatibility-gate variant (Appendix C) against the
+    shared prompt cache."""
+    tail = KVCache(model.cfg.n_layers)
+
+    def nxt(q):
+        return model.decode(q[-1], prefix, tail)
+
+    return gate.soft_probe(last_logits, nxt, table, k, c, K, rho, eos, min_match, steps)
+
+
 @dataclass
 class GatedResult:
     hit: bool

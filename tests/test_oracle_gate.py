@@ -79,3 +79,94 @@ def test_early_exit_decision_equals_full_probe(seed):
 
 def test_table_entries_csr():
     assert gate.table_entries(np.array([0, 2, 5]), np.array([4, 5, 6, 7, 8])) == [[4, 5], [6, 7, 8]]
+
+
+# ---- soft compatibility gate (Appendix C) ----
+
+def _probs_logits(p):
+    """logits whose softmax is exactly the distribution p."""
+    return np.log(np.asarray(p, np.float64))
+
+
+def test_top_k_order_ties_and_probabilities():
+    z = _probs_logits([0.1, 0.4, 0.4, 0.05, 0.05])
+    got = gate.top_k(z, 3)
+    assert [a for a, _ in got] == [1, 2, 0]          # equal logits: lower id first
+    assert np.allclose([pa for _, pa in got], [0.4, 0.4, 0.1])
+
+
+def _soft_scene(p_after_i):
+    """Scripted probe: token 1 is I; after [I] the next-token distribution is
+    p_after_i; after that, DOT forever."""
+    first = _probs_logits([0.01] * 1 + [0.9] + [0.01] * 8)    # argmax I (= 1)
+    p_dot = [0.02] * 10
+    p_dot[DOT] = 0.82
+
+    def nxt(q):
+        return _probs_logits(p_after_i) if len(q) == 1 else _probs_logits(p_dot)
+    return first, nxt
+
+
+# after "I": greedy " think" (0.5), then " cannot" (0.2), " can't" (0.15)
+P_AFTER_I = [0.02, 0.02, 0.2, 0.15, 0.02, 0.5, 0.02, 0.03, 0.02, 0.02]
+SOFT_TABLE = [[I, CANNOT, HELP, DOT], [I, CANT, HELP, DOT], [I, M_SORRY, DOT]]
+
+
+def test_soft_gate_continues_with_the_most_probable_compatible_alternative():
+    first, nxt = _soft_scene(P_AFTER_I)
+    # compatible mass 0.2 + 0.15 + 0.02 (" cannot", " can't", "'m sorry") = 0.37 >= 0.1:
+    # " cannot", the most probable of them, replaces " think"
+    steps = []
+    q, ev = gate.soft_probe(first, nxt, SOFT_TABLE, k=6, c=3, K=10, rho=0.1, steps=steps)
+    assert q[:2] == [I, CANNOT]
+    assert np.isclose(steps[0].mass, 0.37) and steps[0].greedy == THINK and steps[0].appended == CANNOT
+    # the probe goes on greedily: DOT after "I cannot" leaves every entry -> third token fails
+    assert (q, ev) == ([I, CANNOT, DOT], gate.INCOMPAT)
+
+
+def test_soft_gate_mass_below_rho_samples():
+    first, nxt = _soft_scene(P_AFTER_I)
+    assert gate.soft_probe(first, nxt, SOFT_TABLE, k=6, c=3, K=10, rho=0.4) == ([I, THINK], gate.INCOMPAT)
+
+
+def test_soft_gate_mass_uses_the_full_vocabulary_softmax_within_top_k():
+    first, nxt = _soft_scene(P_AFTER_I)
+    # top-2 = " think" 0.5, " cannot" 0.2: mass 0.2 (not renormalised to 0.2/0.7 over the top-K)
+    assert gate.soft_probe(first, nxt, SOFT_TABLE, k=6, c=3, K=2, rho=0.25)[1] == gate.INCOMPAT
+    q, _ = gate.soft_probe(first, nxt, SOFT_TABLE, k=6, c=3, K=2, rho=0.2)
+    assert q[:2] == [I, CANNOT]
+    # " can't" (rank 3) is outside the top-2 and does not count
+    assert gate.soft_probe(first, nxt, [[I, CANT, DOT]], k=6, c=3, K=2, rho=0.01)[1] == gate.INCOMPAT
+    assert gate.soft_probe(first, nxt, [[I, CANT, DOT]], k=6, c=3, K=3, rho=0.01)[0][:2] == [I, CANT]
+
+
+def test_soft_steps_are_only_the_first_c_tokens():
+    first, nxt = _soft_scene(P_AFTER_I)
+    # the incompatible greedy token is token 2: soft with c >= 2, hard with c = 1
+    assert gate.soft_probe(first, nxt, SOFT_TABLE, k=6, c=1, K=10, rho=0.1) == ([I, THINK], gate.INCOMPAT)
+    assert gate.soft_probe(first, nxt, SOFT_TABLE, k=6, c=2, K=10, rho=0.1)[0][:2] == [I, CANNOT]
+
+
+def test_soft_gate_maxlen_after_substitution():
+    first, nxt = _soft_scene(P_AFTER_I)
+    # a 2-token budget ends right after the substituted token: a hit with the soft probe
+    assert gate.soft_probe(first, nxt, SOFT_TABLE, k=2, c=3, K=10, rho=0.1) == ([I, CANNOT], gate.MAXLEN)
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_soft_gate_reduces_to_the_hard_gate(seed):
+    """rho above 1 (no mass can reach it) or K = 1 (the only candidate is the
+    failing greedy token) give exactly the hard probe."""
+    g = np.random.default_rng(seed)
+    V = 6
+    table = [list(g.integers(0, V, size=g.integers(2, 5))) for _ in range(4)]
+    seqs = g.normal(size=(12, V)) * 2
+    first, nxt = seqs[0], (lambda q: seqs[len(q)])
+    hard = gate.probe(first, nxt, table, k=8)
+    assert gate.soft_probe(first, nxt, table, k=8, c=8, K=V, rho=1.5) == hard
+    assert gate.soft_probe(first, nxt, table, k=8, c=8, K=1, rho=0.0) == hard
+
+
+def test_fixed_length_probe_without_table():
+    first, nxt = _scripted([3, 1, 4, 1, 5, 9])
+    assert gate.probe(first, nxt, None, k=5) == ([3, 1, 4, 1, 5], gate.MAXLEN)
