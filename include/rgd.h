@@ -166,10 +166,29 @@ int32_t rgd_prefill_kv(rgd_model* m, rgd_kv* kv, const int32_t* tokens, int32_t 
  * each of the first c tokens and then every c tokens, and stops launching
  * steps once no prompt is undecided (early exit); the decision does not depend
  * on c.  Outputs (dev): probe_tokens int32 [B][k], probe_len int32 [B],
- * event int32 [B] (rgd_event).  Synchronous.  tbl may not be NULL. */
+ * event int32 [B] (rgd_event).  Synchronous.  tbl NULL: no refusal set, every
+ * probe stays compatible, so the probe runs to k tokens (or eos): the
+ * fixed-length probe of the paper's ablations. */
 int32_t rgd_probe(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_table* tbl,
                   int32_t B, int32_t k, int32_t c, int32_t eos_id, int32_t* probe_tokens,
                   int32_t* probe_len, int32_t* event, rgd_stream stream);
+
+/* Probe with the soft compatibility gate (Appendix C, the soft-gate
+ * algorithm); arguments and outputs as rgd_probe.  Tokens 1..c are soft steps:
+ * when the greedy token would make the probe incompatible, the topk most
+ * probable next tokens (softmax of the logits at temperature 1 over the whole
+ * vocabulary; equal logits: lower id first) are examined, and if those that
+ * keep the probe compatible carry a probability mass >= rho, the most probable
+ * of them is appended instead and the probe goes on.  Otherwise the failing
+ * greedy token is recorded with event INCOMPAT.  Tokens after c follow the
+ * hard rule of rgd_probe (there c only sets the polling cadence; here it is
+ * also the number of soft steps).  1 <= topk <= 32 and topk <= vocab; rho is
+ * any non-NaN value (rho > 1 never accepts: the hard gate).  The probe tokens
+ * then hold the substituted tokens, which is what a hit returns.
+ * Synchronous. */
+int32_t rgd_probe_soft(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_table* tbl,
+                       int32_t B, int32_t k, int32_t c, int32_t eos_id, int32_t topk, float rho,
+                       int32_t* probe_tokens, int32_t* probe_len, int32_t* event, rgd_stream stream);
 
 /* Gate (Algorithm 1, the return branches): prompt b is a hit (return the
  * greedy probe) iff event[b] is STOP or MAXLEN, otherwise a miss (sample from
@@ -275,6 +294,19 @@ int32_t rgd_kernel_argmax(const float* z, int32_t R, int32_t V, void* workspace,
 int32_t rgd_kernel_sample(const float* z, int32_t R, int32_t V, float T, float min_p,
                           const uint64_t* seeds, uint32_t ctr, uint32_t stream0, int32_t draws,
                           void* workspace, int32_t* out, rgd_stream stream);
+
+/* One probe step (Algorithm 1, or the soft gate of Appendix C when topk > 0)
+ * for prompts 0..R-1 of the table, given their next-token logits dev fp32
+ * [R][vocab of m] and their probe state probe_tokens dev int32 [R][k],
+ * probe_len, event dev int32 [R] (updated in place; prompts whose event is
+ * not -1 are left alone): appends one token and sets the event as rgd_probe
+ * and rgd_probe_soft do for their step (c: soft steps when topk > 0; tbl NULL:
+ * no table).  Uses m's workspace, so calls on one model must not overlap.
+ * Asynchronous. */
+int32_t rgd_kernel_probe_step(rgd_model* m, const float* logits, int32_t R, const rgd_table* tbl,
+                              int32_t k, int32_t c, int32_t eos_id, int32_t topk, float rho,
+                              int32_t* probe_tokens, int32_t* probe_len, int32_t* event,
+                              rgd_stream stream);
 
 #ifdef __cplusplus
 }

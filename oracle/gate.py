@@ -92,12 +92,39 @@ def top_k(z, K: int):
 class SoftStep:
     """What a soft step decided, with the margins that make it fragile under
     rounding: the gap between the K-th and (K+1)-th logit (top-K membership) and
-    |m - rho| (the mass test); None where the step did not use them."""
+    the relative distance |m - rho| / max(m, rho) of the mass test; None where
+    the step did not use them."""
     greedy: int
     appended: int
     mass: float | None = None
     topk_gap: float | None = None
     rho_margin: float | None = None
+
+
+def soft_step(q, logits, table, c: int, K: int, rho: float, min_match: int = 2):
+    """One probe step from probe q with next-token logits: returns (token,
+    passed, SoftStep or None).  The greedy token is taken when q stays
+    compatible; otherwise, while len(q) < c (tokens 1..c are soft steps), the
+    most probable compatible token of the top K is taken when the compatible
+    ones of the top K carry mass >= rho.  passed False: the greedy token failed
+    (INCOMPAT).  The SoftStep is returned for soft steps that met an
+    incompatible greedy token."""
+    from .sampler import argmax
+    q = list(q)
+    y = int(argmax(logits))
+    if compatible(q + [y], table, min_match):
+        return y, True, None
+    if len(q) >= c:
+        return y, False, None
+    cand = top_k(logits, K)
+    alts = [(a, pa) for a, pa in cand if compatible(q + [a], table, min_match)]
+    mass = sum(pa for _, pa in alts)
+    zs = np.sort(np.asarray(logits, np.float64))[::-1]
+    gap = float(zs[K - 1] - zs[K]) if K < len(zs) else None
+    ok = bool(alts) and mass >= rho
+    scale = max(mass, abs(rho))
+    info = SoftStep(y, alts[0][0] if ok else y, mass, gap, abs(mass - rho) / scale if scale > 0 else 0.0)
+    return (alts[0][0], True, info) if ok else (y, False, info)
 
 
 def soft_probe(first_logits, next_logits, table, k: int, c: int, K: int, rho: float,
@@ -107,28 +134,16 @@ def soft_probe(first_logits, next_logits, table, k: int, c: int, K: int, rho: fl
     on INCOMPAT the last token of q is the greedy token that failed.  `steps`,
     when given, collects one SoftStep per soft step that met an incompatible
     greedy token."""
-    from .sampler import argmax
     q = []
     logits = first_logits
     while True:
-        y = int(argmax(logits))
-        if compatible(q + [y], table, min_match):
-            q.append(y)
-        elif len(q) < c:
-            cand = top_k(logits, K)
-            alts = [(a, pa) for a, pa in cand if compatible(q + [a], table, min_match)]
-            mass = sum(pa for _, pa in alts)
-            zs = np.sort(np.asarray(logits, np.float64))[::-1]
-            gap = float(zs[K - 1] - zs[K]) if K < len(zs) else None
-            ok = bool(alts) and mass >= rho
-            if steps is not None:
-                steps.append(SoftStep(y, alts[0][0] if ok else y, mass, gap, abs(mass - rho)))
-            if not ok:
-                return q + [y], INCOMPAT
-            q.append(alts[0][0])  # the most probable compatible alternative
-        else:
-            return q + [y], INCOMPAT
-        if eos >= 0 and q[-1] == eos:
+        t, passed, info = soft_step(q, logits, table, c, K, rho, min_match)
+        if info is not None and steps is not None:
+            steps.append(info)
+        q.append(t)
+        if not passed:
+            return q, INCOMPAT
+        if eos >= 0 and t == eos:
             return q, STOP
         if len(q) >= k:
             return q, MAXLEN

@@ -21,9 +21,9 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librgd.so")
 EXPORTS = (
     "rgd_version", "rgd_last_error", "rgd_model_create", "rgd_model_destroy", "rgd_kv_create",
     "rgd_kv_destroy", "rgd_kv_set_prefix_len", "rgd_table_create", "rgd_table_destroy",
-    "rgd_prefill_kv", "rgd_probe", "rgd_gate", "rgd_sample_continuations", "rgd_check_status",
+    "rgd_prefill_kv", "rgd_probe", "rgd_probe_soft", "rgd_gate", "rgd_sample_continuations", "rgd_check_status",
     "rgd_kernel_attention", "rgd_kernel_lm_head", "rgd_sampler_workspace_bytes",
-    "rgd_kernel_argmax", "rgd_kernel_sample", "rgd_timing_enable", "rgd_timing_read",
+    "rgd_kernel_argmax", "rgd_kernel_sample", "rgd_kernel_probe_step", "rgd_timing_enable", "rgd_timing_read",
 )
 
 DTYPE_F32, DTYPE_BF16 = 0, 1
@@ -82,6 +82,8 @@ _sig("rgd_table_create", I32, I32P, I32P, I32, I32P, I32, C.POINTER(VP))
 _sig("rgd_table_destroy", None, VP)
 _sig("rgd_prefill_kv", I32, VP, VP, VP, I32, I32, I32, VP, VP)
 _sig("rgd_probe", I32, VP, VP, VP, VP, I32, I32, I32, I32, VP, VP, VP, VP)
+_sig("rgd_probe_soft", I32, VP, VP, VP, VP, I32, I32, I32, I32, I32, C.c_float, VP, VP, VP, VP)
+_sig("rgd_kernel_probe_step", I32, VP, VP, I32, VP, I32, I32, I32, I32, C.c_float, VP, VP, VP, VP)
 _sig("rgd_gate", I32, VP, VP, I32, I32P, I32P, I32P, VP)
 _sig("rgd_sample_continuations", I32, VP, VP, VP, I32P, I32, I32, I32, F32, F32, VP, VP, VP, VP, VP)
 _sig("rgd_check_status", I32, VP, VP)
@@ -215,8 +217,23 @@ def prefill_kv(model, kv, tokens, start_pos, last_logits):
 
 
 def probe(model, kv, last_logits, table, B, k, c, eos, probe_tokens, probe_len, event):
-    _check(lib.rgd_probe(model.h, kv.h, _ptr(last_logits), table.h, B, k, c, eos,
-                         _ptr(probe_tokens), _ptr(probe_len), _ptr(event), _stream()))
+    """table None: fixed-length probe (no refusal set)."""
+    _check(lib.rgd_probe(model.h, kv.h, _ptr(last_logits), table.h if table is not None else None, B, k, c,
+                         eos, _ptr(probe_tokens), _ptr(probe_len), _ptr(event), _stream()))
+
+
+def kernel_probe_step(model, logits, table, k, c, eos, topk, rho, probe_tokens, probe_len, event):
+    """One probe step for prompts 0..R-1 (R = logits rows) on given logits."""
+    _check(lib.rgd_kernel_probe_step(model.h, _ptr(logits), logits.shape[0],
+                                     table.h if table is not None else None, k, c, eos, topk, float(rho),
+                                     _ptr(probe_tokens), _ptr(probe_len), _ptr(event), _stream()))
+
+
+def probe_soft(model, kv, last_logits, table, B, k, c, eos, topk, rho, probe_tokens, probe_len, event):
+    """Probe with the soft compatibility gate: tokens 1..c are soft steps."""
+    _check(lib.rgd_probe_soft(model.h, kv.h, _ptr(last_logits), table.h if table is not None else None, B, k,
+                              c, eos, topk, float(rho), _ptr(probe_tokens), _ptr(probe_len), _ptr(event),
+                              _stream()))
 
 
 def gate(kv, event, B):

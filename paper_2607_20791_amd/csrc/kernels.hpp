@@ -153,8 +153,25 @@ struct GateArgs {
   const int* offsets; const int* tokens; const int* owner; int n_entries; int min_match;
   int eos;
   unsigned long long* best_reset;  // same as best (cleared after use)
+  int all_compatible;              // no refusal table (fixed-length probe): every probe passes
 };
 hipError_t probe_update(const GateArgs& a, hipStream_t s);
+
+// Soft compatibility gate (Appendix C): a probe step whose greedy token would
+// make the probe incompatible may instead append the most probable
+// compatible token among the K most probable ones, when their probability
+// mass (softmax at temperature 1 over the whole vocabulary) reaches rho.
+constexpr int kMaxTopK = 32;
+struct SoftArgs {
+  GateArgs g;                   // best/best_reset unused
+  const float* z; long long ldz; int V;   // logits of the step, row r at z + r * ldz
+  int chunk, nchunks, K;
+  unsigned long long* keys;     // workspace [R][nchunks][K]
+  float* cmax; float* csum;     // workspace [R][nchunks]
+  float rho; int soft_steps;    // tokens 1..soft_steps are soft steps, later ones hard
+};
+// one probe step for rows 0..R-1 (a.g.R): chunk pass + decision
+hipError_t probe_update_soft(const SoftArgs& a, hipStream_t s);
 hipError_t gate_decide(const int* event, int B, int* decision, int* n_miss, int* miss_idx,
                        hipStream_t s);
 

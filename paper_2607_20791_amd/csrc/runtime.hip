@@ -117,6 +117,8 @@ struct rgd_model {
   int* cur_tok = nullptr;
   int* status = nullptr;
   int* row_map = nullptr;
+  unsigned long long* soft_keys = nullptr;  // soft gate: per-chunk top-K keys [R][nchunks][kMaxTopK]
+  float* soft_cm = nullptr;                 // soft gate: chunk maxima and sums [2][R][nchunks]
   // per-call row arrays
   int* d_prompt = nullptr;
   int* d_base = nullptr;
@@ -688,6 +690,8 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
   A(&m->cur_tok, (size_t)R * 4);
   A(&m->status, 4);
   A(&m->row_map, (size_t)R * 4);
+  A(&m->soft_keys, (size_t)R * m->nchunks * kMaxTopK * 8);
+  A(&m->soft_cm, (size_t)2 * R * m->nchunks * 4);
   A(&m->d_prompt, (size_t)R * 4);
   A(&m->d_base, (size_t)R * 4);
   A(&m->d_plen, (size_t)R * 4);
@@ -902,11 +906,13 @@ int32_t rgd_prefill_kv(rgd_model* m, rgd_kv* kv, const int32_t* tokens, int32_t 
   return RGD_OK;
 }
 
-int32_t rgd_probe(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_table* tbl, int32_t B, int32_t k,
-                  int32_t c, int32_t eos_id, int32_t* probe_tokens, int32_t* probe_len, int32_t* event,
-                  rgd_stream stream) {
-  g_err.clear();
-  if (!m || !kv || !last_logits || !tbl || !probe_tokens || !probe_len || !event)
+namespace {
+
+// The probe loop shared by the hard and the soft gate (topk > 0: tokens 1..c
+// are soft steps).
+int probe_impl(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_table* tbl, int B, int k, int c,
+               int eos_id, int topk, float rho, int* probe_tokens, int* probe_len, int* event, rgd_stream stream) {
+  if (!m || !kv || !last_logits || !probe_tokens || !probe_len || !event)
     return fail(RGD_E_INVALID_ARG, "null argument");
   if (kv->m != m) return fail(RGD_E_INVALID_ARG, "kv belongs to another model");
   if (B < 1 || B > kv->max_prompts || B > m->max_rows) return fail(RGD_E_INVALID_ARG, "B out of range");
@@ -945,12 +951,41 @@ int32_t rgd_probe(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_
   ga.k = k;
   ga.probe_len = probe_len;
   ga.event = event;
-  ga.offsets = tbl->d_offsets;
-  ga.tokens = tbl->d_tokens;
-  ga.owner = tbl->d_owner;
-  ga.n_entries = tbl->n_entries;
-  ga.min_match = tbl->min_match;
+  if (tbl) {
+    ga.offsets = tbl->d_offsets;
+    ga.tokens = tbl->d_tokens;
+    ga.owner = tbl->d_owner;
+    ga.n_entries = tbl->n_entries;
+    ga.min_match = tbl->min_match;
+  } else {
+    ga.all_compatible = 1;  // fixed-length probe
+  }
   ga.eos = eos_id;
+  SoftArgs sa{};
+  sa.V = V;
+  sa.chunk = kSampleChunk;
+  sa.nchunks = m->nchunks;
+  sa.K = topk;
+  sa.keys = m->soft_keys;
+  sa.cmax = m->soft_cm;
+  sa.csum = m->soft_cm + (size_t)m->max_rows * m->nchunks;
+  sa.rho = rho;
+  sa.soft_steps = c;
+  // one probe step on logits z (row r of the alive set at z + r * V): soft
+  // for tokens 1..c when a soft gate is asked for, hard otherwise
+  auto step = [&](const float* z, int R, int token) -> int {
+    ga.R = R;
+    if (topk > 0 && token <= c) {
+      sa.g = ga;
+      sa.z = z;
+      sa.ldz = V;
+      HIP_OK(probe_update_soft(sa, s));
+    } else {
+      HIP_OK(argmax_rows(z, V, R, V, m->best, s));
+      HIP_OK(probe_update(ga, s));
+    }
+    return RGD_OK;
+  };
 
   std::vector<int> alive(B);
   for (int b = 0; b < B; ++b) alive[b] = b;
@@ -986,10 +1021,8 @@ int32_t rgd_probe(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_
   HostRows h;
   std::vector<int> pages;
   RGD_TRY(set_rows(h, pages));
-  // token 1: argmax of the prompt logits (rows are prompts 0..B-1 here)
-  HIP_OK(argmax_rows(last_logits, V, B, V, m->best, s));
-  ga.R = B;
-  HIP_OK(probe_update(ga, s));
+  // token 1 from the prompt logits (rows are prompts 0..B-1 here)
+  RGD_TRY(step(last_logits, B, 1));
   for (int j = 2;; ++j) {
     const int done_tokens = j - 1;
     const bool check = done_tokens <= c || done_tokens % c == 0 || done_tokens >= k;
@@ -1013,12 +1046,30 @@ int32_t rgd_probe(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_
     Rows rows = device_rows(m, kv, R, j - 2, false);
     RGD_TRY(forward_rows(m, kv, rows, h, m->cur_tok, 1, s));
     RGD_TRY(lm_head(m, m->xn, m->cfg.d_model, R, m->logits, s));
-    HIP_OK(argmax_rows(m->logits, V, R, V, m->best, s));
-    ga.R = R;
-    HIP_OK(probe_update(ga, s));
+    RGD_TRY(step(m->logits, R, j));
   }
   HIP_OK(hipStreamSynchronize(s));
   return RGD_OK;
+}
+
+}  // namespace
+
+int32_t rgd_probe(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_table* tbl, int32_t B, int32_t k,
+                  int32_t c, int32_t eos_id, int32_t* probe_tokens, int32_t* probe_len, int32_t* event,
+                  rgd_stream stream) {
+  g_err.clear();
+  return probe_impl(m, kv, last_logits, tbl, B, k, c, eos_id, 0, 0.f, probe_tokens, probe_len, event, stream);
+}
+
+int32_t rgd_probe_soft(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_table* tbl, int32_t B,
+                       int32_t k, int32_t c, int32_t eos_id, int32_t topk, float rho, int32_t* probe_tokens,
+                       int32_t* probe_len, int32_t* event, rgd_stream stream) {
+  g_err.clear();
+  if (!m) return fail(RGD_E_INVALID_ARG, "null model");
+  if (topk < 1 || topk > kMaxTopK || topk > m->cfg.vocab)
+    return fail(RGD_E_INVALID_ARG, "topk must be in [1, %d] and at most the vocabulary", kMaxTopK);
+  if (!(rho == rho)) return fail(RGD_E_INVALID_ARG, "rho is NaN");
+  return probe_impl(m, kv, last_logits, tbl, B, k, c, eos_id, topk, rho, probe_tokens, probe_len, event, stream);
 }
 
 int32_t rgd_gate(rgd_kv* kv, const int32_t* event, int32_t B, int32_t* decision_host, int32_t* n_miss_host,
@@ -1252,6 +1303,61 @@ uint64_t rgd_sampler_workspace_bytes(int32_t R, int32_t V) {
   const long long nch = cdiv(V, kSampleChunk);
   // best u64 [R], chunk maxima f32 [R][nch], chunk sums f32 [R][nch]
   return (uint64_t)(8LL * R + 8LL * R * nch + 256);
+}
+
+int32_t rgd_kernel_probe_step(rgd_model* m, const float* logits, int32_t R, const rgd_table* tbl, int32_t k,
+                              int32_t c, int32_t eos_id, int32_t topk, float rho, int32_t* probe_tokens,
+                              int32_t* probe_len, int32_t* event, rgd_stream stream) {
+  g_err.clear();
+  if (!m || !logits || !probe_tokens || !probe_len || !event) return fail(RGD_E_INVALID_ARG, "null argument");
+  if (R < 1 || R > m->max_rows) return fail(RGD_E_INVALID_ARG, "R out of range");
+  if (k < 1 || c < 0) return fail(RGD_E_INVALID_ARG, "k must be >= 1 and c >= 0");
+  if (topk < 0 || topk > kMaxTopK || topk > m->cfg.vocab) return fail(RGD_E_INVALID_ARG, "topk out of range");
+  if (!(rho == rho)) return fail(RGD_E_INVALID_ARG, "rho is NaN");
+  hipStream_t s = (hipStream_t)stream;
+  const int V = m->cfg.vocab;
+  std::vector<int> ident(R);
+  for (int r = 0; r < R; ++r) ident[r] = r;
+  RGD_TRY(upload(m, {{m->d_prompt, ident.data(), (size_t)R}}, s));
+  GateArgs ga{};
+  ga.best = m->best;
+  ga.best_reset = m->best;
+  ga.row_prompt = m->d_prompt;
+  ga.R = R;
+  ga.probe_tokens = probe_tokens;
+  ga.k = k;
+  ga.probe_len = probe_len;
+  ga.event = event;
+  if (tbl) {
+    ga.offsets = tbl->d_offsets;
+    ga.tokens = tbl->d_tokens;
+    ga.owner = tbl->d_owner;
+    ga.n_entries = tbl->n_entries;
+    ga.min_match = tbl->min_match;
+  } else {
+    ga.all_compatible = 1;
+  }
+  ga.eos = eos_id;
+  if (topk > 0) {
+    SoftArgs sa{};
+    sa.g = ga;
+    sa.z = logits;
+    sa.ldz = V;
+    sa.V = V;
+    sa.chunk = kSampleChunk;
+    sa.nchunks = m->nchunks;
+    sa.K = topk;
+    sa.keys = m->soft_keys;
+    sa.cmax = m->soft_cm;
+    sa.csum = m->soft_cm + (size_t)m->max_rows * m->nchunks;
+    sa.rho = rho;
+    sa.soft_steps = c;
+    HIP_OK(probe_update_soft(sa, s));
+  } else {
+    HIP_OK(argmax_rows(logits, V, R, V, m->best, s));
+    HIP_OK(probe_update(ga, s));
+  }
+  return RGD_OK;
 }
 
 int32_t rgd_kernel_argmax(const float* z, int32_t R, int32_t V, void* workspace, int32_t* out, rgd_stream stream) {

@@ -9,6 +9,7 @@
 // block-wide prefix scan.  Logits are read once per draw from HBM (plus the
 // one rescanned chunk); the row maximum comes in as partial maxima (from the
 // LM-head epilogue or a chunk-max pass).  No cross-workgroup synchronisation.
+#include "gatecheck.hpp"
 #include "kernels.hpp"
 #include "philox.hpp"
 #include "rownorm.hpp"
@@ -364,16 +365,8 @@ __global__ __launch_bounds__(64) void probe_update_kernel(GateArgs a) {
   const int j = a.probe_len[b];
   const int* q = a.probe_tokens + (long long)b * a.k;
   bool any = false;
-  for (int e = threadIdx.x; e < a.n_entries; e += 64) {
-    if (a.owner && a.owner[e] != -1 && a.owner[e] != b) continue;
-    const int o0 = a.offsets[e], len = a.offsets[e + 1] - o0;
-    if (len < a.min_match) continue;
-    const int n = min(len, j + 1);
-    bool match = true;
-    for (int i = 0; i < n && match; ++i) match = a.tokens[o0 + i] == (i < j ? q[i] : tok);
-    any = any || match;
-  }
-  const bool compat = __any(any);
+  for (int e = threadIdx.x; e < a.n_entries; e += 64) any = any || entry_matches(a, e, b, q, j, tok);
+  const bool compat = a.all_compatible || __any(any);
   if (threadIdx.x == 0) {
     a.probe_tokens[(long long)b * a.k + j] = tok;
     a.probe_len[b] = j + 1;
