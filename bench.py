@@ -54,6 +54,55 @@ def measured_traffic(name="lm_head_c2_traffic.md"):
         return None
 
 
+SOFT_TOPK, SOFT_RHO = 10, 0.1
+
+
+def gate_variants(rgd, torch, model, kv, w, last, table, prefill, k, c, N, S, sampling_ms, reps=5):
+    """Probe + gate wall time (median of `reps`, ms) of the hard gate, the soft
+    compatibility gate (top-10, rho = 0.1) and the fixed-length probe (no
+    table), on the typical table and on an adversarial one (an entry equal to
+    the first k-1 greedy tokens and different at token k: a full-length miss),
+    each also as a fraction of ungated sampling time per step."""
+    import statistics
+    import numpy as np
+    dev = "cuda"
+    ptok = torch.empty(1, k, dtype=torch.int32, device=dev)
+    plen = torch.empty(1, dtype=torch.int32, device=dev)
+    ev = torch.empty(1, dtype=torch.int32, device=dev)
+    prefill()
+    torch.cuda.synchronize()
+
+    def timed(fn):
+        ts = []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            fn()
+            rgd.gate(kv, ev, 1)
+            ts.append((time.perf_counter() - t0) * 1e3)
+        return statistics.median(ts), int(plen.item()), int(ev.item())
+
+    g = torch.empty(1, 1, k, dtype=torch.int32, device=dev)
+    rgd.sample_continuations(model, kv, last, [0], 1, k, 0.0, 0.0, torch.zeros(1, dtype=torch.int64, device=dev), g)
+    gl = g[0, 0].cpu().numpy()
+    adv = rgd.Table(np.array([0, k], np.int32), np.array(list(gl[:k - 1]) + [int((gl[k - 1] + 1) % w.vocab)],
+                                                        np.int32))
+    out = {"soft_topk": SOFT_TOPK, "soft_rho": SOFT_RHO, "sampling_ms_per_step": round(sampling_ms, 3)}
+    cases = {
+        "hard_typical": lambda: rgd.probe(model, kv, last, table, 1, k, c, -1, ptok, plen, ev),
+        "soft_typical": lambda: rgd.probe_soft(model, kv, last, table, 1, k, c, -1, SOFT_TOPK, SOFT_RHO,
+                                               ptok, plen, ev),
+        "hard_adversarial": lambda: rgd.probe(model, kv, last, adv, 1, k, c, -1, ptok, plen, ev),
+        "soft_adversarial": lambda: rgd.probe_soft(model, kv, last, adv, 1, k, c, -1, SOFT_TOPK, SOFT_RHO,
+                                                   ptok, plen, ev),
+        "fixed_length": lambda: rgd.probe(model, kv, last, None, 1, k, c, -1, ptok, plen, ev),
+    }
+    for name, fn in cases.items():
+        ms, n, e = timed(fn)
+        out[name] = {"probe_gate_ms": round(ms, 3), "probe_tokens": n, "event": e,
+                     "overhead": round(ms / sampling_ms, 5) if sampling_ms > 0 else None}
+    return out
+
+
 def algorithmic(w, R, P, tails):
     """Algorithmic bytes / flops per launch of the three named kernels."""
     d, V, Hq, Hkv, D = w.d_model, w.vocab, w.n_heads, w.n_kv_heads, w.head_dim
@@ -312,6 +361,9 @@ def main():
         "wall_ms_per_step_with_prefill": round(elapsed / args.steps * 1e3, 3),
     }
     line.update(res)
+    log("gate variants ...")
+    line["gate_variants"] = gate_variants(rgd, torch, model, kv, w, last, table, prefill, k, c, N, S,
+                                          sample_s / args.steps * 1e3)
     log("sampler sweep ...")
     line["sampler_sweep"] = sampler_sweep(rgd, torch)
     if not args.no_cpu_baseline:
