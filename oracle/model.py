@@ -122,14 +122,18 @@ class Decoder:
     def embed(self, tokens) -> np.ndarray:
         return widen(self.W.embed[np.asarray(tokens)])
 
-    def prefill(self, tokens, cache: KVCache, start_pos: int | None = None) -> np.ndarray:
+    def prefill(self, tokens, cache: KVCache, start_pos: int | None = None, taps: dict | None = None) -> np.ndarray:
         """Causal forward of a prompt segment appended to `cache` (which holds
-        positions [0, start_pos)); returns the last position's logits."""
+        positions [0, start_pos)); returns the last position's logits.  taps,
+        when given, receives the last position's residual stream: taps[0] the
+        embedding, taps[l] the output of block l (1-based)."""
         tokens = np.asarray(tokens)
         start = cache.length() if start_pos is None else start_pos
         assert start == cache.length()
         pos = np.arange(start, start + len(tokens))
         x = self.embed(tokens)
+        if taps is not None:
+            taps[0] = x[-1].copy()
         for l in range(self.cfg.n_layers):
             Kc, Vc = cache.arrays(l)
             Kc = Kc.reshape(-1, self.hkv, self.d)
@@ -141,6 +145,8 @@ class Decoder:
             x, k, v = self._block(l, x, pos, visible)
             cache.k[l].extend(list(k))
             cache.v[l].extend(list(v))
+            if taps is not None:
+                taps[l + 1] = x[-1].copy()
         return self.logits(x[-1])
 
     def decode(self, token: int, prefix: KVCache, tail: KVCache) -> np.ndarray:
