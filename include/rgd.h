@@ -52,7 +52,8 @@ enum rgd_status {
 enum rgd_dtype { RGD_DTYPE_F32 = 0, RGD_DTYPE_BF16 = 1 };
 
 /* Decisive probe events (Algorithm 1: incompatibility, stop, length cap). */
-enum rgd_event { RGD_EVENT_INCOMPAT = 0, RGD_EVENT_STOP = 1, RGD_EVENT_MAXLEN = 2 };
+enum rgd_event { RGD_EVENT_INCOMPAT = 0, RGD_EVENT_STOP = 1, RGD_EVENT_MAXLEN = 2,
+                 RGD_EVENT_SKIPPED = 3 /* pre-check score <= theta: sampled without a check */ };
 
 /* Target model M: a pre-norm decoder (RMSNorm, grouped-query attention with
  * rotate-half RoPE, SwiGLU feed-forward, untied LM head).  The paper runs
@@ -157,6 +158,16 @@ void rgd_table_destroy(rgd_table* t);
 int32_t rgd_prefill_kv(rgd_model* m, rgd_kv* kv, const int32_t* tokens, int32_t B, int32_t n,
                        int32_t start_pos, float* last_logits, rgd_stream stream);
 
+/* rgd_prefill_kv plus the residual-stream classifier pre-check (Appendix A):
+ * for each prompt b, scores[b] = 1 / (1 + exp(-(cls_w . h_b + cls_b))) where
+ * h_b is the fp32 residual stream of the prompt's last position after block
+ * cls_layer (1..n_layers; 0 = the embedding).  cls_w dev fp32 [d_model]
+ * (caller-owned), scores dev fp32 [B].  The logits and the KV written are those
+ * of rgd_prefill_kv.  Asynchronous. */
+int32_t rgd_prefill_kv_scored(rgd_model* m, rgd_kv* kv, const int32_t* tokens, int32_t B, int32_t n,
+                              int32_t start_pos, float* last_logits, int32_t cls_layer, const float* cls_w,
+                              float cls_b, float* scores, rgd_stream stream);
+
 /* Greedy probe (Algorithm 1: the c-token gate G_M and the post-cap probe B_M)
  * for prompts 0..B-1.  Token 1 is the argmax of last_logits (dev fp32
  * [B][vocab]); each further token is the argmax after feeding the probe, whose
@@ -190,9 +201,19 @@ int32_t rgd_probe_soft(rgd_model* m, rgd_kv* kv, const float* last_logits, const
                        int32_t B, int32_t k, int32_t c, int32_t eos_id, int32_t topk, float rho,
                        int32_t* probe_tokens, int32_t* probe_len, int32_t* event, rgd_stream stream);
 
+/* The adaptive gate (Appendix A): prompts whose pre-check score (scores dev
+ * fp32 [B], from rgd_prefill_kv_scored) is <= theta skip the greedy check: they
+ * get event RGD_EVENT_SKIPPED and probe_len 0 (a miss for rgd_gate, sampled
+ * without any check token); the others are probed as by rgd_probe (topk 0) or
+ * rgd_probe_soft (topk >= 1, with rho).  Synchronous. */
+int32_t rgd_probe_adaptive(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_table* tbl,
+                           int32_t B, int32_t k, int32_t c, int32_t eos_id, int32_t topk, float rho,
+                           const float* scores, float theta, int32_t* probe_tokens, int32_t* probe_len,
+                           int32_t* event, rgd_stream stream);
+
 /* Gate (Algorithm 1, the return branches): prompt b is a hit (return the
- * greedy probe) iff event[b] is STOP or MAXLEN, otherwise a miss (sample from
- * the prompt).  Releases every probe-tail page (the probe's K/V is dropped,
+ * greedy probe) iff event[b] is STOP or MAXLEN, otherwise (INCOMPAT, SKIPPED)
+ * a miss (sample from the prompt).  Releases every probe-tail page (the probe's K/V is dropped,
  * never copied; the shared prefix is untouched).  event dev int32 [B].
  * decision_host int32 [B] (1 = hit, 0 = miss), *n_miss_host, miss_idx_host
  * int32 [B] (first *n_miss_host entries: missed prompts in increasing order).

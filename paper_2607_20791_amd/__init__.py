@@ -21,13 +21,13 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librgd.so")
 EXPORTS = (
     "rgd_version", "rgd_last_error", "rgd_model_create", "rgd_model_destroy", "rgd_kv_create",
     "rgd_kv_destroy", "rgd_kv_set_prefix_len", "rgd_table_create", "rgd_table_destroy",
-    "rgd_prefill_kv", "rgd_probe", "rgd_probe_soft", "rgd_gate", "rgd_sample_continuations", "rgd_check_status",
+    "rgd_prefill_kv", "rgd_prefill_kv_scored", "rgd_probe", "rgd_probe_soft", "rgd_probe_adaptive", "rgd_gate", "rgd_sample_continuations", "rgd_check_status",
     "rgd_kernel_attention", "rgd_kernel_lm_head", "rgd_sampler_workspace_bytes",
     "rgd_kernel_argmax", "rgd_kernel_sample", "rgd_kernel_probe_step", "rgd_timing_enable", "rgd_timing_read",
 )
 
 DTYPE_F32, DTYPE_BF16 = 0, 1
-EVENT_INCOMPAT, EVENT_STOP, EVENT_MAXLEN = 0, 1, 2
+EVENT_INCOMPAT, EVENT_STOP, EVENT_MAXLEN, EVENT_SKIPPED = 0, 1, 2, 3
 STATUS = {0: "OK", 1: "INVALID_ARG", 2: "OOM", 3: "HIP", 4: "UNSUPPORTED", 5: "NONFINITE", 6: "STATE"}
 
 # PyTorch ships its own HIP runtime (same soname as the system one).  Loading it
@@ -83,6 +83,8 @@ _sig("rgd_table_destroy", None, VP)
 _sig("rgd_prefill_kv", I32, VP, VP, VP, I32, I32, I32, VP, VP)
 _sig("rgd_probe", I32, VP, VP, VP, VP, I32, I32, I32, I32, VP, VP, VP, VP)
 _sig("rgd_probe_soft", I32, VP, VP, VP, VP, I32, I32, I32, I32, I32, C.c_float, VP, VP, VP, VP)
+_sig("rgd_probe_adaptive", I32, VP, VP, VP, VP, I32, I32, I32, I32, I32, C.c_float, VP, C.c_float, VP, VP, VP, VP)
+_sig("rgd_prefill_kv_scored", I32, VP, VP, VP, I32, I32, I32, VP, I32, VP, C.c_float, VP, VP)
 _sig("rgd_kernel_probe_step", I32, VP, VP, I32, VP, I32, I32, I32, I32, C.c_float, VP, VP, VP, VP)
 _sig("rgd_gate", I32, VP, VP, I32, I32P, I32P, I32P, VP)
 _sig("rgd_sample_continuations", I32, VP, VP, VP, I32P, I32, I32, I32, F32, F32, VP, VP, VP, VP, VP)
@@ -227,6 +229,21 @@ def kernel_probe_step(model, logits, table, k, c, eos, topk, rho, probe_tokens, 
     _check(lib.rgd_kernel_probe_step(model.h, _ptr(logits), logits.shape[0],
                                      table.h if table is not None else None, k, c, eos, topk, float(rho),
                                      _ptr(probe_tokens), _ptr(probe_len), _ptr(event), _stream()))
+
+
+def prefill_kv_scored(model, kv, tokens, start_pos, last_logits, cls_layer, cls_w, cls_b, scores):
+    """Prefill plus the residual-stream pre-check score of each prompt."""
+    B, n = tokens.shape
+    _check(lib.rgd_prefill_kv_scored(model.h, kv.h, _ptr(tokens), B, n, start_pos, _ptr(last_logits), cls_layer,
+                                     _ptr(cls_w), float(cls_b), _ptr(scores), _stream()))
+
+
+def probe_adaptive(model, kv, last_logits, table, B, k, c, eos, topk, rho, scores, theta, probe_tokens,
+                   probe_len, event):
+    """Adaptive gate: prompts scored <= theta are SKIPPED, the others probed."""
+    _check(lib.rgd_probe_adaptive(model.h, kv.h, _ptr(last_logits), table.h if table is not None else None, B,
+                                  k, c, eos, topk, float(rho), _ptr(scores), float(theta), _ptr(probe_tokens),
+                                  _ptr(probe_len), _ptr(event), _stream()))
 
 
 def probe_soft(model, kv, last_logits, table, B, k, c, eos, topk, rho, probe_tokens, probe_len, event):

@@ -19,6 +19,18 @@ __global__ __launch_bounds__(kNormThreads) void embed_rmsnorm_kernel(const int* 
   embed_norm_row(tok[(long long)r * tok_stride], E, d, V, g, eps, x + (long long)r * d, xn + (long long)r * d);
 }
 
+// Logistic readout of one residual row per workgroup (fixed reduction order).
+__global__ __launch_bounds__(256) void residual_readout_kernel(const float* x, long long row0, long long stride,
+                                                               int d, const float* w, float b, float* out) {
+  __shared__ float red[4];
+  const int r = blockIdx.x;
+  const float* xr = x + (row0 + r * stride) * d;
+  float acc = 0.f;
+  for (int i = threadIdx.x; i < d; i += 256) acc = fmaf(xr[i], w[i], acc);
+  acc = block_sum(acc, red);
+  if (threadIdx.x == 0) out[r] = 1.0f / (1.0f + expf(-(acc + b)));
+}
+
 template <typename T>
 __global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(float* x, const float* parts, int nparts,
                                                                       long long part_stride, const float* g,
@@ -122,6 +134,13 @@ hipError_t embed_rmsnorm(const int* tok, int tok_stride, int R, const T* E, int 
   if (d % 4 || d > kChunks * 4 * kNormThreads) return hipErrorInvalidValue;
   hipLaunchKernelGGL(embed_rmsnorm_kernel<T>, dim3(R), dim3(kNormThreads), 0, s, tok, tok_stride, E, d, V, x,
                      g, eps, xn);
+  return hipGetLastError();
+}
+
+hipError_t residual_readout(const float* x, long long row0, long long stride, int nrows, int d, const float* w,
+                            float b, float* out, hipStream_t s) {
+  if (nrows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(residual_readout_kernel, dim3(nrows), dim3(256), 0, s, x, row0, stride, d, w, b, out);
   return hipGetLastError();
 }
 

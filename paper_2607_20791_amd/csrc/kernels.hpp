@@ -83,6 +83,11 @@ hipError_t qkv_rope_store(const float* parts, int nparts, long long part_stride,
                           int Hkv, int D, const float* rope_cs, int max_pos, T* q, const KVLayout& kv,
                           hipStream_t s);
 
+// Residual-stream readout (Appendix A): out[r] = 1 / (1 + exp(-(w . x_r + b)))
+// for rows x_r = x + (row0 + r * stride) * d of the fp32 residual stream.
+hipError_t residual_readout(const float* x, long long row0, long long stride, int nrows, int d, const float* w,
+                            float b, float* out, hipStream_t s);
+
 // -------------------------------------------------------------- attention ----
 struct AttnArgs {
   const void* q;            // [R][Hq][D]

@@ -148,3 +148,31 @@ def test_bf16_c2_full_size_properties(rgd, c2):
     assert t.equal(before[0], c2.kv.prefix_k) and t.equal(before[1], c2.kv.prefix_v)
     # the probe's first token is the argmax of the prompt's last logits
     assert int(ptok[0, 0]) == int(c2.last[0].argmax())
+
+
+@pytest.mark.parametrize("layer", [0, 1])
+def test_c1_residual_precheck_score(rgd, c1, layer):
+    """Residual-stream classifier pre-check (Appendix A) on the 8B-shaped layer:
+    the score of the prefilled last token within the bf16 tolerance of the
+    oracle's, and the prefill's logits unchanged by the readout."""
+    t = torch()
+    d = c1.w.d_model
+    g = np.random.default_rng(11 + layer)
+    w = (g.normal(size=d) / np.sqrt(d)).astype(np.float32)
+    b = 0.1
+    scores = t.empty(1, dtype=t.float32, device="cuda")
+    plain = c1.last.clone()
+    c1.prefill(rgd)
+    plain.copy_(c1.last)
+    c1.kv.set_prefix_len(0, c1.P)
+    rgd.prefill_kv_scored(c1.model, c1.kv, c1.tok, c1.P, c1.last, layer, t.from_numpy(w).cuda(), b, scores)
+    t.cuda.synchronize()
+    assert t.equal(plain, c1.last)
+    taps = {}
+    cache = KVCache.from_arrays([c1.kp[0]], [c1.vp[0]])
+    c1.dec.prefill([c1.last_tok], cache, start_pos=c1.P, taps=taps)
+    from oracle import precheck
+    ref = precheck.residual_score(taps[layer], w.astype(np.float64), b)
+    got = float(scores.item())
+    print("C1 pre-check score layer", layer, got, "oracle", ref)
+    assert abs(got - ref) <= TOL
