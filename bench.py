@@ -57,12 +57,14 @@ def measured_traffic(name="lm_head_c2_traffic.md"):
 SOFT_TOPK, SOFT_RHO = 10, 0.1
 
 
-def gate_variants(rgd, torch, model, kv, w, last, table, prefill, k, c, N, S, sampling_ms, reps=5):
+def gate_variants(rgd, torch, model, kv, w, last, last_tok, table, prefill, k, c, sampling_ms, reps=5):
     """Probe + gate wall time (median of `reps`, ms) of the hard gate, the soft
     compatibility gate (top-10, rho = 0.1) and the fixed-length probe (no
     table), on the typical table and on an adversarial one (an entry equal to
     the first k-1 greedy tokens and different at token k: a full-length miss),
-    each also as a fraction of ungated sampling time per step."""
+    each also as a fraction of ungated sampling time per step; and the cost of
+    the residual-stream pre-check (its readout inside the prefill, and probe +
+    gate of a prompt it skips)."""
     import statistics
     import numpy as np
     dev = "cuda"
@@ -100,6 +102,35 @@ def gate_variants(rgd, torch, model, kv, w, last, table, prefill, k, c, N, S, sa
         ms, n, e = timed(fn)
         out[name] = {"probe_gate_ms": round(ms, 3), "probe_tokens": n, "event": e,
                      "overhead": round(ms / sampling_ms, 5) if sampling_ms > 0 else None}
+
+    # residual-stream pre-check (random classifier weights: the cost, not the accuracy): the
+    # prefill with and without the readout, and probe + gate of a prompt it skips (theta = 1)
+    d = w.d_model
+    cls_w = torch.from_numpy((np.random.default_rng(0).normal(size=d) / np.sqrt(d)).astype(np.float32)).to(dev)
+    scores = torch.empty(1, dtype=torch.float32, device=dev)
+    tok = torch.tensor([[int(last_tok)]], dtype=torch.int32, device=dev)
+
+    def pf(scored):
+        kv.set_prefix_len(0, w.synthetic_prefix)
+        if scored:
+            rgd.prefill_kv_scored(model, kv, tok, w.synthetic_prefix, last, w.n_layers, cls_w, 0.0, scores)
+        else:
+            rgd.prefill_kv(model, kv, tok, w.synthetic_prefix, last)
+        torch.cuda.synchronize()
+
+    def med(fn, n=reps * 2):
+        ts = []
+        for _ in range(n):
+            t0 = time.perf_counter()
+            fn()
+            ts.append((time.perf_counter() - t0) * 1e3)
+        return statistics.median(ts)
+    plain_ms, scored_ms = med(lambda: pf(False)), med(lambda: pf(True))
+    skip_ms, n, e = timed(lambda: rgd.probe_adaptive(model, kv, last, table, 1, k, c, -1, 0, 0.0, scores, 1.0,
+                                                     ptok, plen, ev))
+    out["precheck"] = {"layer": w.n_layers, "prefill_ms": round(plain_ms, 3), "prefill_scored_ms": round(scored_ms, 3),
+                       "skipped_probe_gate_ms": round(skip_ms, 3), "probe_tokens": n, "event": e,
+                       "overhead": round(skip_ms / sampling_ms, 5) if sampling_ms > 0 else None}
     return out
 
 
@@ -362,7 +393,7 @@ def main():
     }
     line.update(res)
     log("gate variants ...")
-    line["gate_variants"] = gate_variants(rgd, torch, model, kv, w, last, table, prefill, k, c, N, S,
+    line["gate_variants"] = gate_variants(rgd, torch, model, kv, w, last, last_tok, table, prefill, k, c,
                                           sample_s / args.steps * 1e3)
     log("sampler sweep ...")
     line["sampler_sweep"] = sampler_sweep(rgd, torch)
