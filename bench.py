@@ -152,7 +152,7 @@ def sampler_sweep(rgd, torch, reps=10):
     (argmax): average time per call over `reps` calls, events on the launch
     stream.  Algorithmic bytes per call: the logits once plus the tokens."""
     import synth
-    s = synth.C3
+    s = synth.SWEEP
     z = torch.from_numpy(synth.sweep_logits(s)).cuda()
     R, V = z.shape
     ws = torch.empty(rgd.sampler_workspace_bytes(R, V), dtype=torch.uint8, device="cuda")
@@ -249,7 +249,7 @@ def main():
     from paper_2607_20791_amd import session
 
     assert torch.cuda.is_available(), "no GPU visible"
-    w = synth.C2
+    w = synth.LAYER_P8192
     P = w.synthetic_prefix
     Pp = w.prefix_positions
     k, c, N, S = w.probe_k, 3, w.n_branches, w.steps

@@ -69,19 +69,19 @@ class Workload:
         return self.prompt_len if self.prompt_len else self.synthetic_prefix + 1
 
 
-C0 = Workload("c0-tiny-fp32", 0, "f32", n_layers=2, d_model=256, n_heads=4,
+TINY_FP32 = Workload("tiny-fp32-2layer", 0, "f32", n_layers=2, d_model=256, n_heads=4,
               n_kv_heads=2, head_dim=64, ffn=1024, vocab=8192, n_prompts=16,
               prompt_len=64, probe_k=8, n_entries=16, per_prompt_table=True,
               n_branches=1, steps=32, temperature=2.0, min_p=0.1)
-C1 = Workload("c1-8b-layer-p512", 1, "bf16", n_layers=1, d_model=4096, n_heads=32,
+LAYER_P512 = Workload("8b-layer-p512", 1, "bf16", n_layers=1, d_model=4096, n_heads=32,
               n_kv_heads=8, head_dim=128, ffn=14336, vocab=128256, n_prompts=1,
               synthetic_prefix=512, probe_k=16, n_entries=64, n_branches=16,
               steps=64, temperature=1.5, min_p=0.1)
-C2 = Workload("c2-8b-layer-p8192", 2, "bf16", n_layers=1, d_model=4096, n_heads=32,
+LAYER_P8192 = Workload("8b-layer-p8192", 2, "bf16", n_layers=1, d_model=4096, n_heads=32,
               n_kv_heads=8, head_dim=128, ffn=14336, vocab=128256, n_prompts=1,
               synthetic_prefix=8192, probe_k=16, n_entries=64, n_branches=64,
               steps=128, temperature=2.0, min_p=0.05)
-C4 = Workload("c4-8b-8layer-b32", 4, "bf16", n_layers=8, d_model=4096, n_heads=32,
+MODEL_8LAYER = Workload("8b-8layer-32x1024", 4, "bf16", n_layers=8, d_model=4096, n_heads=32,
               n_kv_heads=8, head_dim=128, ffn=14336, vocab=128256, n_prompts=32,
               prompt_len=1024, probe_k=16, n_entries=64, n_branches=8, steps=256,
               temperature=2.0, min_p=0.1)
@@ -89,7 +89,7 @@ C4 = Workload("c4-8b-8layer-b32", 4, "bf16", n_layers=8, d_model=4096, n_heads=3
 
 @dataclass(frozen=True)
 class SamplerSweep:
-    name: str = "c3-sampler-sweep"
+    name: str = "sampler-sweep-256x152064"
     index: int = 3
     vocab: int = 152064
     rows: int = 256
@@ -100,9 +100,9 @@ class SamplerSweep:
     max_gap: float = 12.0
 
 
-C3 = SamplerSweep()
+SWEEP = SamplerSweep()
 
-WORKLOADS = {"c0": C0, "c1": C1, "c2": C2, "c3": C3, "c4": C4}
+WORKLOADS = {w.name: w for w in (TINY_FP32, LAYER_P512, LAYER_P8192, SWEEP, MODEL_8LAYER)}
 
 
 def scaled(w: Workload, **kw) -> Workload:
@@ -243,7 +243,7 @@ def forced_history(w: Workload, rows: int, steps: int, name: str = "forced") -> 
     return rng(w.index, name).integers(0, w.vocab, size=(rows, steps), dtype=np.int32)
 
 
-def sweep_logits(s: SamplerSweep = C3, rows: int | None = None, vocab: int | None = None) -> np.ndarray:
+def sweep_logits(s: SamplerSweep = SWEEP, rows: int | None = None, vocab: int | None = None) -> np.ndarray:
     """[rows][V] float32 logits: z_i = eps_i + b_{pi(i)}, eps ~ N(0,1), with rank
     bias b_r = gap * (r^-s - V^-s) / (1 - V^-s), r = 1..V, and pi a uniform random
     permutation per row, so b_1 - b_V = gap exactly."""

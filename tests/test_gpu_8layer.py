@@ -21,7 +21,7 @@ from oracle import gate as ogate
 from tests.gpu_common import seeds_tensor, torch
 
 pytestmark = pytest.mark.gpu
-W4 = synth.C4
+W4 = synth.MODEL_8LAYER
 
 
 @pytest.fixture(scope="module")
@@ -31,7 +31,7 @@ def rgd():
 
 
 @pytest.fixture(scope="module")
-def c4(rgd):
+def m8(rgd):
     t = torch()
     from paper_2607_20791_amd import session
     w = W4
@@ -46,7 +46,7 @@ def c4(rgd):
     t0 = time.perf_counter()
     rgd.prefill_kv(m, kv, toks, 0, last)
     t.cuda.synchronize()
-    print(f"C4 prefill of {B} x {n} tokens: {time.perf_counter() - t0:.3f} s")
+    print(f"8-layer model: prefill of {B} x {n} tokens: {time.perf_counter() - t0:.3f} s")
     return dict(w=w, model=m, kv=kv, last=last, B=B, k=k, N=N, S=S)
 
 
@@ -58,10 +58,10 @@ def _ungated(rgd, c, prompts, seeds):
     return out
 
 
-def test_c4_gated_vs_ungated(rgd, c4):
+def test_8layer_gated_vs_ungated(rgd, m8):
     t = torch()
-    w, m, kv, last = c4["w"], c4["model"], c4["kv"], c4["last"]
-    B, k, N, S = c4["B"], c4["k"], c4["N"], c4["S"]
+    w, m, kv, last = m8["w"], m8["model"], m8["kv"], m8["last"]
+    B, k, N, S = m8["B"], m8["k"], m8["N"], m8["S"]
     before = (kv.prefix_k.clone(), kv.prefix_v.clone())
     # greedy sequences of every prompt (T = 0), used to seed the table
     greedy = t.full((B, 1, k), -1, dtype=t.int32, device="cuda")
@@ -85,18 +85,18 @@ def test_c4_gated_vs_ungated(rgd, c4):
     rgd.probe(m, kv, last, table, B, k, 3, -1, ptok, plen, ev)
     dec, miss = rgd.gate(kv, ev, B)
     miss_seeds = np.concatenate([seeds_all[b * N:(b + 1) * N] for b in miss])
-    gated = _ungated(rgd, c4, miss, seeds_tensor(miss_seeds))
+    gated = _ungated(rgd, m8, miss, seeds_tensor(miss_seeds))
     t.cuda.synchronize()
     t_gated = time.perf_counter() - t0
     # ungated: every prompt sampled, no probe
     t0 = time.perf_counter()
-    full = _ungated(rgd, c4, range(B), seeds_tensor(seeds_all))
+    full = _ungated(rgd, m8, range(B), seeds_tensor(seeds_all))
     t.cuda.synchronize()
     t_ungated = time.perf_counter() - t0
     rgd.check_status(m)
 
     hits = [b for b in range(B) if dec[b] == 1]
-    print(f"C4: {len(hits)} hits, {len(miss)} misses; gated {t_gated:.3f} s "
+    print(f"8-layer model: {len(hits)} hits, {len(miss)} misses; gated {t_gated:.3f} s "
           f"({len(miss) * N * S + sum(int(x) for x in plen.cpu()[hits])} tokens returned), "
           f"ungated {t_ungated:.3f} s ({B * N * S} tokens)")
     # the decision of each prompt follows from its greedy sequence (exact integer logic)
@@ -114,7 +114,7 @@ def test_c4_gated_vs_ungated(rgd, c4):
     full_h, gated_h = full.cpu().numpy(), gated.cpu().numpy()
     for i, b in enumerate(miss):       # a gated miss samples what ungated sampling does
         assert np.array_equal(gated_h[i], full_h[b]), b
-    again = _ungated(rgd, c4, range(B), seeds_tensor(seeds_all))
+    again = _ungated(rgd, m8, range(B), seeds_tensor(seeds_all))
     t.cuda.synchronize()
     assert t.equal(again, full)
     assert t.equal(before[0], kv.prefix_k) and t.equal(before[1], kv.prefix_v)

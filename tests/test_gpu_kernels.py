@@ -11,11 +11,11 @@ pytestmark = pytest.mark.gpu
 
 # head layout of the Llama-3-8B layer, with a small d_model/ffn/vocab where
 # the kernel under test does not depend on them
-ATTN_BF16 = synth.scaled(synth.C2, name="attn-bf16", d_model=512, ffn=512, vocab=1024)
-ATTN_F32 = synth.scaled(synth.C0, name="attn-f32", vocab=1024)
+ATTN_BF16 = synth.scaled(synth.LAYER_P8192, name="attn-bf16", d_model=512, ffn=512, vocab=1024)
+ATTN_F32 = synth.scaled(synth.TINY_FP32, name="attn-f32", vocab=1024)
 # 8 and 16 query heads per KV head (the tail merge loops over heads per wave)
-ATTN_G8 = synth.scaled(synth.C2, name="attn-g8", n_kv_heads=4, d_model=512, ffn=512, vocab=1024)
-ATTN_G16 = synth.scaled(synth.C2, name="attn-g16", n_kv_heads=2, d_model=512, ffn=512, vocab=1024)
+ATTN_G8 = synth.scaled(synth.LAYER_P8192, name="attn-g8", n_kv_heads=4, d_model=512, ffn=512, vocab=1024)
+ATTN_G16 = synth.scaled(synth.LAYER_P8192, name="attn-g16", n_kv_heads=2, d_model=512, ffn=512, vocab=1024)
 
 
 @pytest.fixture(scope="module")
@@ -34,7 +34,7 @@ def head_model(rgd):
     """A model whose LM head is the full 128256 x 4096 bf16 head of the 8B-shaped
     workloads (its other tensors are tiny and unused by this kernel)."""
     from paper_2607_20791_amd import session
-    w = synth.C2
+    w = synth.LAYER_P8192
     head = synth.tensor(w, "lm_head", (w.vocab, w.d_model), 0.02)
     mini = synth.scaled(w, name="lm-mini", ffn=128, n_heads=1, n_kv_heads=1)
     small = synth.model_weights(synth.scaled(mini, vocab=128))

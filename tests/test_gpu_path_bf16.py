@@ -52,12 +52,12 @@ class World:
 
 @pytest.fixture(scope="module")
 def c1(rgd):
-    return World(rgd, synth.C1)
+    return World(rgd, synth.LAYER_P512)
 
 
 @pytest.fixture(scope="module")
 def c2(rgd):
-    return World(rgd, synth.C2)
+    return World(rgd, synth.LAYER_P8192)
 
 
 def _last_logits(rgd, wd):
@@ -174,5 +174,5 @@ def test_c1_residual_precheck_score(rgd, c1, layer):
     from oracle import precheck
     ref = precheck.residual_score(taps[layer], w.astype(np.float64), b)
     got = float(scores.item())
-    print("C1 pre-check score layer", layer, got, "oracle", ref)
+    print("512-prefix layer: pre-check score after block", layer, got, "oracle", ref)
     assert abs(got - ref) <= TOL

@@ -12,7 +12,7 @@ from oracle.model import Decoder, KVCache
 from tests.gpu_common import judge_draw, rel_err, seeds_tensor, torch
 
 pytestmark = pytest.mark.gpu
-W0 = synth.C0
+W0 = synth.TINY_FP32
 MARGIN = 1e-4
 
 

@@ -13,7 +13,7 @@ from oracle.model import Decoder, KVCache
 from tests.gpu_common import torch
 
 pytestmark = pytest.mark.gpu
-W0 = synth.C0
+W0 = synth.TINY_FP32
 TOL = 1e-5
 
 

@@ -60,8 +60,8 @@ def _check_rows(z, T, pmin, got, seeds, ctr, stream):
     return counts
 
 
-@pytest.mark.parametrize("T", synth.C3.temperatures)
-@pytest.mark.parametrize("pmin", synth.C3.min_ps)
+@pytest.mark.parametrize("T", synth.SWEEP.temperatures)
+@pytest.mark.parametrize("pmin", synth.SWEEP.min_ps)
 def test_minp_single_draw_grid(rgd, z, T, pmin):
     rows = z[:48]
     seeds = np.arange(48, dtype=np.uint64)

@@ -15,7 +15,7 @@ from tests.gpu_common import torch
 
 pytestmark = pytest.mark.gpu
 MARGIN = 1e-4
-W0 = synth.C0
+W0 = synth.TINY_FP32
 
 
 @pytest.fixture(scope="module")
@@ -30,7 +30,7 @@ def vocab_model(rgd):
     (tiny otherwise: the probe-step hook uses only its vocabulary and
     workspace)."""
     from paper_2607_20791_amd import session
-    w = synth.scaled(synth.C2, name="soft-mini", d_model=128, ffn=128, n_heads=1, n_kv_heads=1)
+    w = synth.scaled(synth.LAYER_P8192, name="soft-mini", d_model=128, ffn=128, n_heads=1, n_kv_heads=1)
     return session.build_model(synth.model_weights(w), max_rows=64, max_pos=64)
 
 

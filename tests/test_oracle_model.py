@@ -9,7 +9,7 @@ import synth
 from oracle import model as om
 from oracle.model import Decoder, KVCache
 
-TINY = synth.scaled(synth.C0, name="tiny", n_layers=2, d_model=32, n_heads=4, n_kv_heads=2,
+TINY = synth.scaled(synth.TINY_FP32, name="tiny", n_layers=2, d_model=32, n_heads=4, n_kv_heads=2,
                     head_dim=8, ffn=48, vocab=97, weight_std=0.3)
 
 

@@ -9,7 +9,7 @@ import synth
 from oracle import gate, precheck, rgd, sampler
 from oracle.model import Decoder, KVCache, rmsnorm, linear
 
-TINY = synth.scaled(synth.C0, name="tiny-pre", n_layers=2, d_model=32, n_heads=4, n_kv_heads=2,
+TINY = synth.scaled(synth.TINY_FP32, name="tiny-pre", n_layers=2, d_model=32, n_heads=4, n_kv_heads=2,
                     head_dim=8, ffn=48, vocab=61, weight_std=0.5)
 PROMPT = [3, 14, 15, 9, 2, 6]
 

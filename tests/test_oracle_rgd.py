@@ -7,7 +7,7 @@ import synth
 from oracle import gate, philox, rgd, sampler
 from oracle.model import Decoder, KVCache
 
-TINY = synth.scaled(synth.C0, name="tiny-rgd", n_layers=1, d_model=32, n_heads=4, n_kv_heads=2,
+TINY = synth.scaled(synth.TINY_FP32, name="tiny-rgd", n_layers=1, d_model=32, n_heads=4, n_kv_heads=2,
                     head_dim=8, ffn=48, vocab=61, weight_std=0.5)
 
 
