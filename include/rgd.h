@@ -44,7 +44,7 @@ enum rgd_status {
   RGD_E_INVALID_ARG = 1, /* null pointer, size out of range, bad enum */
   RGD_E_OOM = 2,         /* page pool or workspace exhausted */
   RGD_E_HIP = 3,         /* a HIP runtime call failed */
-  RGD_E_UNSUPPORTED = 4, /* dtype or shape this build does not handle */
+  RGD_E_UNSUPPORTED = 4, /* dtype or shape the library does not handle */
   RGD_E_NONFINITE = 5,   /* a logit row had a non-finite maximum */
   RGD_E_STATE = 6        /* entry points called out of order */
 };
