@@ -56,7 +56,26 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
   constexpr int NTH = NW * 64, XSEG = MT * 16 * 8 * XS, XPT = (XSEG + NTH - 1) / NTH;
   static_assert(XS % SW == 0 || SW % XS == 0, "ring slots must stay static within an X stage");
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, col16 = lane & 15;
-  const int m0 = blockIdx.y * (MT * 16);
+  // Workgroups are handed out in linear order (x fastest), round-robin over
+  // the chip's 8 XCDs, each with its own L2.  With several row blocks, the
+  // work is reordered so that the row blocks of one column group are 8 apart
+  // in that order: on one XCD at nearly the same time, so the later blocks'
+  // weight reads can hit the lines the first one brought into that L2.
+  int gx = blockIdx.x, gy = blockIdx.y;
+  if (MT > 4 && gridDim.y > 1) {  // 64-row tiles are launched as one row block
+    const int G = gridDim.x, Y = gridDim.y;
+    const int lin = blockIdx.x + blockIdx.y * G;
+    const int full = (G / 8) * 8;  // column groups in whole octets
+    if (lin < full * Y) {
+      gy = (lin / 8) % Y;
+      gx = (lin / 8 / Y) * 8 + lin % 8;
+    } else {
+      const int rem = lin - full * Y, gr = G - full;
+      gx = full + rem % gr;
+      gy = rem / gr;
+    }
+  }
+  const int m0 = gy * (MT * 16);
   const int split = blockIdx.z;
   const int K = a.K, nst = K / kStep;
   const int st0 = int((long long)split * nst / a.splits), st1 = int((long long)(split + 1) * nst / a.splits);
@@ -64,7 +83,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
   // panels of this wave
   constexpr int HALF = (MODE == GEMM_SILU) ? NW / 2 : NW;
   const int wslot = (MODE == GEMM_SILU) ? (wave % HALF) : wave;
-  const int p0 = (blockIdx.x * HALF + wslot) * NT;  // first panel (in units of 16 columns)
+  const int p0 = (gx * HALF + wslot) * NT;  // first panel (in units of 16 columns)
   const bf16_t* wp[NT];
   int ncol[NT];
 #pragma unroll
@@ -218,7 +237,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
       float v = red[0][t];
       for (int w = 1; w < NW; ++w) v = fmaxf(v, red[w][t]);
       const int m = m0 + t;
-      if (m < a.M) a.tilemax[(long long)m * a.ntiles + blockIdx.x] = v;
+      if (m < a.M) a.tilemax[(long long)m * a.ntiles + gx] = v;
     }
   }
 }
@@ -305,6 +324,10 @@ int gemm_groups(int mode, int N) {
 // LDS stage), chosen by measurement at the decode shapes of an 8B-class layer:
 // split-K projections <1, 8, 4, 2>, SwiGLU <1, 4, 4, 4>, LM head <4, 8, 2, 1> (512 columns per
 // workgroup: the X rows every workgroup streams through LDS cost half as much per weight byte).
+// Above 64 rows (128-row tiles) each X fragment read from LDS must feed more than one MFMA, or
+// LDS reads, not HBM, set the pace: split-K and SwiGLU then run two panels per wave on four
+// waves (<2, 4, 4>; the same 128 columns per workgroup for split-K, twice the columns for
+// SwiGLU).  A row's arithmetic is the same under every shape (same k order, same split-K).
 hipError_t gemm_bf16(const GemmArgs& a, hipStream_t s) {
   if (a.K % kStep != 0 || a.M < 1 || a.splits < 1 || a.splits > a.K / kStep) return hipErrorInvalidValue;
   const int g = gemm_groups(a.mode, a.N);
@@ -312,10 +335,11 @@ hipError_t gemm_bf16(const GemmArgs& a, hipStream_t s) {
     case GEMM_STORE:
       for (int i = 1; i < a.nseg; ++i)
         if (a.seg[i].n0 % 128) return hipErrorInvalidValue;  // a workgroup never straddles segments
-      return launch_bf16<1, 8, 4, GEMM_STORE, 2>(a, g, s);
+      return a.M > 64 ? launch_bf16<2, 4, 4, GEMM_STORE, 2>(a, g, s) : launch_bf16<1, 8, 4, GEMM_STORE, 2>(a, g, s);
     case GEMM_SILU:
       if (a.splits != 1) return hipErrorInvalidValue;
-      return launch_bf16<1, 4, 4, GEMM_SILU, 4>(a, g, s);
+      return a.M > 64 ? launch_bf16<2, 4, 4, GEMM_SILU, 4>(a, (a.N + 63) / 64, s)
+                      : launch_bf16<1, 4, 4, GEMM_SILU, 4>(a, g, s);
     case GEMM_LOGITS:
       if (a.splits != 1 || a.ntiles != g) return hipErrorInvalidValue;
       return launch_bf16<4, 8, 2, GEMM_LOGITS, 1>(a, g, s);
