@@ -146,11 +146,14 @@ def algorithmic(w, R, P, tails):
     return lm_bytes, lm_flops, att_bytes, att_flops, samp_bytes
 
 
-def sampler_sweep(rgd, torch, reps=10):
+def sampler_sweep(rgd, torch, reps=20, flush_mode="read"):
     """The standalone min-p sampler on the sampler-sweep workload (256 rows of
     152064 Zipf-biased logits) at every (T, p_min) grid point, plus T = 0
-    (argmax): average time per call over `reps` calls, events on the launch
-    stream.  Algorithmic bytes per call: the logits once plus the tokens."""
+    (argmax): median time of `reps` calls, each timed alone with events on the
+    launch stream after a 512 MiB write that evicts the logits from the
+    last-level cache (the 155.7 MB of logits would otherwise stay resident in
+    it from one call to the next).  Algorithmic bytes per call: the logits
+    once plus the tokens."""
     import synth
     s = synth.SWEEP
     z = torch.from_numpy(synth.sweep_logits(s)).cuda()
@@ -160,17 +163,26 @@ def sampler_sweep(rgd, torch, reps=10):
     seeds = torch.arange(R, dtype=torch.int64, device="cuda")
     nbytes = R * V * 4 + R * 4
 
+    flush = torch.ones(128 << 20, dtype=torch.float32, device="cuda")
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+
+    def evict():
+        if flush_mode == "read":
+            flush.max()
+        elif flush_mode == "write":
+            flush.fill_(1)
+
     def timed(f):
-        for _ in range(2):
+        for _ in range(3):
             f()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(reps):
+        for e0, e1 in ev:
+            evict()
+            e0.record()
             f()
-        e1.record()
+            e1.record()
         torch.cuda.synchronize()
-        return e0.elapsed_time(e1) * 1e3 / reps
+        t = sorted(e0.elapsed_time(e1) * 1e3 for e0, e1 in ev)
+        return t[len(t) // 2]
 
     pts = []
     for T in s.temperatures:

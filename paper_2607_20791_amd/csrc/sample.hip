@@ -7,8 +7,14 @@
 // chunk's kept-weight sum; the second has one workgroup per row, forms the
 // chunk prefix in chunk order, locates u * W and rescans that one chunk with a
 // block-wide prefix scan.  Logits are read once per draw from HBM (plus the
-// one rescanned chunk); the row maximum comes in as partial maxima (from the
-// LM-head epilogue or a chunk-max pass).  No cross-workgroup synchronisation.
+// one rescanned chunk); the row maximum comes in as partial maxima from the
+// LM-head epilogue.  Standalone rows have no such maxima: the chunk pass keeps
+// each chunk's maximum and its sum relative to it, and only chunks inside the
+// min-p window below the row maximum are summed again; with many rows one
+// workgroup per row does all of it in one launch.  No cross-workgroup
+// synchronisation: a release/acquire handshake between the workgroups of a
+// row (the last to arrive makes the draw) writes back the whole L2 at every
+// release and measured ten times slower.
 #include "gatecheck.hpp"
 #include "kernels.hpp"
 #include "philox.hpp"
@@ -19,6 +25,12 @@ namespace rgd {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+
+// Standalone rows: from this many rows on, one workgroup per row (one launch)
+// keeps every CU streaming; below it, chunk workgroups (two launches) spread a
+// few rows over the whole chip.  Measured on the 152064-logit sweep rows:
+// 256 rows 39 us vs 41 us; 16 rows 25 us vs 16 us.
+constexpr int kRowKernelMinRows = 128;
 
 // Kept-weight of one logit.  The hardware 2^x (no denormal range fix-up: a
 // weight below 2^-126 flushes to 0); the chunk sums and the rescan use this
@@ -145,19 +157,22 @@ RGD_DEV float block_inclusive_scan(float v, float* wsum) {
 }
 
 // Selects the token of row r for target u (in [0,1)); `mine` is chunk
-// threadIdx.x's kept sum (0 past the last chunk).  Returns the token id (valid
-// in every thread).
+// threadIdx.x's kept sum (0 past the last chunk).  NTH threads; chunk / NTH
+// must be a multiple of 4 and at most 16.  Returns the token id (valid in every
+// thread).
+template <int NTH>
 RGD_DEV int select_token(const SampleArgs& a, int r, float mx, float u, float mine) {
+  constexpr int NW = NTH / 64, PMAX = 4096 / NTH;
   __shared__ float csum[256];
   __shared__ int sh_chunk, sh_last_nz;
   __shared__ float sh_base, sh_target;
-  __shared__ float wsum[4];
-  __shared__ int red_i[4];
+  __shared__ float wsum[NW];
+  __shared__ int red_i[NW];
   const float kT = kLog2e / a.T;
   // running sum over chunks in chunk order (one chunk per thread)
   const int c = threadIdx.x;
   const float incl_c = block_inclusive_scan(mine, wsum);
-  csum[c] = incl_c;
+  if (c < 256) csum[c] = incl_c;
   if (c == 0) {
     sh_chunk = 0x7FFFFFFF;
     sh_last_nz = 0;
@@ -178,19 +193,19 @@ RGD_DEV int select_token(const SampleArgs& a, int r, float mx, float u, float mi
   }
   __syncthreads();
   // rescan of the chosen chunk: thread t owns `per` consecutive logits
-  // (per = chunk / 256 <= 16, a multiple of 4; V is a multiple of 4)
+  // (per = chunk / NTH <= PMAX, a multiple of 4; V is a multiple of 4)
   const int lo = sh_chunk * a.chunk, hi = min(a.V, lo + a.chunk);
-  const int per = a.chunk / 256;
+  const int per = a.chunk / NTH;
   const int e0 = lo + threadIdx.x * per, e1 = min(hi, e0 + per);
   const float* zr = a.z + r * a.ldz;
-  float4 zv[4];
+  float4 zv[PMAX / 4];
 #pragma unroll
-  for (int k = 0; k < 4; ++k)
+  for (int k = 0; k < PMAX / 4; ++k)
     zv[k] = (4 * k < per && e0 + 4 * k < e1) ? *(const float4*)(zr + e0 + 4 * k) : float4{0.f, 0.f, 0.f, 0.f};
-  float wv[16];
+  float wv[PMAX];
   float ts = 0.f;
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
+  for (int i = 0; i < PMAX; ++i) {
     const float zi = i % 4 == 0 ? zv[i / 4].x : i % 4 == 1 ? zv[i / 4].y : i % 4 == 2 ? zv[i / 4].z : zv[i / 4].w;
     const float w = (i < per && e0 + i < e1) ? kept_weight(zi, mx, kT, a.p_min) : -1.f;
     wv[i] = w;
@@ -200,7 +215,7 @@ RGD_DEV int select_token(const SampleArgs& a, int r, float mx, float u, float mi
   float run = sh_base + (incl - ts);
   int found = 0x7FFFFFFF, last = -1;
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
+  for (int i = 0; i < PMAX; ++i) {
     if (wv[i] >= 0.f) {
       run += wv[i];
       last = e0 + i;
@@ -218,12 +233,12 @@ RGD_DEV int select_token(const SampleArgs& a, int r, float mx, float u, float mi
   if ((threadIdx.x & 63) == 0) red_i[threadIdx.x >> 6] = f;
   __syncthreads();
   int fb = red_i[0];
-  for (int i = 1; i < 4; ++i) fb = min(fb, red_i[i]);
+  for (int i = 1; i < NW; ++i) fb = min(fb, red_i[i]);
   __syncthreads();
   if ((threadIdx.x & 63) == 0) red_i[threadIdx.x >> 6] = l;
   __syncthreads();
   int lb = red_i[0];
-  for (int i = 1; i < 4; ++i) lb = max(lb, red_i[i]);
+  for (int i = 1; i < NW; ++i) lb = max(lb, red_i[i]);
   return fb != 0x7FFFFFFF ? fb : lb;
 }
 
@@ -260,8 +275,8 @@ __global__ __launch_bounds__(256) void minp_sum_kernel(SampleArgs a) {
 // logits.  Pass 1 writes each chunk's maximum m_c and its kept sum relative
 // to m_c.  With m the row maximum, a chunk whose m_c == m has the exact sum,
 // a chunk whose best weight exp2((m_c - m) kT) is below p_min keeps nothing,
-// and only the chunks in between are read again (pass 2) to sum the weights
-// relative to m.
+// and only the chunks in between are read again (by the second kernel, which
+// then makes the draw) to sum the weights relative to m.
 __global__ __launch_bounds__(256) void minp_cand_kernel(SampleArgs a, float* cmax) {
   __shared__ float red[4];
   const int c = blockIdx.x, r = blockIdx.y;
@@ -292,32 +307,146 @@ __global__ __launch_bounds__(256) void minp_cand_kernel(SampleArgs a, float* cma
   }
 }
 
-__global__ __launch_bounds__(256) void minp_fix_kernel(SampleArgs a) {
-  __shared__ float red[4];
-  const int c = blockIdx.x, r = blockIdx.y;
-  const float mx = row_max_from_partials(a.pmax, a.npmax, r, red);
-  const float mc = a.pmax[(long long)r * a.npmax + c];
+// Standalone rows, second kernel (one workgroup of 1024 threads per row): the
+// row maximum from the chunk maxima, the kept sums of the chunks pass 1 could
+// not settle, then the draw.  Each wave recomputes whole chunks (16 KB, 16
+// float4 per lane) so that up to 16 of them are in flight at once.  The
+// settled sums are written back for further draws from the same row.
+__global__ __launch_bounds__(1024) void minp_fixsel_kernel(SampleArgs a) {
+  __shared__ float red[16];
+  __shared__ float fixed[256];
+  __shared__ int wlist[256];
+  __shared__ int nwin;
+  const int r = blockIdx.x, c = threadIdx.x;
+  const long long r0 = (long long)r * a.nchunks;
+  const bool own = c < a.nchunks;
+  const float mc = own ? a.pmax[r0 + c] : -INFINITY;
+  float mine = own ? a.chunk_sums[r0 + c] : 0.f;
+  if (c == 0) nwin = 0;
+  const float mx = block_max(mc, red);  // its barriers also publish nwin = 0
   const float kT = kLog2e / a.T;
-  if (mc == mx) return;                         // exact already
-  if (kept_weight(mc, mx, kT, a.p_min) < 0.f) {  // nothing of this chunk is kept
-    if (threadIdx.x == 0) a.chunk_sums[(long long)r * a.nchunks + c] = 0.f;
-    return;
-  }
+  const bool exact = mc == mx;
+  const bool empty = !exact && kept_weight(mc, mx, kT, a.p_min) < 0.f;
+  if (own && !exact && !empty) wlist[atomicAdd(&nwin, 1)] = c;
+  __syncthreads();
+  const int nw = nwin, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const float* zr = a.z + r * a.ldz;
-  const int lo = c * a.chunk, hi = min(a.V, lo + a.chunk);
-  float sum = 0.f;
+  for (int i = wave; i < nw; i += 16) {
+    const int ch = wlist[i];
+    const int lo = ch * a.chunk, hi = min(a.V, lo + a.chunk);
+    float4 v[16];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int i = lo + (threadIdx.x + k * 256) * 4;
-    if (i < hi) {
-      const float4 v = *(const float4*)(zr + i);
-      const float w0 = kept_weight(v.x, mx, kT, a.p_min), w1 = kept_weight(v.y, mx, kT, a.p_min);
-      const float w2 = kept_weight(v.z, mx, kT, a.p_min), w3 = kept_weight(v.w, mx, kT, a.p_min);
+    for (int k = 0; k < 16; ++k) {
+      const int e = lo + (lane + k * 64) * 4;
+      v[k] = e < hi ? *(const float4*)(zr + e) : float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+    }
+    float sum = 0.f;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const float w0 = kept_weight(v[k].x, mx, kT, a.p_min), w1 = kept_weight(v[k].y, mx, kT, a.p_min);
+      const float w2 = kept_weight(v[k].z, mx, kT, a.p_min), w3 = kept_weight(v[k].w, mx, kT, a.p_min);
       sum += (w0 > 0.f ? w0 : 0.f) + (w1 > 0.f ? w1 : 0.f) + (w2 > 0.f ? w2 : 0.f) + (w3 > 0.f ? w3 : 0.f);
     }
+    sum = wave_sum(sum);
+    if (lane == 0) fixed[ch] = sum;
   }
-  sum = block_sum(sum, red);
-  if (threadIdx.x == 0) a.chunk_sums[(long long)r * a.nchunks + c] = sum;
+  __syncthreads();
+  if (own && !exact) {
+    mine = empty ? 0.f : fixed[c];
+    a.chunk_sums[r0 + c] = mine;
+  }
+  const float u = philox_uniform(a.seeds[r], a.ctr, a.stream);
+  const int tok = select_token<1024>(a, r, mx, u, mine);
+  if (threadIdx.x == 0) {
+    a.out[r * a.out_stride + a.out_col] = tok;
+    if (a.cur_tok) a.cur_tok[r] = tok;
+  }
+}
+
+// Standalone rows in one launch: one workgroup of 1024 threads per row.  Each
+// wave streams whole 4096-logit chunks (16 float4 per lane, one coalesced
+// 1 KiB request per load instruction) and keeps the chunk's maximum m_c and
+// its kept sum relative to m_c in LDS.  After a barrier the row maximum is
+// known; the chunks whose maximum lies inside the min-p window below it are
+// summed again relative to it (rereads), and the draw follows.  The chunk
+// maxima and settled sums are also written out for further draws.
+__global__ __launch_bounds__(1024) void minp_row_kernel(SampleArgs a, float* cmax) {
+  __shared__ float cm[256], cs[256];
+  __shared__ float red[16];
+  __shared__ int wlist[256];
+  __shared__ int nwin;
+  const int r = blockIdx.x, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const float* zr = a.z + r * a.ldz;
+  const float kT = kLog2e / a.T;
+  for (int c = wave; c < a.nchunks; c += 16) {
+    const int lo = c * a.chunk, hi = min(a.V, lo + a.chunk);
+    float4 v[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const int e = lo + (lane + k * 64) * 4;
+      v[k] = e < hi ? *(const float4*)(zr + e) : float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+    }
+    float mc = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) mc = fmaxf(mc, fmaxf(fmaxf(v[k].x, v[k].y), fmaxf(v[k].z, v[k].w)));
+    mc = wave_max(mc);
+    float sum = 0.f;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const float w0 = kept_weight(v[k].x, mc, kT, a.p_min), w1 = kept_weight(v[k].y, mc, kT, a.p_min);
+      const float w2 = kept_weight(v[k].z, mc, kT, a.p_min), w3 = kept_weight(v[k].w, mc, kT, a.p_min);
+      sum += (w0 > 0.f ? w0 : 0.f) + (w1 > 0.f ? w1 : 0.f) + (w2 > 0.f ? w2 : 0.f) + (w3 > 0.f ? w3 : 0.f);
+    }
+    sum = wave_sum(sum);
+    if (lane == 0) {
+      cm[c] = mc;
+      cs[c] = sum;
+    }
+  }
+  if (threadIdx.x == 0) nwin = 0;
+  __syncthreads();
+  const int c = threadIdx.x;
+  const bool own = c < a.nchunks;
+  const float mc = own ? cm[c] : -INFINITY;
+  float mine = own ? cs[c] : 0.f;
+  const float mx = block_max(mc, red);
+  const bool exact = mc == mx;
+  const bool empty = !exact && kept_weight(mc, mx, kT, a.p_min) < 0.f;
+  if (own && !exact && !empty) wlist[atomicAdd(&nwin, 1)] = c;
+  __syncthreads();
+  const int nw = nwin;
+  for (int i = wave; i < nw; i += 16) {
+    const int ch = wlist[i];
+    const int lo = ch * a.chunk, hi = min(a.V, lo + a.chunk);
+    float4 v[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const int e = lo + (lane + k * 64) * 4;
+      v[k] = e < hi ? *(const float4*)(zr + e) : float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+    }
+    float sum = 0.f;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const float w0 = kept_weight(v[k].x, mx, kT, a.p_min), w1 = kept_weight(v[k].y, mx, kT, a.p_min);
+      const float w2 = kept_weight(v[k].z, mx, kT, a.p_min), w3 = kept_weight(v[k].w, mx, kT, a.p_min);
+      sum += (w0 > 0.f ? w0 : 0.f) + (w1 > 0.f ? w1 : 0.f) + (w2 > 0.f ? w2 : 0.f) + (w3 > 0.f ? w3 : 0.f);
+    }
+    sum = wave_sum(sum);
+    if (lane == 0) cs[ch] = sum;
+  }
+  __syncthreads();
+  if (own) {
+    if (!exact) mine = empty ? 0.f : cs[c];
+    const long long rc = (long long)r * a.nchunks + c;
+    cmax[rc] = mc;
+    a.chunk_sums[rc] = mine;
+  }
+  const float u = philox_uniform(a.seeds[r], a.ctr, a.stream);
+  const int tok = select_token<1024>(a, r, mx, u, mine);
+  if (threadIdx.x == 0) {
+    a.out[r * a.out_stride + a.out_col] = tok;
+    if (a.cur_tok) a.cur_tok[r] = tok;
+  }
 }
 
 __global__ __launch_bounds__(256) void minp_select_kernel(SampleArgs a) {
@@ -327,7 +456,7 @@ __global__ __launch_bounds__(256) void minp_select_kernel(SampleArgs a) {
   const float mine = (int)threadIdx.x < a.nchunks ? a.chunk_sums[(long long)r * a.nchunks + threadIdx.x] : 0.f;
   const float mx = row_max_from_partials(a.pmax, a.npmax, r, red);
   const float u = philox_uniform(a.seeds[r], a.ctr, a.stream);
-  const int tok = select_token(a, r, mx, u, mine);
+  const int tok = select_token<256>(a, r, mx, u, mine);
   if (threadIdx.x == 0) {
     a.out[r * a.out_stride + a.out_col] = tok;
     if (a.cur_tok) a.cur_tok[r] = tok;
@@ -349,7 +478,7 @@ __global__ __launch_bounds__(256) void minp_multi_kernel(SampleArgs a, unsigned 
   const float mine = (int)threadIdx.x < a.nchunks ? a.chunk_sums[(long long)r * a.nchunks + threadIdx.x] : 0.f;
   const float mx = row_max_from_partials(a.pmax, a.npmax, r, red);
   const float u = philox_uniform(a.seeds[r], a.ctr, stream0 + unsigned(d));
-  const int tok = select_token(a, r, mx, u, mine);
+  const int tok = select_token<256>(a, r, mx, u, mine);
   if (threadIdx.x == 0) out[(long long)r * draws + d] = tok;
 }
 
@@ -429,9 +558,12 @@ hipError_t minp_sample_standalone(const SampleArgs& a0, float* cmax, hipStream_t
   SampleArgs a = a0;
   a.pmax = cmax;
   a.npmax = a.nchunks;
-  hipLaunchKernelGGL(minp_cand_kernel, dim3(a.nchunks, a.R), dim3(256), 0, s, a, cmax);
-  hipLaunchKernelGGL(minp_fix_kernel, dim3(a.nchunks, a.R), dim3(256), 0, s, a);
-  hipLaunchKernelGGL(minp_select_kernel, dim3(a.R), dim3(256), 0, s, a);
+  if (a.R >= kRowKernelMinRows) {
+    hipLaunchKernelGGL(minp_row_kernel, dim3(a.R), dim3(1024), 0, s, a, cmax);
+  } else {
+    hipLaunchKernelGGL(minp_cand_kernel, dim3(a.nchunks, a.R), dim3(256), 0, s, a, cmax);
+    hipLaunchKernelGGL(minp_fixsel_kernel, dim3(a.R), dim3(1024), 0, s, a);
+  }
   return hipGetLastError();
 }
 

@@ -122,3 +122,32 @@ def test_deterministic(rgd, z):
     a = sample_gpu(rgd, z[:64], 3.0, 0.05, seeds, ctr=3, draws=4)
     b = sample_gpu(rgd, z[:64], 3.0, 0.05, seeds, ctr=3, draws=4)
     assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("T,pmin", [(0.7, 0.05), (2.0, 0.05), (3.0, 0.05), (3.0, 0.2)])
+def test_minp_one_workgroup_per_row_with_further_draws(rgd, z, T, pmin):
+    """128 or more rows take the one-launch path (one workgroup per row, which
+    also settles the chunk sums that later draws reuse); 3 draws per row, from
+    no window chunk at all (T = 0.7) to every chunk inside the window (T = 3,
+    p_min = 0.05)."""
+    rows = z[:160]
+    seeds = np.arange(160, dtype=np.uint64) * 31 + 5
+    D = 3
+    got = sample_gpu(rgd, rows, T, pmin, seeds, ctr=11, stream0=2, draws=D)
+    counts = {"exact": 0, "margin-equal": 0, "margin-diff": 0}
+    for r in range(rows.shape[0]):
+        for d in range(D):
+            u = float(philox.uniform(int(seeds[r]), 11, 2 + d))
+            counts[judge_draw(rows[r], T, pmin, u, int(got[r, d]))] += 1
+    print(f"T={T} p_min={pmin}: {counts}")
+    # every draw was judged above; most margin cases still give the oracle's token
+    assert counts["margin-diff"] <= 0.05 * rows.shape[0] * D
+
+
+def test_edge_cases_tiny_vocab_many_rows(rgd):
+    z = np.array([[0.0, 3.0, 1.0, 3.0, -2.0, 0.5, 2.9, 1.0]] * 130, np.float32)
+    seeds = np.arange(130, dtype=np.uint64)
+    got = sample_gpu(rgd, z, 1.0, 1.0, seeds, draws=4)
+    assert set(np.unique(got)) == {1, 3}
+    got = sample_gpu(rgd, z, 1.0, 0.0, seeds, draws=8)
+    assert set(np.unique(got)) == set(range(8))
