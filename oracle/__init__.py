@@ -1,8 +1,8 @@
 """CPU oracle for refusal-gated decoding (test infrastructure only).
 
 A plain, slow, float64 numpy reference for everything the GPU path computes:
-Philox4x32-10 draws, greedy argmax, temperature-scaled min-p sampling with an
-inverse-CDF draw, grouped-query attention over a shared prompt KV plus a
+Philox4x32-10 draws, greedy argmax, temperature-scaled min-p and p-less
+sampling with an inverse-CDF draw, grouped-query attention over a shared prompt KV plus a
 per-row tail, a Llama-style decoder step and prefill, the refusal-prefix
 compatibility predicate, the greedy probe with early exit and the gate of
 Algorithm 1 (Section 3).

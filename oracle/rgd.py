@@ -12,7 +12,7 @@ from dataclasses import dataclass
 
 import numpy as np
 
-from . import gate, philox, sampler
+from . import gate, philox, pless, sampler
 from .model import Decoder, KVCache
 
 
@@ -25,9 +25,10 @@ class BranchResult:
 
 def sample_branch(model: Decoder, prefix: KVCache, last_logits, seed: int, steps: int,
                   T: float, p_min: float, forced=None, keep_logits: bool = False,
-                  stream: int = 0) -> BranchResult:
+                  stream: int = 0, truncation: str = "minp") -> BranchResult:
     """S_{T,theta}(M, p) for one branch: token s uses Philox counter (s, stream).
-    With `forced`, token forced[s] (not the drawn one) is fed after step s."""
+    With `forced`, token forced[s] (not the drawn one) is fed after step s.
+    truncation "minp" (threshold p_min) or "pless" (p_min unused)."""
     tail = KVCache(model.cfg.n_layers)
     logits = np.asarray(last_logits, np.float64)
     toks, draws, kept = [], [], []
@@ -35,7 +36,7 @@ def sample_branch(model: Decoder, prefix: KVCache, last_logits, seed: int, steps
         if keep_logits:
             kept.append(logits)
         u = float(philox.uniform(seed, s, stream))
-        d = sampler.sample_minp(logits, T, p_min, u)
+        d = pless.sample_pless(logits, T, u) if truncation == "pless" else sampler.sample_minp(logits, T, p_min, u)
         toks.append(d.token)
         draws.append(d)
         if s + 1 < steps:
