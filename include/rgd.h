@@ -242,6 +242,17 @@ int32_t rgd_sample_continuations(rgd_model* m, rgd_kv* kv, const float* last_log
                                  float T, float min_p, const uint64_t* seeds, const int32_t* forced,
                                  float* logits_tap, int32_t* out, rgd_stream stream);
 
+/* As rgd_sample_continuations, with p-less truncation in place of min-p (the
+ * truncation Section 4 samples with; its rule, from the cited p-less paper:
+ * with p = softmax(z/T), keep token i iff p_i >= sum_j p_j^2, which is
+ * exp((z_i - max z)/T) >= S2/S1 for S1, S2 the sums of those weights and of
+ * their squares).  No parameter besides T; T == 0 is greedy argmax.  The
+ * vocabulary must be a multiple of 4 (RGD_E_UNSUPPORTED otherwise). */
+int32_t rgd_sample_continuations_pless(rgd_model* m, rgd_kv* kv, const float* last_logits,
+                                       const int32_t* prompt_idx, int32_t n, int32_t N, int32_t steps,
+                                       float T, const uint64_t* seeds, const int32_t* forced,
+                                       float* logits_tap, int32_t* out, rgd_stream stream);
+
 /* Checks the device status flag raised by the sampler (non-finite row
  * maximum) and clears it.  Synchronous. */
 int32_t rgd_check_status(rgd_model* m, rgd_stream stream);
@@ -298,8 +309,8 @@ int32_t rgd_kernel_attention(rgd_model* m, const void* q, int32_t R, const int32
  * (model dtype, the already normalised final hidden state).  Asynchronous. */
 int32_t rgd_kernel_lm_head(rgd_model* m, const void* h, int32_t R, float* logits, rgd_stream stream);
 
-/* Bytes of caller-provided device workspace the two sampler entry points
- * below need for R rows of V logits. */
+/* Bytes of caller-provided device workspace the sampler entry points below
+ * need for R rows of V logits. */
 uint64_t rgd_sampler_workspace_bytes(int32_t R, int32_t V);
 
 /* Greedy token of each row of z dev fp32 [R][V] (first index of the maximum)
@@ -315,6 +326,14 @@ int32_t rgd_kernel_argmax(const float* z, int32_t R, int32_t V, void* workspace,
 int32_t rgd_kernel_sample(const float* z, int32_t R, int32_t V, float T, float min_p,
                           const uint64_t* seeds, uint32_t ctr, uint32_t stream0, int32_t draws,
                           void* workspace, int32_t* out, rgd_stream stream);
+
+/* p-less draws on z dev fp32 [R][V] (keep p_i >= sum_j p_j^2 of softmax(z/T),
+ * see rgd_sample_continuations_pless; V a multiple of 4, V <= 1048576,
+ * T > 0); seeds, counters, workspace and out as for rgd_kernel_sample.
+ * Asynchronous. */
+int32_t rgd_kernel_sample_pless(const float* z, int32_t R, int32_t V, float T, const uint64_t* seeds,
+                                uint32_t ctr, uint32_t stream0, int32_t draws, void* workspace,
+                                int32_t* out, rgd_stream stream);
 
 /* One probe step (Algorithm 1, or the soft gate of Appendix C when topk > 0)
  * for prompts 0..R-1 of the table, given their next-token logits dev fp32

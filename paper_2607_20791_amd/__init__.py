@@ -12,8 +12,8 @@ import os
 
 __all__ = [
     "RGDError", "lib", "ModelConfig", "Model", "KV", "Table", "prefill_kv", "probe", "gate",
-    "sample_continuations", "check_status", "kernel_attention", "kernel_lm_head", "kernel_argmax",
-    "kernel_sample", "sampler_workspace_bytes", "timing_enable", "timing_read", "TIMERS", "EVENT_INCOMPAT", "EVENT_STOP", "EVENT_MAXLEN",
+    "sample_continuations", "sample_continuations_pless", "check_status", "kernel_attention", "kernel_lm_head", "kernel_argmax",
+    "kernel_sample", "kernel_sample_pless", "sampler_workspace_bytes", "timing_enable", "timing_read", "TIMERS", "EVENT_INCOMPAT", "EVENT_STOP", "EVENT_MAXLEN",
     "DTYPE_F32", "DTYPE_BF16",
 ]
 
@@ -21,9 +21,9 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librgd.so")
 EXPORTS = (
     "rgd_version", "rgd_last_error", "rgd_model_create", "rgd_model_destroy", "rgd_kv_create",
     "rgd_kv_destroy", "rgd_kv_set_prefix_len", "rgd_table_create", "rgd_table_destroy",
-    "rgd_prefill_kv", "rgd_prefill_kv_scored", "rgd_probe", "rgd_probe_soft", "rgd_probe_adaptive", "rgd_gate", "rgd_sample_continuations", "rgd_check_status",
+    "rgd_prefill_kv", "rgd_prefill_kv_scored", "rgd_probe", "rgd_probe_soft", "rgd_probe_adaptive", "rgd_gate", "rgd_sample_continuations", "rgd_sample_continuations_pless", "rgd_check_status",
     "rgd_kernel_attention", "rgd_kernel_lm_head", "rgd_sampler_workspace_bytes",
-    "rgd_kernel_argmax", "rgd_kernel_sample", "rgd_kernel_probe_step", "rgd_timing_enable", "rgd_timing_read",
+    "rgd_kernel_argmax", "rgd_kernel_sample", "rgd_kernel_sample_pless", "rgd_kernel_probe_step", "rgd_timing_enable", "rgd_timing_read",
 )
 
 DTYPE_F32, DTYPE_BF16 = 0, 1
@@ -88,6 +88,7 @@ _sig("rgd_prefill_kv_scored", I32, VP, VP, VP, I32, I32, I32, VP, I32, VP, C.c_f
 _sig("rgd_kernel_probe_step", I32, VP, VP, I32, VP, I32, I32, I32, I32, C.c_float, VP, VP, VP, VP)
 _sig("rgd_gate", I32, VP, VP, I32, I32P, I32P, I32P, VP)
 _sig("rgd_sample_continuations", I32, VP, VP, VP, I32P, I32, I32, I32, F32, F32, VP, VP, VP, VP, VP)
+_sig("rgd_sample_continuations_pless", I32, VP, VP, VP, I32P, I32, I32, I32, F32, VP, VP, VP, VP, VP)
 _sig("rgd_check_status", I32, VP, VP)
 _sig("rgd_kernel_attention", I32, VP, VP, I32, I32P, I32P, VP, VP, I32, I32, VP, VP, I32, VP, I32,
      I32, I32, VP, VP)
@@ -95,6 +96,7 @@ _sig("rgd_kernel_lm_head", I32, VP, VP, I32, VP, VP)
 _sig("rgd_sampler_workspace_bytes", U64, I32, I32)
 _sig("rgd_kernel_argmax", I32, VP, I32, I32, VP, VP, VP)
 _sig("rgd_kernel_sample", I32, VP, I32, I32, F32, F32, VP, U32, U32, I32, VP, VP, VP)
+_sig("rgd_kernel_sample_pless", I32, VP, I32, I32, F32, VP, U32, U32, I32, VP, VP, VP)
 _sig("rgd_timing_enable", I32, VP, I32)
 _sig("rgd_timing_read", I32, VP, C.POINTER(C.c_double), C.POINTER(C.c_int64))
 
@@ -272,6 +274,14 @@ def sample_continuations(model, kv, last_logits, prompt_idx, N, steps, T, min_p,
                                         _ptr(out), _stream()))
 
 
+def sample_continuations_pless(model, kv, last_logits, prompt_idx, N, steps, T, seeds, out,
+                               forced=None, logits_tap=None):
+    pi, pip = _host_i32(prompt_idx)
+    _check(lib.rgd_sample_continuations_pless(model.h, kv.h, _ptr(last_logits), pip, len(pi), N, steps,
+                                              T, _ptr(seeds), _ptr(forced), _ptr(logits_tap),
+                                              _ptr(out), _stream()))
+
+
 def check_status(model):
     _check(lib.rgd_check_status(model.h, _stream()))
 
@@ -316,3 +326,9 @@ def kernel_sample(z, T, min_p, seeds, ctr, stream0, draws, workspace, out):
     R, V = z.shape
     _check(lib.rgd_kernel_sample(_ptr(z), R, V, T, min_p, _ptr(seeds), ctr, stream0, draws,
                                  _ptr(workspace), _ptr(out), _stream()))
+
+
+def kernel_sample_pless(z, T, seeds, ctr, stream0, draws, workspace, out):
+    R, V = z.shape
+    _check(lib.rgd_kernel_sample_pless(_ptr(z), R, V, T, _ptr(seeds), ctr, stream0, draws,
+                                       _ptr(workspace), _ptr(out), _stream()))

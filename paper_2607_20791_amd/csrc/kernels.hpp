@@ -138,12 +138,18 @@ struct SampleArgs {
   // selecting workgroup (null embed: not fused; needs d % 4 == 0, d <= 4096)
   const void* embed; int embed_bf16; int d; int vocab;
   const float* gain; float eps; float* x; void* xn;
+  // optional [R] per-row threshold on w (p-less); null: p_min for every row
+  const float* row_thr;
 };
 hipError_t minp_sample(const SampleArgs& a, hipStream_t s);
 // rows without producer maxima: chunk maxima into cmax [R][nchunks] and the
 // chunk sums in one read of the logits (plus rereads of chunks whose maximum
 // is within the min-p window of the row maximum), then the draw
 hipError_t minp_sample_standalone(const SampleArgs& a, float* cmax, hipStream_t s);
+// p-less truncation: chunk statistics into stats [3][R][nchunks] (maxima, sum
+// of w, sum of w^2 relative to the chunk maximum), the per-row threshold into
+// thr [R], the chunk kept sums, then the draw (chunk == 4096, V % 4 == 0)
+hipError_t pless_sample(const SampleArgs& a, float* stats, float* thr, hipStream_t s);
 // many draws per row from precomputed chunk sums (counter (ctr, stream0 + d))
 hipError_t minp_multi_draw(const SampleArgs& a, int draws, unsigned int stream0, int* out,
                            hipStream_t s);

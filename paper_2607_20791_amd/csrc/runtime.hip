@@ -113,6 +113,8 @@ struct rgd_model {
   float* logits = nullptr;
   float* tilemax = nullptr;
   float* chunk_sums = nullptr;
+  float* pl_stats = nullptr;  // p-less: chunk maxima, sums of w and w^2 [3][R][nchunks]
+  float* pl_thr = nullptr;    // p-less: per-row threshold on w [R]
   unsigned long long* best = nullptr;
   int* cur_tok = nullptr;
   int* status = nullptr;
@@ -559,13 +561,15 @@ __global__ void probe_feed_kernel(const int* prompt, int R, const int* probe_tok
   if (r < R) cur[r] = probe_tokens[(long long)prompt[r] * k + j];
 }
 
-// Selects one token per row from logits z (ldz).  T == 0: argmax.  With
+// Selects one token per row from logits z (ldz).  T == 0: argmax; otherwise
+// min-p with p_min, or p-less when pless is set (p_min unused).  With
 // fuse_embed the sampling workgroups also write the next step's input rows
 // (embedding + first RMSNorm into m->x, m->xn) where the shapes allow it;
 // *embedded tells the caller whether they did.
 int select_tokens(rgd_model* m, const float* z, long long ldz, int R, const float* pmax, int npmax, float T,
                   float p_min, const unsigned long long* seeds, unsigned ctr, int* out, long long out_stride,
-                  int out_col, int* cur, hipStream_t s, bool fuse_embed = false, bool* embedded = nullptr) {
+                  int out_col, int* cur, hipStream_t s, bool fuse_embed = false, bool* embedded = nullptr,
+                  bool pless = false) {
   const int V = m->cfg.vocab;
   if (embedded) *embedded = false;
   if (T == 0.f) {
@@ -589,7 +593,10 @@ int select_tokens(rgd_model* m, const float* z, long long ldz, int R, const floa
     if (embedded) *embedded = true;
   }
   TimeScope ts(m, RGD_TIMER_SAMPLER, s);
-  HIP_OK(minp_sample(a, s));
+  if (pless)
+    HIP_OK(pless_sample(a, m->pl_stats, m->pl_thr, s));
+  else
+    HIP_OK(minp_sample(a, s));
   return RGD_OK;
 }
 
@@ -707,6 +714,8 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
   A(&m->logits, (size_t)R * cfg->vocab * 4);
   A(&m->tilemax, (size_t)R * m->ntiles * 4);
   A(&m->chunk_sums, (size_t)R * m->nchunks * 4);
+  A(&m->pl_stats, (size_t)3 * R * m->nchunks * 4);
+  A(&m->pl_thr, (size_t)R * 4);
   A(&m->best, (size_t)R * 8);
   A(&m->cur_tok, (size_t)R * 4);
   A(&m->status, 4);
@@ -1165,15 +1174,22 @@ int32_t rgd_gate(rgd_kv* kv, const int32_t* event, int32_t B, int32_t* decision_
   return RGD_OK;
 }
 
-int32_t rgd_sample_continuations(rgd_model* m, rgd_kv* kv, const float* last_logits, const int32_t* prompt_idx,
-                                 int32_t n, int32_t N, int32_t steps, float T, float min_p, const uint64_t* seeds,
-                                 const int32_t* forced, float* logits_tap, int32_t* out, rgd_stream stream) {
-  g_err.clear();
+}  // extern "C"
+
+namespace {
+
+int32_t sample_continuations(rgd_model* m, rgd_kv* kv, const float* last_logits, const int32_t* prompt_idx,
+                             int32_t n, int32_t N, int32_t steps, float T, float min_p, bool pless,
+                             const uint64_t* seeds, const int32_t* forced, float* logits_tap, int32_t* out,
+                             rgd_stream stream) {
   if (!m || !kv || !last_logits || !prompt_idx || !seeds || !out) return fail(RGD_E_INVALID_ARG, "null argument");
   if (kv->m != m) return fail(RGD_E_INVALID_ARG, "kv belongs to another model");
   if (n < 1 || N < 1 || steps < 1) return fail(RGD_E_INVALID_ARG, "n, N and steps must be >= 1");
   if ((long long)n * N > m->max_rows) return fail(RGD_E_INVALID_ARG, "n*N exceeds max_rows");
-  if (!(T >= 0.f) || !(min_p >= 0.f && min_p <= 1.f)) return fail(RGD_E_INVALID_ARG, "T must be >= 0, min_p in [0,1]");
+  if (!(T >= 0.f)) return fail(RGD_E_INVALID_ARG, "T must be >= 0");
+  if (!pless && !(min_p >= 0.f && min_p <= 1.f)) return fail(RGD_E_INVALID_ARG, "min_p must be in [0,1]");
+  if (pless && T > 0.f && (m->cfg.vocab % 4 || m->nchunks > 256))
+    return fail(RGD_E_UNSUPPORTED, "p-less sampling needs a vocabulary that is a multiple of 4");
   if (kv->probe_held) return fail(RGD_E_STATE, "probe tails not released (call rgd_gate)");
   for (int i = 0; i < n; ++i) {
     const int b = prompt_idx[i];
@@ -1228,7 +1244,7 @@ int32_t rgd_sample_continuations(rgd_model* m, rgd_kv* kv, const float* last_log
   hipLaunchKernelGGL(gather_rows_kernel, dim3((int)cdiv(V, 256 * 8), R), dim3(256), 0, s, last_logits, (long long)V,
                      m->row_map, V, z0);
   HIP_OK(hipGetLastError());
-  if (T > 0.f) HIP_OK(chunk_max(z0, V, R, V, kSampleChunk, m->tilemax, s));
+  if (T > 0.f && !pless) HIP_OK(chunk_max(z0, V, R, V, kSampleChunk, m->tilemax, s));
   struct StepIndex {  // restores the timing step index on every exit
     rgd_model* m;
     ~StepIndex() { m->tstep = 0; }
@@ -1238,7 +1254,7 @@ int32_t rgd_sample_continuations(rgd_model* m, rgd_kv* kv, const float* last_log
   // forced (teacher forcing feeds other tokens) or no step follows
   bool embedded = false;
   RGD_TRY(select_tokens(m, z0, V, R, m->tilemax, m->nchunks, T, min_p, sd, 0u, out, steps, 0, m->cur_tok, s,
-                        !forced && steps > 1, &embedded));
+                        !forced && steps > 1, &embedded, pless));
   for (int st = 1; st < steps; ++st) {
     m->tstep = st - 1;
     TimeScope tstep(m, RGD_TIMER_STEP, s);
@@ -1249,10 +1265,31 @@ int32_t rgd_sample_continuations(rgd_model* m, rgd_kv* kv, const float* last_log
     float* z = logits_tap ? logits_tap + (size_t)st * R * V : m->logits;
     RGD_TRY(lm_head(m, m->xn, m->cfg.d_model, R, z, s));
     RGD_TRY(select_tokens(m, z, V, R, m->tilemax, m->ntiles, T, min_p, sd, (unsigned)st, out, steps, st,
-                          m->cur_tok, s, !forced && st + 1 < steps, &embedded));
+                          m->cur_tok, s, !forced && st + 1 < steps, &embedded, pless));
   }
   // pages are returned to the pool by `give` (work on them stays ordered on `s`)
   return RGD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t rgd_sample_continuations(rgd_model* m, rgd_kv* kv, const float* last_logits, const int32_t* prompt_idx,
+                                 int32_t n, int32_t N, int32_t steps, float T, float min_p, const uint64_t* seeds,
+                                 const int32_t* forced, float* logits_tap, int32_t* out, rgd_stream stream) {
+  g_err.clear();
+  return sample_continuations(m, kv, last_logits, prompt_idx, n, N, steps, T, min_p, false, seeds, forced,
+                              logits_tap, out, stream);
+}
+
+int32_t rgd_sample_continuations_pless(rgd_model* m, rgd_kv* kv, const float* last_logits,
+                                       const int32_t* prompt_idx, int32_t n, int32_t N, int32_t steps, float T,
+                                       const uint64_t* seeds, const int32_t* forced, float* logits_tap,
+                                       int32_t* out, rgd_stream stream) {
+  g_err.clear();
+  return sample_continuations(m, kv, last_logits, prompt_idx, n, N, steps, T, 0.f, true, seeds, forced,
+                              logits_tap, out, stream);
 }
 
 int32_t rgd_check_status(rgd_model* m, rgd_stream stream) {
@@ -1365,8 +1402,9 @@ int32_t rgd_kernel_lm_head(rgd_model* m, const void* hvec, int32_t R, float* log
 uint64_t rgd_sampler_workspace_bytes(int32_t R, int32_t V) {
   if (R < 1 || V < 1) return 0;
   const long long nch = cdiv(V, kSampleChunk);
-  // best u64 [R], chunk maxima f32 [R][nch], chunk sums f32 [R][nch]
-  return (uint64_t)(8LL * R + 8LL * R * nch + 256);
+  // best u64 [R], chunk sums f32 [R][nch], chunk maxima, sums of w and of w^2
+  // f32 [3][R][nch] (the last two for p-less), p-less thresholds f32 [R]
+  return (uint64_t)(8LL * R + 16LL * R * nch + 4LL * R + 256);
 }
 
 int32_t rgd_kernel_probe_step(rgd_model* m, const float* logits, int32_t R, const rgd_table* tbl, int32_t k,
@@ -1439,20 +1477,25 @@ int32_t rgd_kernel_argmax(const float* z, int32_t R, int32_t V, void* workspace,
   return RGD_OK;
 }
 
-int32_t rgd_kernel_sample(const float* z, int32_t R, int32_t V, float T, float min_p, const uint64_t* seeds,
-                          uint32_t ctr, uint32_t stream0, int32_t draws, void* workspace, int32_t* out,
-                          rgd_stream stream) {
-  g_err.clear();
+}  // extern "C"
+
+namespace {
+
+int32_t kernel_sample(const float* z, int32_t R, int32_t V, float T, float min_p, bool pless,
+                      const uint64_t* seeds, uint32_t ctr, uint32_t stream0, int32_t draws, void* workspace,
+                      int32_t* out, rgd_stream stream) {
   if (!z || !seeds || !workspace || !out) return fail(RGD_E_INVALID_ARG, "null argument");
   if (R < 1 || V < 4 || V % 4 || (long long)V > 256LL * kSampleChunk || draws < 1)
     return fail(RGD_E_INVALID_ARG, "bad R/V/draws");
-  if (!(T > 0.f) || !(min_p >= 0.f && min_p <= 1.f)) return fail(RGD_E_INVALID_ARG, "T must be > 0, min_p in [0,1]");
+  if (!(T > 0.f)) return fail(RGD_E_INVALID_ARG, "T must be > 0");
+  if (!pless && !(min_p >= 0.f && min_p <= 1.f)) return fail(RGD_E_INVALID_ARG, "min_p must be in [0,1]");
   if ((uintptr_t)workspace % 256) return fail(RGD_E_INVALID_ARG, "workspace must be 256-byte aligned");
   hipStream_t s = (hipStream_t)stream;
   const int nch = (int)cdiv(V, kSampleChunk);
   char* w = (char*)workspace;
-  float* cmax = (float*)(w + 8LL * R);
-  float* csum = cmax + (long long)R * nch;
+  float* csum = (float*)(w + 8LL * R);
+  float* cmax = csum + (long long)R * nch;  // start of the [3][R][nch] statistics
+  float* thr = cmax + 3LL * R * nch;
   SampleArgs a{};
   a.z = z;
   a.ldz = V;
@@ -1473,9 +1516,32 @@ int32_t rgd_kernel_sample(const float* z, int32_t R, int32_t V, float T, float m
   a.out_col = 0;
   a.cur_tok = nullptr;
   a.status = nullptr;
-  HIP_OK(minp_sample_standalone(a, cmax, s));
+  if (pless) {
+    HIP_OK(pless_sample(a, cmax, thr, s));
+    a.row_thr = thr;
+  } else {
+    HIP_OK(minp_sample_standalone(a, cmax, s));
+  }
   if (draws > 1) HIP_OK(minp_multi_draw(a, draws, stream0, out, s));
   return RGD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t rgd_kernel_sample(const float* z, int32_t R, int32_t V, float T, float min_p, const uint64_t* seeds,
+                          uint32_t ctr, uint32_t stream0, int32_t draws, void* workspace, int32_t* out,
+                          rgd_stream stream) {
+  g_err.clear();
+  return kernel_sample(z, R, V, T, min_p, false, seeds, ctr, stream0, draws, workspace, out, stream);
+}
+
+int32_t rgd_kernel_sample_pless(const float* z, int32_t R, int32_t V, float T, const uint64_t* seeds,
+                                uint32_t ctr, uint32_t stream0, int32_t draws, void* workspace, int32_t* out,
+                                rgd_stream stream) {
+  g_err.clear();
+  return kernel_sample(z, R, V, T, 0.f, true, seeds, ctr, stream0, draws, workspace, out, stream);
 }
 
 }  // extern "C"

@@ -169,6 +169,7 @@ RGD_DEV int select_token(const SampleArgs& a, int r, float mx, float u, float mi
   __shared__ float wsum[NW];
   __shared__ int red_i[NW];
   const float kT = kLog2e / a.T;
+  const float thr = a.row_thr ? a.row_thr[r] : a.p_min;  // kept: w >= thr
   // running sum over chunks in chunk order (one chunk per thread)
   const int c = threadIdx.x;
   const float incl_c = block_inclusive_scan(mine, wsum);
@@ -207,7 +208,7 @@ RGD_DEV int select_token(const SampleArgs& a, int r, float mx, float u, float mi
 #pragma unroll
   for (int i = 0; i < PMAX; ++i) {
     const float zi = i % 4 == 0 ? zv[i / 4].x : i % 4 == 1 ? zv[i / 4].y : i % 4 == 2 ? zv[i / 4].z : zv[i / 4].w;
-    const float w = (i < per && e0 + i < e1) ? kept_weight(zi, mx, kT, a.p_min) : -1.f;
+    const float w = (i < per && e0 + i < e1) ? kept_weight(zi, mx, kT, thr) : -1.f;
     wv[i] = w;
     ts += w > 0.f ? w : 0.f;
   }
@@ -449,6 +450,92 @@ __global__ __launch_bounds__(1024) void minp_row_kernel(SampleArgs a, float* cma
   }
 }
 
+// ------------------------------------------------------------------ p-less --
+// p-less truncation (temperature first): with w_i = exp2((z_i - m) log2(e)/T),
+// S1 = sum w_i and S2 = sum w_i^2, softmax(z/T) gives p_i = w_i / S1 and
+// sum_j p_j^2 = S2 / S1^2, so p_i >= sum_j p_j^2 iff w_i >= S2 / S1.  The
+// threshold depends on the whole row, so the chunk sums need one more pass
+// than min-p: (1) per chunk, its maximum m_c and S1, S2 relative to m_c;
+// (2) per chunk, the row's m, S1, S2 combined from all chunk statistics in one
+// fixed order (so every workgroup of the row and the draw see the same
+// threshold), then the chunk's kept sum relative to m (chunks whose best
+// weight is under the threshold are not read); (3) the min-p draw kernel with
+// the per-row threshold.
+
+__global__ __launch_bounds__(256) void pless_stats_kernel(SampleArgs a, float* cmax, float* s1, float* s2) {
+  __shared__ float red[4];
+  const int c = blockIdx.x, r = blockIdx.y;
+  const float* zr = a.z + r * a.ldz;
+  const int lo = c * a.chunk, hi = min(a.V, lo + a.chunk);
+  float4 v[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int i = lo + (threadIdx.x + k * 256) * 4;
+    v[k] = i < hi ? *(const float4*)(zr + i) : float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+  }
+  float mc = -INFINITY;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) mc = fmaxf(mc, fmaxf(fmaxf(v[k].x, v[k].y), fmaxf(v[k].z, v[k].w)));
+  mc = block_max(mc, red);
+  const float kT = kLog2e / a.T;
+  float t1 = 0.f, t2 = 0.f;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const float w0 = __builtin_amdgcn_exp2f((v[k].x - mc) * kT), w1 = __builtin_amdgcn_exp2f((v[k].y - mc) * kT);
+    const float w2 = __builtin_amdgcn_exp2f((v[k].z - mc) * kT), w3 = __builtin_amdgcn_exp2f((v[k].w - mc) * kT);
+    t1 += (w0 + w1) + (w2 + w3);
+    t2 += (w0 * w0 + w1 * w1) + (w2 * w2 + w3 * w3);
+  }
+  t1 = block_sum(t1, red);
+  t2 = block_sum(t2, red);
+  if (threadIdx.x == 0) {
+    const long long rc = (long long)r * a.nchunks + c;
+    cmax[rc] = mc;
+    s1[rc] = t1;
+    s2[rc] = t2;
+  }
+}
+
+__global__ __launch_bounds__(256) void pless_sum_kernel(SampleArgs a, const float* cmax, const float* s1,
+                                                        const float* s2, float* thr_out) {
+  __shared__ float red[4];
+  const int c = blockIdx.x, r = blockIdx.y, t = threadIdx.x;
+  const long long r0 = (long long)r * a.nchunks;
+  // every chunk's statistics, one chunk per thread (nchunks <= 256)
+  const bool own = t < a.nchunks;
+  const float mt = own ? cmax[r0 + t] : -INFINITY;
+  const float a1 = own ? s1[r0 + t] : 0.f, a2 = own ? s2[r0 + t] : 0.f;
+  const float m = block_max(mt, red);
+  const float kT = kLog2e / a.T;
+  const float e = own ? __builtin_amdgcn_exp2f((mt - m) * kT) : 0.f;
+  const float S1 = block_sum(a1 * e, red);
+  const float S2 = block_sum(a2 * e * e, red);
+  const float thr = S2 / S1;
+  if (c == 0 && t == 0) {
+    thr_out[r] = thr;
+    if (a.status && !(m > -INFINITY && m < INFINITY)) atomicOr(a.status, 1);
+  }
+  float sum = 0.f;
+  if (kept_weight(cmax[r0 + c], m, kT, thr) >= 0.f) {  // uniform: one value per workgroup
+    const float* zr = a.z + r * a.ldz;
+    const int lo = c * a.chunk, hi = min(a.V, lo + a.chunk);
+    float4 v[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int i = lo + (t + k * 256) * 4;
+      v[k] = i < hi ? *(const float4*)(zr + i) : float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const float w0 = kept_weight(v[k].x, m, kT, thr), w1 = kept_weight(v[k].y, m, kT, thr);
+      const float w2 = kept_weight(v[k].z, m, kT, thr), w3 = kept_weight(v[k].w, m, kT, thr);
+      sum += (w0 > 0.f ? w0 : 0.f) + (w1 > 0.f ? w1 : 0.f) + (w2 > 0.f ? w2 : 0.f) + (w3 > 0.f ? w3 : 0.f);
+    }
+    sum = block_sum(sum, red);
+  }
+  if (t == 0) a.chunk_sums[r0 + c] = sum;
+}
+
 __global__ __launch_bounds__(256) void minp_select_kernel(SampleArgs a) {
   __shared__ float red[4];
   const int r = blockIdx.x;
@@ -564,6 +651,22 @@ hipError_t minp_sample_standalone(const SampleArgs& a0, float* cmax, hipStream_t
     hipLaunchKernelGGL(minp_cand_kernel, dim3(a.nchunks, a.R), dim3(256), 0, s, a, cmax);
     hipLaunchKernelGGL(minp_fixsel_kernel, dim3(a.R), dim3(1024), 0, s, a);
   }
+  return hipGetLastError();
+}
+
+hipError_t pless_sample(const SampleArgs& a0, float* stats, float* thr, hipStream_t s) {
+  if (a0.chunk != 4096 || a0.V % 4 || a0.ldz % 4 || a0.nchunks > 256 || a0.nchunks * a0.chunk < a0.V ||
+      !(a0.T > 0.f))
+    return hipErrorInvalidValue;
+  SampleArgs a = a0;
+  const long long n = (long long)a.R * a.nchunks;
+  float* cmax = stats;
+  a.pmax = cmax;
+  a.npmax = a.nchunks;
+  a.row_thr = thr;
+  hipLaunchKernelGGL(pless_stats_kernel, dim3(a.nchunks, a.R), dim3(256), 0, s, a, cmax, stats + n, stats + 2 * n);
+  hipLaunchKernelGGL(pless_sum_kernel, dim3(a.nchunks, a.R), dim3(256), 0, s, a, cmax, stats + n, stats + 2 * n, thr);
+  hipLaunchKernelGGL(minp_select_kernel, dim3(a.R), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

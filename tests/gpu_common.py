@@ -51,6 +51,24 @@ def argmax_gpu(rgd, z_np):
 MARGIN = 1e-4
 
 
+def _robust(w, kept, amb, u, tok, margin):
+    """True when the oracle's draw `tok` cannot change under any flip of the
+    mask decisions within the margin (tokens in `amb`) or a relative error of
+    `margin` in the running sums: tok itself is not ambiguous and u * W lies
+    inside tok's CDF interval by more than twice the ambiguous weight plus
+    margin * W on both sides.  Such draws must match exactly even though some
+    mask decision elsewhere is a near tie."""
+    if amb[tok]:
+        return False
+    wk = np.where(kept, w, 0.0)
+    W = wk.sum()
+    lo = wk[:tok].sum()
+    hi = lo + wk[tok]
+    t = u * W
+    slack = 2.0 * w[amb].sum() + margin * W
+    return t - lo > slack and hi - t > slack
+
+
 def judge_draw(z, T, pmin, u, got, margin=MARGIN):
     """Classifies one GPU draw against the oracle on the same logits.
 
@@ -62,14 +80,14 @@ def judge_draw(z, T, pmin, u, got, margin=MARGIN):
     Returns "exact", "margin-equal" or "margin-diff"."""
     from oracle import sampler
     d = sampler.sample_minp(z, T, pmin, u)
-    if d.cdf_margin >= margin and d.logit_margin >= margin:
+    w, _ = sampler.minp_weights(z, T, pmin)
+    lw = np.log(np.maximum(w, 1e-300))
+    amb = np.abs(lw - np.log(pmin)) < margin if pmin > 0 else np.zeros_like(w, bool)
+    if (d.cdf_margin >= margin and d.logit_margin >= margin) or _robust(w, w >= pmin, amb, u, d.token, margin):
         assert got == d.token, (got, d)
         return "exact"
     if got == d.token:
         return "margin-equal"
-    w, _ = sampler.minp_weights(z, T, pmin)
-    lw = np.log(np.maximum(w, 1e-300))
-    amb = np.abs(lw - np.log(pmin)) < margin if pmin > 0 else np.zeros_like(w, bool)
     kept = w >= pmin * np.exp(-margin)
     assert kept[got], ("token outside the relaxed min-p set", got)
     wk = np.where(w >= pmin, w, 0.0)
@@ -78,5 +96,31 @@ def judge_draw(z, T, pmin, u, got, margin=MARGIN):
     lo, hi = c[got] - wk[got], c[got]
     t = u * W
     slack = margin * W + w[amb].sum()
+    assert lo - slack <= t <= hi + slack, ("draw too far from u*W", got, d.token)
+    return "margin-diff"
+
+
+def judge_draw_pless(z, T, u, got, margin=MARGIN):
+    """judge_draw for the p-less rule (keep p_i >= sum_j p_j^2): identical token
+    outside margin cases (CDF margin and |ln p_i - ln sum p^2| >= margin for
+    every token), otherwise a valid outcome under the mask relaxed by the
+    margin."""
+    from oracle import pless
+    d = pless.sample_pless(z, T, u)
+    p, thr, _ = pless.pless_probabilities(z, T)
+    lp = np.log(np.maximum(p, 1e-300))
+    amb = np.abs(lp - np.log(thr)) < margin
+    if (d.cdf_margin >= margin and d.logit_margin >= margin) or _robust(p, p >= thr, amb, u, d.token, margin):
+        assert got == d.token, (got, d)
+        return "exact"
+    if got == d.token:
+        return "margin-equal"
+    assert p[got] >= thr * np.exp(-margin), ("token outside the relaxed p-less set", got)
+    pk = np.where(p >= thr, p, 0.0)
+    W = pk.sum()
+    c = np.cumsum(pk)
+    lo, hi = c[got] - pk[got], c[got]
+    t = u * W
+    slack = margin * W + p[amb].sum()
     assert lo - slack <= t <= hi + slack, ("draw too far from u*W", got, d.token)
     return "margin-diff"
