@@ -190,12 +190,53 @@ def sampler_sweep(rgd, torch, reps=20, flush_mode="read"):
             us = timed(lambda: rgd.kernel_sample(z, T, pm, seeds, 0, 0, 1, ws, out))
             pts.append({"T": T, "min_p": pm, "us": round(us, 2)})
     am = timed(lambda: rgd.kernel_argmax(z, ws, out[:, 0]))
+    pl = [{"T": T, "us": round(timed(lambda: rgd.kernel_sample_pless(z, T, seeds, 0, 0, 1, ws, out)), 2)}
+          for T in s.temperatures]
     us_all = sorted(p["us"] for p in pts)
     med = us_all[len(us_all) // 2]
+    pl_med = sorted(p["us"] for p in pl)[len(pl) // 2]
     return {"workload": s.name, "rows": R, "vocab": V, "bytes_per_call": nbytes, "points": pts,
             "median_us": med, "median_gbs": round(nbytes / (med * 1e-6) / 1e9, 1),
             "median_frac": round(nbytes / (med * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
-            "argmax_us": round(am, 2)}
+            "argmax_us": round(am, 2),
+            "pless": {"points": pl, "median_us": pl_med,
+                      "median_frac": round(nbytes / (pl_med * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}}
+
+
+def pless_variant(rgd, torch, model, kv, w, last, N, S, seeds, out, minp_ms, reps=3):
+    """The same N x S sampling call with p-less truncation (keep p_i >= sum_j
+    p_j^2 of softmax(z/T), the truncation of the paper's experiments) in place
+    of min-p: wall time per call (device synchronisations around it), tokens/s,
+    and the library's event timings of the p-less sampler and of a decode
+    step.  Algorithmic sampler bytes: the logits once (R x V x 4); the kernels
+    read them twice (statistics, then the chunks above the threshold)."""
+    def run(timed):
+        if timed:
+            rgd.timing_enable(model, TIMING_PERIOD)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        rgd.sample_continuations_pless(model, kv, last, [0], N, S, w.temperature, seeds, out)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        if timed:
+            rgd.timing_enable(model, 0)
+        return dt
+
+    run(False)
+    rgd.timing_read(model)
+    ts = sorted(run(True) for _ in range(reps))
+    rgd.check_status(model)
+    tim = rgd.timing_read(model)
+    sp_ms, sp_n = tim["sampler"]
+    st_ms, st_n = tim["step"]
+    med = ts[len(ts) // 2]
+    sb = N * w.vocab * 4
+    sp_us = sp_ms / sp_n * 1e3
+    return {"sampling_ms": round(med * 1e3, 3), "tokens_per_s": round(N * S / med, 1),
+            "vs_minp_sampling": round(med * 1e3 / minp_ms, 4),
+            "sampler_avg_us": round(sp_us, 2), "sampler_gbs": round(sb / (sp_us * 1e-6) / 1e9, 1),
+            "sampler_frac": round(sb / (sp_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+            "decode_step_avg_us": round(st_ms / st_n * 1e3, 2)}
 
 
 def cpu_baseline(weights, w, P, last_tok, kp, vp, budget_s=15.0):
@@ -404,6 +445,8 @@ def main():
         "wall_ms_per_step_with_prefill": round(elapsed / args.steps * 1e3, 3),
     }
     line.update(res)
+    log("p-less sampling ...")
+    line["pless"] = pless_variant(rgd, torch, model, kv, w, last, N, S, seeds, out, sample_s / args.steps * 1e3)
     log("gate variants ...")
     line["gate_variants"] = gate_variants(rgd, torch, model, kv, w, last, last_tok, table, prefill, k, c,
                                           sample_s / args.steps * 1e3)
