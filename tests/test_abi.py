@@ -83,6 +83,8 @@ def test_entry_points_reject_null_handles(rgd):
     assert rgd.lib.rgd_gate(None, None, 1, p, p, p, None) == 1
     assert rgd.lib.rgd_sample_continuations(None, None, None, p, 1, 1, 1, 1.0, 0.1, None, None, None,
                                             None, None) == 1
+    assert rgd.lib.rgd_sample_continuations_pless(None, None, None, p, 1, 1, 1, 1.0, None, None, None,
+                                                  None, None) == 1
     assert rgd.lib.rgd_kv_create(None, 1, 1, 1, 16, None, None, None, None, C.byref(C.c_void_p())) == 1
     assert rgd.lib.rgd_kv_set_prefix_len(None, 0, 0) == 1
     assert rgd.lib.rgd_check_status(None, None) == 1
@@ -98,7 +100,11 @@ def test_kernel_sampler_validation(rgd):
     assert rgd.lib.rgd_kernel_sample(fake, 2, 6, 1.0, 0.1, fake, 0, 0, 1, fake, fake, None) == 1
     assert rgd.lib.rgd_kernel_sample(fake, 2, 8, 1.0, 0.1, fake, 0, 0, 0, fake, fake, None) == 1
     assert rgd.lib.rgd_kernel_sample(fake, 2, 8, 1.0, 0.1, fake, 0, 0, 1, C.c_void_p(260), fake, None) == 1
+    assert rgd.lib.rgd_kernel_sample_pless(fake, 2, 8, 0.0, fake, 0, 0, 1, fake, fake, None) == 1
+    assert rgd.lib.rgd_kernel_sample_pless(fake, 2, 6, 1.0, fake, 0, 0, 1, fake, fake, None) == 1
+    assert rgd.lib.rgd_kernel_sample_pless(None, 2, 8, 1.0, fake, 0, 0, 1, fake, fake, None) == 1
+    assert rgd.lib.rgd_kernel_sample_pless(fake, 2, 8, 1.0, fake, 0, 0, 1, C.c_void_p(260), fake, None) == 1
     assert rgd.lib.rgd_kernel_argmax(None, 2, 8, fake, fake, None) == 1
     assert rgd.lib.rgd_kernel_argmax(fake, 0, 8, fake, fake, None) == 1
-    assert rgd.lib.rgd_sampler_workspace_bytes(4, 152064) >= 8 * 4 + 4 * 4 + 8 * 4 * 38
+    assert rgd.lib.rgd_sampler_workspace_bytes(4, 152064) >= 8 * 4 + 4 * 4 + 16 * 4 * 38
     assert rgd.lib.rgd_sampler_workspace_bytes(0, 8) == 0
