@@ -14,7 +14,7 @@ import synth
 from oracle import philox
 from oracle import rgd as orgd
 from oracle.model import Decoder, KVCache
-from tests.gpu_common import judge_draw, rel_err, seeds_tensor, torch
+from tests.gpu_common import judge_draw, judge_draw_pless, rel_err, seeds_tensor, torch
 
 pytestmark = pytest.mark.gpu
 TOL = 2e-2
@@ -69,7 +69,7 @@ def _last_logits(rgd, wd):
     assert err <= TOL
 
 
-def _teacher_forced(rgd, wd, rows, steps, T, p_min):
+def _teacher_forced(rgd, wd, rows, steps, T, p_min, pless=False):
     t = torch()
     from paper_2607_20791_amd import session
     wd.prefill(rgd)
@@ -78,20 +78,28 @@ def _teacher_forced(rgd, wd, rows, steps, T, p_min):
     seeds = synth.branch_seeds(1, rows, base=500)
     out = t.full((1, rows, steps), -1, dtype=t.int32, device="cuda")
     tap = t.empty(steps, rows, V, dtype=t.float32, device="cuda")
-    rgd.sample_continuations(wd.model, wd.kv, wd.last, [0], rows, steps, T, p_min, seeds_tensor(seeds), out,
-                             forced=session.to_device(forced), logits_tap=tap)
+    if pless:
+        rgd.sample_continuations_pless(wd.model, wd.kv, wd.last, [0], rows, steps, T, seeds_tensor(seeds), out,
+                                       forced=session.to_device(forced), logits_tap=tap)
+    else:
+        rgd.sample_continuations(wd.model, wd.kv, wd.last, [0], rows, steps, T, p_min, seeds_tensor(seeds), out,
+                                 forced=session.to_device(forced), logits_tap=tap)
     t.cuda.synchronize()
     rgd.check_status(wd.model)
     tap_h, got = tap.cpu().numpy(), out.cpu().numpy()[0]
     worst = 0.0
     for r in range(rows):
         br = orgd.sample_branch(wd.dec, wd.cache, wd.ref_last, int(seeds[r]), steps, T, p_min,
-                                forced=forced[r], keep_logits=True)
+                                forced=forced[r], keep_logits=True, truncation="pless" if pless else "minp")
         err = rel_err(tap_h[:, r], np.stack(br.logits))
         worst = max(worst, float(err.max()))
         assert err.max() <= TOL, (r, err)
         for s in range(steps):   # the sampler on the GPU's own logits
-            judge_draw(tap_h[s, r], T, p_min, float(philox.uniform(int(seeds[r]), s)), int(got[r, s]))
+            u = float(philox.uniform(int(seeds[r]), s))
+            if pless:
+                judge_draw_pless(tap_h[s, r], T, u, int(got[r, s]))
+            else:
+                judge_draw(tap_h[s, r], T, p_min, u, int(got[r, s]))
     print(w.name, "teacher-forced logits rel err (worst)", worst)
 
 
@@ -101,6 +109,12 @@ def test_bf16_c1_prompt_logits(rgd, c1):
 
 def test_bf16_c1_teacher_forced(rgd, c1):
     _teacher_forced(rgd, c1, rows=2, steps=3, T=c1.w.temperature, p_min=c1.w.min_p)
+
+
+def test_bf16_c1_teacher_forced_pless(rgd, c1):
+    """p-less truncation on the 8B-shaped layer: logits within the bf16
+    tolerance and each token the oracle's p-less draw on the GPU's logits."""
+    _teacher_forced(rgd, c1, rows=2, steps=3, T=c1.w.temperature, p_min=0.0, pless=True)
 
 
 def test_bf16_c2_prompt_logits(rgd, c2):
