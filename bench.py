@@ -270,6 +270,94 @@ def cpu_baseline(weights, w, P, last_tok, kp, vp, budget_s=15.0):
                       f"{el:.1f} s"}
 
 
+def eight_layer(rgd, torch, reps):
+    """The 8-layer 8B-shaped model, 32 prompts of 1024 tokens (prefill timed on
+    its own), a shared 64-entry table in which 16 entries are the first 4 greedy
+    tokens of the even prompts, and 8 branches x 256 min-p tokens (T=2,
+    p_min=0.1) per miss.  Gated (probe k=16, c=3, gate, sampling of the misses)
+    against ungated (every prompt sampled, no probe) wall time, median of reps,
+    with the cost row of the miss prompts: the check tokens they decoded, the
+    probe + gate time, and the ratio of gated to direct latency for them."""
+    import numpy as np
+    import synth
+    from paper_2607_20791_amd import session
+    w = synth.MODEL_8LAYER
+    B, n, k, N, S = w.n_prompts, w.prompt_len, w.probe_k, w.n_branches, w.steps
+    log("8-layer model: weights ...")
+    m = session.build_model(synth.model_weights(w), max_rows=B * N, max_pos=n + S)
+    pages = B * N * ((S - 1 + 15) // 16) + B * ((k - 1 + 15) // 16) + 8
+    kv = session.alloc_kv(m, w, max_prompts=B, max_prefix=n, n_pages=pages)
+    toks = session.to_device(synth.prompt_tokens(w))
+    last = torch.empty(B, w.vocab, dtype=torch.float32, device="cuda")
+    log("8-layer model: prefill ...")
+    rgd.prefill_kv(m, kv, toks, 0, last)
+    torch.cuda.synchronize()
+    for b in range(B):            # the timed prefill rewrites the same prompt KV
+        kv.set_prefix_len(b, 0)
+    t0 = time.perf_counter()
+    rgd.prefill_kv(m, kv, toks, 0, last)
+    torch.cuda.synchronize()
+    prefill_s = time.perf_counter() - t0
+    greedy = torch.full((B, 1, k), -1, dtype=torch.int32, device="cuda")
+    rgd.sample_continuations(m, kv, last, list(range(B)), 1, k, 0.0, 0.0,
+                             torch.arange(B, dtype=torch.int64, device="cuda"), greedy)
+    g = greedy[:, 0].cpu().numpy()
+    off, tk = synth.random_table(w, n_entries=w.n_entries - B // 2)
+    ents = [list(tk[off[i]:off[i + 1]]) for i in range(len(off) - 1)]
+    ents += [list(g[b, :4]) for b in range(0, B, 2)]
+    offs = np.concatenate([[0], np.cumsum([len(e) for e in ents])]).astype(np.int32)
+    table = rgd.Table(offs, np.concatenate(ents).astype(np.int32))
+    seeds_all = torch.from_numpy(synth.branch_seeds(B, N).view(np.int64)).cuda()
+    ptok = torch.empty(B, k, dtype=torch.int32, device="cuda")
+    plen = torch.empty(B, dtype=torch.int32, device="cuda")
+    ev = torch.empty(B, dtype=torch.int32, device="cuda")
+    out = torch.empty(B, N, S, dtype=torch.int32, device="cuda")
+
+    def rows_of(prompts):
+        return torch.tensor([b * N + j for b in prompts for j in range(N)], dtype=torch.int64, device="cuda")
+
+    def gated():
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        rgd.probe(m, kv, last, table, B, k, 3, -1, ptok, plen, ev)
+        dec, miss = rgd.gate(kv, ev, B)
+        t1 = time.perf_counter()
+        if len(miss):
+            rgd.sample_continuations(m, kv, last, list(miss), N, S, w.temperature, w.min_p,
+                                     seeds_all[rows_of(miss)], out[:len(miss)])
+        torch.cuda.synchronize()
+        return time.perf_counter() - t0, t1 - t0, list(dec), list(miss)
+
+    def ungated(prompts):
+        sd = seeds_all[rows_of(prompts)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        rgd.sample_continuations(m, kv, last, list(prompts), N, S, w.temperature, w.min_p, sd, out[:len(prompts)])
+        torch.cuda.synchronize()
+        return time.perf_counter() - t0
+
+    log("8-layer model: gated and ungated runs ...")
+    gated()
+    runs = sorted((gated() for _ in range(reps)), key=lambda r: r[0])
+    t_g, t_pg, dec, miss = runs[len(runs) // 2]
+    t_u = sorted(ungated(range(B)) for _ in range(reps))[reps // 2]
+    t_um = sorted(ungated(miss) for _ in range(reps))[reps // 2] if miss else 0.0
+    rgd.check_status(m)
+    pl = plen.cpu().numpy()
+    hits = [b for b in range(B) if dec[b] == 1]
+    returned = len(miss) * N * S + int(sum(int(pl[b]) for b in hits))
+    return {"workload": w.name, "prompts": B, "prompt_len": n, "branches": N, "steps": S, "probe_k": k,
+            "hits": len(hits), "misses": len(miss), "prefill_s": round(prefill_s, 4),
+            "gated_s": round(t_g, 4), "gated_tokens_returned": returned,
+            "gated_tokens_per_s": round(returned / t_g, 1),
+            "ungated_s": round(t_u, 4), "ungated_tokens": B * N * S,
+            "ungated_tokens_per_s": round(B * N * S / t_u, 1),
+            "miss_cost": {"check_tokens_per_miss": round(float(np.mean([pl[b] for b in miss])), 3) if miss else None,
+                          "probe_gate_ms": round(t_pg * 1e3, 3),
+                          "direct_sampling_of_misses_ms": round(t_um * 1e3, 3),
+                          "ratio": round((t_pg + t_um) / t_um, 4) if t_um > 0 else None}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -277,6 +365,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--table", choices=("typical", "adversarial"), default="typical")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workload", choices=("8b-layer-p8192", "8b-8layer-32x1024"), default="8b-layer-p8192",
+                    help="the default (one 8B-shaped layer, 8192-position prefix, 64 x 128 branches) or the "
+                         "8-layer model with 32 prompts (gated vs ungated wall time, its own JSON line)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (scales the HBM byte counters)")
     args = ap.parse_args()
@@ -295,6 +386,15 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes_per_launch": 1 << 30, "launches": 3}))
+        return
+
+    if args.workload == "8b-8layer-32x1024":
+        import paper_2607_20791_amd as rgd
+        res = eight_layer(rgd, torch, reps=max(1, args.steps // 4))
+        print(json.dumps({"metric": "gated vs ungated wall time (8-layer, 32 prompts)",
+                          "value": res["gated_tokens_per_s"], "unit": "tokens/s", "n_gpus": 1,
+                          "higher_is_better": True, "dtype": "bf16", "data": "synthetic",
+                          "config": {"workload": res["workload"]}, "eight_layer": res}), flush=True)
         return
 
     import synth
