@@ -12,11 +12,12 @@ namespace {
 constexpr int kNormThreads = 1024;
 
 template <typename T>
-__global__ __launch_bounds__(kNormThreads) void embed_rmsnorm_kernel(const int* tok, int tok_stride, const T* E,
-                                                                   int d, int V, float* x, const float* g,
-                                                                   float eps, T* xn) {
+__global__ __launch_bounds__(kNormThreads) void embed_rmsnorm_kernel(const int* tok, int tok_stride,
+                                                                   const int* tok_map, const T* E, int d, int V,
+                                                                   float* x, const float* g, float eps, T* xn) {
   const int r = blockIdx.x;
-  embed_norm_row(tok[(long long)r * tok_stride], E, d, V, g, eps, x + (long long)r * d, xn + (long long)r * d);
+  const long long src = tok_map ? tok_map[r] : r;
+  embed_norm_row(tok[src * tok_stride], E, d, V, g, eps, x + (long long)r * d, xn + (long long)r * d);
 }
 
 // Logistic readout of one residual row per workgroup (fixed reduction order).
@@ -129,11 +130,11 @@ __global__ __launch_bounds__(1024) void qkv_rope_kernel(const float* parts, int 
 }  // namespace
 
 template <typename T>
-hipError_t embed_rmsnorm(const int* tok, int tok_stride, int R, const T* E, int d, int V, float* x,
-                         const float* g, float eps, T* xn, hipStream_t s) {
+hipError_t embed_rmsnorm(const int* tok, int tok_stride, const int* tok_map, int R, const T* E, int d, int V,
+                         float* x, const float* g, float eps, T* xn, hipStream_t s) {
   if (d % 4 || d > kChunks * 4 * kNormThreads) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(embed_rmsnorm_kernel<T>, dim3(R), dim3(kNormThreads), 0, s, tok, tok_stride, E, d, V, x,
-                     g, eps, xn);
+  hipLaunchKernelGGL(embed_rmsnorm_kernel<T>, dim3(R), dim3(kNormThreads), 0, s, tok, tok_stride, tok_map, E, d,
+                     V, x, g, eps, xn);
   return hipGetLastError();
 }
 
@@ -165,9 +166,9 @@ hipError_t qkv_rope_store(const float* parts, int nparts, long long part_stride,
   return hipGetLastError();
 }
 
-template hipError_t embed_rmsnorm<float>(const int*, int, int, const float*, int, int, float*, const float*,
+template hipError_t embed_rmsnorm<float>(const int*, int, const int*, int, const float*, int, int, float*, const float*,
                                          float, float*, hipStream_t);
-template hipError_t embed_rmsnorm<bf16_t>(const int*, int, int, const bf16_t*, int, int, float*, const float*,
+template hipError_t embed_rmsnorm<bf16_t>(const int*, int, const int*, int, const bf16_t*, int, int, float*, const float*,
                                           float, bf16_t*, hipStream_t);
 template hipError_t residual_rmsnorm<float>(float*, const float*, int, long long, const float*, float, int, int,
                                             float*, hipStream_t);

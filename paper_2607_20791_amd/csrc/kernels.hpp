@@ -66,10 +66,11 @@ struct KVLayout {
 inline int v_stride(int P) { return (P + 63) / 64 * 64; }
 
 // ------------------------------------------------------------ elementwise ----
-// x[r] = E[tok[r * tok_stride]] (ids clamped to [0, V)); xn[r] = rmsnorm(x[r]) * g
+// x[r] = E[tok[i * tok_stride]] with i = tok_map[r] (tok_map null: i = r), ids
+// clamped to [0, V); xn[r] = rmsnorm(x[r]) * g
 template <typename T>
-hipError_t embed_rmsnorm(const int* tok, int tok_stride, int R, const T* E, int d, int V, float* x,
-                         const float* g, float eps, T* xn, hipStream_t s);
+hipError_t embed_rmsnorm(const int* tok, int tok_stride, const int* tok_map, int R, const T* E, int d, int V,
+                         float* x, const float* g, float eps, T* xn, hipStream_t s);
 // split-K partial outputs a consumer kernel sums (at most)
 constexpr int kMaxSplitK = 16;
 // x[r] += sum_p parts[p][r] (nparts <= kMaxSplitK); xn[r] = rmsnorm(x[r]) * g

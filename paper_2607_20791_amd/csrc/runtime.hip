@@ -396,8 +396,10 @@ struct Readout {
 // feed[r * feed_stride]; embedded: the input rows (m->x, m->xn) were already
 // written by the sampler for these tokens.  Leaves the final normalised hidden
 // state in m->xn.
+// feed: input token of row r at feed[i * feed_stride], i = feed_map[r] (null map: i = r)
 int forward_rows(rgd_model* m, rgd_kv* kv, const Rows& rows, const HostRows& h, const int* feed,
-                 int feed_stride, hipStream_t s, bool embedded = false, const Readout* ro = nullptr) {
+                 int feed_stride, hipStream_t s, bool embedded = false, const Readout* ro = nullptr,
+                 const int* feed_map = nullptr) {
   const rgd_model_config& c = m->cfg;
   const int R = rows.R, d = c.d_model, Hq = c.n_heads, Hkv = c.n_kv_heads, D = c.head_dim;
   const int F = c.ffn_dim;
@@ -405,11 +407,11 @@ int forward_rows(rgd_model* m, rgd_kv* kv, const Rows& rows, const HostRows& h, 
   const int mblocks = (int)cdiv(R, 64);
   const float* g0 = (const float*)m->layers[0].attn_norm;
   if (!embedded && bf)
-    HIP_OK(embed_rmsnorm<bf16_t>(feed, feed_stride, R, (const bf16_t*)m->embed, d, c.vocab, m->x, g0, c.rms_eps,
-                                 (bf16_t*)m->xn, s));
+    HIP_OK(embed_rmsnorm<bf16_t>(feed, feed_stride, feed_map, R, (const bf16_t*)m->embed, d, c.vocab, m->x, g0,
+                                 c.rms_eps, (bf16_t*)m->xn, s));
   else if (!embedded)
-    HIP_OK(embed_rmsnorm<float>(feed, feed_stride, R, (const float*)m->embed, d, c.vocab, m->x, g0, c.rms_eps,
-                                (float*)m->xn, s));
+    HIP_OK(embed_rmsnorm<float>(feed, feed_stride, feed_map, R, (const float*)m->embed, d, c.vocab, m->x, g0,
+                                c.rms_eps, (float*)m->xn, s));
   auto readout = [&](int layer) -> hipError_t {
     if (!ro || ro->layer != layer) return hipSuccess;
     return residual_readout(m->x, ro->row0, ro->stride, ro->nrows, d, ro->w, ro->b, ro->out, s);
@@ -557,11 +559,6 @@ __global__ void probe_init_kernel(int B, int k, int* tokens, int* len, int* even
     len[i] = 0;
     event[i] = (scores && scores[i] <= theta) ? 3 : -1;
   }
-}
-
-__global__ void probe_feed_kernel(const int* prompt, int R, const int* probe_tokens, int k, int j, int* cur) {
-  const int r = blockIdx.x * 256 + threadIdx.x;
-  if (r < R) cur[r] = probe_tokens[(long long)prompt[r] * k + j];
 }
 
 // Selects one token per row from logits z (ldz).  T == 0: argmax; otherwise
@@ -1101,11 +1098,9 @@ int probe_impl(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_tab
     }
     if (j > k) break;  // cannot happen: every prompt is decided after k tokens
     const int R = (int)alive.size();
-    hipLaunchKernelGGL(probe_feed_kernel, dim3((R + 255) / 256), dim3(256), 0, s, m->d_prompt, R, probe_tokens, k,
-                       j - 2, m->cur_tok);
-    HIP_OK(hipGetLastError());
+    // row r feeds token j-1 of its prompt's probe (probe_tokens[prompt[r]][j-2])
     Rows rows = device_rows(m, kv, R, j - 2, false);
-    RGD_TRY(forward_rows(m, kv, rows, h, m->cur_tok, 1, s));
+    RGD_TRY(forward_rows(m, kv, rows, h, probe_tokens + (j - 2), k, s, false, nullptr, m->d_prompt));
     RGD_TRY(lm_head(m, m->xn, m->cfg.d_model, R, m->logits, s));
     RGD_TRY(step(m->logits, R, j));
   }
