@@ -179,7 +179,9 @@ int32_t rgd_prefill_kv_scored(rgd_model* m, rgd_kv* kv, const int32_t* tokens, i
  * on c.  Outputs (dev): probe_tokens int32 [B][k], probe_len int32 [B],
  * event int32 [B] (rgd_event).  Synchronous.  tbl NULL: no refusal set, every
  * probe stays compatible, so the probe runs to k tokens (or eos): the
- * fixed-length probe of the paper's ablations. */
+ * fixed-length probe of the paper's ablations.  On success the probe tails are
+ * held until rgd_gate; a probe that fails after validation (a HIP error) waits
+ * for its stream and releases them itself. */
 int32_t rgd_probe(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_table* tbl,
                   int32_t B, int32_t k, int32_t c, int32_t eos_id, int32_t* probe_tokens,
                   int32_t* probe_len, int32_t* event, rgd_stream stream);

@@ -996,6 +996,22 @@ int probe_impl(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_tab
     }
   }
   kv->probe_held = true;
+  // a probe that fails part way (a HIP error) waits for its stream and returns
+  // the tail pages, so the KV state is not left holding them
+  struct ReleaseOnError {
+    rgd_kv* kv;
+    hipStream_t s;
+    bool ok = false;
+    ~ReleaseOnError() {
+      if (ok) return;
+      (void)hipStreamSynchronize(s);
+      for (auto& pp : kv->probe_pages) {
+        for (int p : pp) kv->free_pages.push_back(p);
+        pp.clear();
+      }
+      kv->probe_held = false;
+    }
+  } release{kv, s};
   hipLaunchKernelGGL(probe_init_kernel, dim3((int)cdiv((long long)B * k, 256)), dim3(256), 0, s, B, k, probe_tokens,
                      probe_len, event, scores, theta);
   HIP_OK(hipGetLastError());
@@ -1105,6 +1121,7 @@ int probe_impl(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_tab
     RGD_TRY(step(m->logits, R, j));
   }
   HIP_OK(hipStreamSynchronize(s));
+  release.ok = true;
   return RGD_OK;
 }
 
