@@ -358,6 +358,91 @@ def eight_layer(rgd, torch, reps):
                           "ratio": round((t_pg + t_um) / t_um, 4) if t_um > 0 else None}}
 
 
+def cpu_baseline_units(reps=3):
+    """The CPU-baseline leg per unit: the oracle (float64 numpy, this host's
+    BLAS threads) timed on the units of the workloads, each on a bounded
+    sample that is stated.  Sampler rows of the sampler sweep at every
+    (T, p_min) point and argmax; attention and LM head of one decode step at
+    the 512- and 8192-position layers (t = 1); one whole decode step of one row
+    of the 512-position layer; the tiny fp32 decoder's refusal-gated run of one
+    prompt; and the LM head again on one thread."""
+    import platform
+    import statistics
+    import numpy as np
+    import synth
+    from oracle import attention, philox, sampler
+    from oracle import rgd as orgd
+    from oracle.model import Decoder, KVCache, linear
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threadpool_limits, threads = None, os.cpu_count() or 1
+    cpu = platform.processor() or "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+
+    def med(fn, n=reps):
+        ts = []
+        for _ in range(n):
+            t0 = time.perf_counter()
+            fn()
+            ts.append(time.perf_counter() - t0)
+        return statistics.median(ts)
+
+    out = {"kind": "oracle", "cpu": cpu, "logical_cpus": os.cpu_count(), "blas_threads": int(threads)}
+    # sampler rows (152064 logits)
+    z = synth.sweep_logits(synth.SWEEP, rows=2)
+    s = synth.SWEEP
+    pts = []
+    for T in s.temperatures:
+        for pm in s.min_ps:
+            u = float(philox.uniform(0, 0))
+            pts.append({"T": T, "min_p": pm, "ms_per_row": round(med(lambda: sampler.sample_minp(z[0], T, pm, u)) * 1e3, 3)})
+    out["sampler_row_ms"] = pts
+    out["argmax_row_ms"] = round(med(lambda: sampler.argmax(z[0])) * 1e3, 3)
+    log("oracle units: 8B-shaped layer weights ...")
+    w1 = synth.LAYER_P512
+    weights = synth.model_weights(w1)
+    dec = Decoder(weights)
+    g = np.random.default_rng(0)
+    for name, P, R in (("p512", 513, 16), ("p8192", 8193, 64)):
+        q = g.normal(size=(32, 128))
+        k = g.normal(size=(P + 1, 8, 128))
+        v = g.normal(size=(P + 1, 8, 128))
+        rows = 2
+        t = med(lambda: [attention.attend(q, k, v) for _ in range(rows)], n=1)
+        out[f"attention_step_{name}_ms"] = round(t / rows * R * 1e3, 1)
+        out[f"attention_step_{name}_sample"] = f"{rows} of the {R} rows timed, scaled to {R}"
+        x = g.normal(size=(R, 4096))
+        out[f"lm_head_step_{name}_ms"] = round(med(lambda: linear(weights.lm_head, x), n=1) * 1e3, 1)
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=1):
+            x = g.normal(size=(16, 4096))
+            out["lm_head_step_p512_1thread_ms"] = round(med(lambda: linear(weights.lm_head, x), n=1) * 1e3, 1)
+    # one decode step of one row of the 512-position layer (prefix of 512 N(0,1) positions)
+    kp, vp = synth.synthetic_prefix_kv(w1, 0)
+    cache = KVCache.from_arrays([kp[0]], [vp[0]])
+    last_tok = int(synth.prompt_tokens(w1)[0, 0])
+    dec.prefill([last_tok], cache, start_pos=w1.synthetic_prefix)
+    tail = KVCache(1)
+    out["decode_step_p512_one_row_ms"] = round(med(lambda: dec.decode(7, cache, tail), n=2) * 1e3, 1)
+    # the tiny fp32 decoder: refusal-gated decoding of one prompt (prefill, probe, gate, 1 x 32 draws)
+    w0 = synth.TINY_FP32
+    d0 = Decoder(synth.model_weights(w0))
+    p0 = synth.prompt_tokens(w0)[1]
+    off, tk = synth.random_table(w0, "table1")
+    ents = [list(tk[off[i]:off[i + 1]]) for i in range(len(off) - 1)]
+    out["tiny_gated_one_prompt_s"] = round(med(lambda: orgd.refusal_gated(d0, p0, ents, w0.probe_k, [1], w0.steps,
+                                                                       w0.temperature, w0.min_p), n=1), 2)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -368,6 +453,8 @@ def main():
     ap.add_argument("--workload", choices=("8b-layer-p8192", "8b-8layer-32x1024"), default="8b-layer-p8192",
                     help="the default (one 8B-shaped layer, 8192-position prefix, 64 x 128 branches) or the "
                          "8-layer model with 32 prompts (gated vs ungated wall time, its own JSON line)")
+    ap.add_argument("--oracle-units", action="store_true",
+                    help="only time the oracle per unit on the host (the CPU-baseline leg; no GPU needed)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (scales the HBM byte counters)")
     args = ap.parse_args()
@@ -375,6 +462,10 @@ def main():
         print(f"bench.py runs on exactly one GPU (got --gpus {args.gpus}); the path is built and "
               "measured on one MI355X only", file=sys.stderr)
         sys.exit(2)
+
+    if args.oracle_units:
+        print(json.dumps(cpu_baseline_units()), flush=True)
+        return
 
     import numpy as np
     import torch
