@@ -129,6 +129,7 @@ struct rgd_model {
   int* h_stage = nullptr;  // pinned staging for uploads
   size_t stage_ints = 0;
   hipEvent_t stage_done = nullptr;
+  int* h_events = nullptr;  // pinned host copy of the probe events [max_rows]
   // in-situ timing: event pairs per timed unit
   bool timing = false;
   std::vector<hipEvent_t> tev[RGD_TIMER_COUNT];
@@ -143,6 +144,7 @@ struct rgd_model {
       for (hipEvent_t e : v) (void)hipEventDestroy(e);
     for (void* p : allocs) (void)hipFree(p);
     if (h_stage) (void)hipHostFree(h_stage);
+    if (h_events) (void)hipHostFree(h_events);
     if (stage_done) (void)hipEventDestroy(stage_done);
   }
   template <typename P>
@@ -771,6 +773,7 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
   }
   m->stage_ints = (size_t)R * 8 + 64;
   if (hipHostMalloc((void**)&m->h_stage, m->stage_ints * sizeof(int), hipHostMallocDefault) != hipSuccess ||
+      hipHostMalloc((void**)&m->h_events, (size_t)R * sizeof(int), hipHostMallocDefault) != hipSuccess ||
       hipEventCreateWithFlags(&m->stage_done, hipEventDisableTiming) != hipSuccess ||
       hipEventRecord(m->stage_done, nullptr) != hipSuccess) {
     delete m;
@@ -1063,13 +1066,7 @@ int probe_impl(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_tab
 
   std::vector<int> alive(B);
   for (int b = 0; b < B; ++b) alive[b] = b;
-  std::vector<int> host_ev(B);
-  int* pinned_ev = nullptr;
-  HIP_OK(hipHostMalloc((void**)&pinned_ev, (size_t)B * 4, hipHostMallocDefault));
-  struct PinnedFree {
-    int* p;
-    ~PinnedFree() { (void)hipHostFree(p); }
-  } pf{pinned_ev};
+  int* pinned_ev = m->h_events;  // B <= max_rows
 
   auto set_rows = [&](HostRows& h, std::vector<int>& pages) -> int {
     h.prompt.clear();
