@@ -129,7 +129,8 @@ struct rgd_model {
   int* h_stage = nullptr;  // pinned staging for uploads
   size_t stage_ints = 0;
   hipEvent_t stage_done = nullptr;
-  int* h_events = nullptr;  // pinned host copy of the probe events [max_rows]
+  int* h_events = nullptr;  // pinned host copies: probe events, gate results [2 * max_rows + 1]
+  int* d_gate = nullptr;    // gate results on the device: decision [R], n_miss, miss list [R]
   // in-situ timing: event pairs per timed unit
   bool timing = false;
   std::vector<hipEvent_t> tev[RGD_TIMER_COUNT];
@@ -722,6 +723,7 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
   A(&m->cur_tok, (size_t)R * 4);
   A(&m->status, 4);
   A(&m->row_map, (size_t)R * 4);
+  A(&m->d_gate, (size_t)(2 * R + 1) * 4);
   A(&m->soft_keys, (size_t)R * m->nchunks * kMaxTopK * 8);
   A(&m->soft_cm, (size_t)2 * R * m->nchunks * 4);
   A(&m->d_prompt, (size_t)R * 4);
@@ -773,7 +775,7 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
   }
   m->stage_ints = (size_t)R * 8 + 64;
   if (hipHostMalloc((void**)&m->h_stage, m->stage_ints * sizeof(int), hipHostMallocDefault) != hipSuccess ||
-      hipHostMalloc((void**)&m->h_events, (size_t)R * sizeof(int), hipHostMallocDefault) != hipSuccess ||
+      hipHostMalloc((void**)&m->h_events, (size_t)(2 * R + 1) * sizeof(int), hipHostMallocDefault) != hipSuccess ||
       hipEventCreateWithFlags(&m->stage_done, hipEventDisableTiming) != hipSuccess ||
       hipEventRecord(m->stage_done, nullptr) != hipSuccess) {
     delete m;
@@ -1166,17 +1168,18 @@ int32_t rgd_gate(rgd_kv* kv, const int32_t* event, int32_t B, int32_t* decision_
   hipStream_t s = (hipStream_t)stream;
   rgd_model* m = const_cast<rgd_model*>(kv->m);
   if (B > m->max_rows) return fail(RGD_E_INVALID_ARG, "B exceeds max_rows");
-  // device decision + ordered miss list into the model's scratch ints
-  int* d_dec = m->d_base;
-  int* d_nmiss = m->row_map;
-  int* d_miss = m->d_plen;
-  HIP_OK(hipEventSynchronize(m->stage_done));
+  // device decision + ordered miss list in one run [decision B | n_miss | miss B],
+  // brought back with one copy into pinned memory
+  int* d_dec = m->d_gate;
+  int* d_nmiss = d_dec + B;
+  int* d_miss = d_nmiss + 1;
   HIP_OK(gate_decide(event, B, d_dec, d_nmiss, d_miss, s));
-  std::vector<int> tmp(2 * (size_t)B + 1);
-  HIP_OK(hipMemcpyAsync(decision_host, d_dec, (size_t)B * 4, hipMemcpyDeviceToHost, s));
-  HIP_OK(hipMemcpyAsync(n_miss_host, d_nmiss, 4, hipMemcpyDeviceToHost, s));
-  HIP_OK(hipMemcpyAsync(miss_idx_host, d_miss, (size_t)B * 4, hipMemcpyDeviceToHost, s));
+  HIP_OK(hipMemcpyAsync(m->h_events, d_dec, (2 * (size_t)B + 1) * 4, hipMemcpyDeviceToHost, s));
   HIP_OK(hipStreamSynchronize(s));
+  const int nm = m->h_events[B];
+  std::memcpy(decision_host, m->h_events, (size_t)B * 4);
+  *n_miss_host = nm;
+  std::memcpy(miss_idx_host, m->h_events + B + 1, (size_t)nm * 4);
   // drop every probe tail: pages go back to the pool, nothing is copied
   for (auto& pp : kv->probe_pages) {
     for (int p : pp) kv->free_pages.push_back(p);
