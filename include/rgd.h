@@ -24,6 +24,10 @@
  *    bfloat16 bit patterns, fp32 values IEEE binary32.
  *  - Results are deterministic: reductions use a fixed order and no floating
  *    point atomics, so equal inputs and seeds give bit-identical outputs.
+ *  - A model and its KV state hold the workspace, staging buffers and page
+ *    pool every call on them uses: calls on one model (or its KV states) must
+ *    not overlap, from several threads or on several streams.  Different
+ *    models are independent.
  */
 #ifndef RGD_H
 #define RGD_H
