@@ -440,6 +440,16 @@ def cpu_baseline_units(reps=3):
     ents = [list(tk[off[i]:off[i + 1]]) for i in range(len(off) - 1)]
     out["tiny_gated_one_prompt_s"] = round(med(lambda: orgd.refusal_gated(d0, p0, ents, w0.probe_k, [1], w0.steps,
                                                                        w0.temperature, w0.min_p), n=1), 2)
+    # the 8-layer 32-prompt workload, extrapolated (the oracle decodes one row at a time): one
+    # layer of a one-row step = the one-row decode step minus the LM head (whose cost hardly
+    # depends on the rows), times 8 layers, plus the LM head; ungated = every prompt's 8 x 256
+    w4 = synth.MODEL_8LAYER
+    layer_s = max(out["decode_step_p512_one_row_ms"] - out["lm_head_step_p512_ms"], 0.0) / 1e3
+    row_step_s = w4.n_layers * layer_s + out["lm_head_step_p512_ms"] / 1e3
+    out["eight_layer_extrapolated"] = {
+        "row_step_s": round(row_step_s, 3),
+        "ungated_hours": round(w4.n_prompts * w4.n_branches * w4.steps * row_step_s / 3600, 1),
+        "basis": "extrapolated from the measured one-row decode step and LM head of one 8B-shaped layer"}
     return out
 
 
