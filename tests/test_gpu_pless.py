@@ -183,3 +183,16 @@ def test_pless_decode_path_teacher_forced(rgd, tiny):
         assert rel_err(tap_h[:, r], np.stack(br.logits)).max() <= 1e-5
         for s in range(S):
             judge_draw_pless(br.logits[s], T, float(philox.uniform(int(seeds[r]), s)), int(got[r, s]))
+
+
+@pytest.mark.parametrize("V", [8, 4100])
+def test_pless_ragged_and_tiny_vocabularies(rgd, V):
+    g = np.random.default_rng(V)
+    z = g.normal(size=(5, V)).astype(np.float32) * 2
+    z[1, V - 1] = 9.0
+    seeds = np.arange(5, dtype=np.uint64) + 7
+    for T in (0.7, 2.0):
+        got = sample_pless_gpu(rgd, z, T, seeds, ctr=2, draws=3)
+        for r in range(5):
+            for d in range(3):
+                judge_draw_pless(z[r], T, float(philox.uniform(int(seeds[r]), 2, d)), int(got[r, d]))

@@ -151,3 +151,21 @@ def test_edge_cases_tiny_vocab_many_rows(rgd):
     assert set(np.unique(got)) == {1, 3}
     got = sample_gpu(rgd, z, 1.0, 0.0, seeds, draws=8)
     assert set(np.unique(got)) == set(range(8))
+
+
+@pytest.mark.parametrize("R", [1, 130])
+@pytest.mark.parametrize("V", [4100, 12288 + 4])
+def test_minp_ragged_last_chunk(rgd, R, V):
+    """A last 4096-logit chunk holding 4 logits, through the chunk kernels (1
+    row) and the one-workgroup-per-row kernel (130 rows): the maximum and a
+    heavy token placed in the ragged chunk."""
+    g = np.random.default_rng(V + R)
+    z = g.normal(size=(R, V)).astype(np.float32)
+    z[:, V - 2] = 6.0            # the row maximum, in the ragged last chunk
+    z[::2, V - 3] = 5.5
+    seeds = np.arange(R, dtype=np.uint64) + 3
+    for T, pmin in ((1.0, 0.1), (3.0, 0.05)):
+        got = sample_gpu(rgd, z, T, pmin, seeds, ctr=1, stream0=0, draws=2)
+        for r in range(R):
+            for d in range(2):
+                judge_draw(z[r], T, pmin, float(philox.uniform(int(seeds[r]), 1, d)), int(got[r, d]))
