@@ -37,7 +37,7 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def measured_traffic(name="lm_head_c2_traffic.md"):
+def measured_traffic(name="lm_head_8b_layer_p8192_traffic.md"):
     """HBM bytes per launch from the committed counter summary, or None when
     the kernel source changed since the counters were taken."""
     import hashlib

@@ -51,12 +51,12 @@ class World:
 
 
 @pytest.fixture(scope="module")
-def c1(rgd):
+def p512(rgd):
     return World(rgd, synth.LAYER_P512)
 
 
 @pytest.fixture(scope="module")
-def c2(rgd):
+def p8192(rgd):
     return World(rgd, synth.LAYER_P8192)
 
 
@@ -103,43 +103,43 @@ def _teacher_forced(rgd, wd, rows, steps, T, p_min, pless=False):
     print(w.name, "teacher-forced logits rel err (worst)", worst)
 
 
-def test_bf16_c1_prompt_logits(rgd, c1):
-    _last_logits(rgd, c1)
+def test_bf16_p512_prompt_logits(rgd, p512):
+    _last_logits(rgd, p512)
 
 
-def test_bf16_c1_teacher_forced(rgd, c1):
-    _teacher_forced(rgd, c1, rows=2, steps=3, T=c1.w.temperature, p_min=c1.w.min_p)
+def test_bf16_p512_teacher_forced(rgd, p512):
+    _teacher_forced(rgd, p512, rows=2, steps=3, T=p512.w.temperature, p_min=p512.w.min_p)
 
 
-def test_bf16_c1_teacher_forced_pless(rgd, c1):
+def test_bf16_p512_teacher_forced_pless(rgd, p512):
     """p-less truncation on the 8B-shaped layer: logits within the bf16
     tolerance and each token the oracle's p-less draw on the GPU's logits."""
-    _teacher_forced(rgd, c1, rows=2, steps=3, T=c1.w.temperature, p_min=0.0, pless=True)
+    _teacher_forced(rgd, p512, rows=2, steps=3, T=p512.w.temperature, p_min=0.0, pless=True)
 
 
-def test_bf16_c2_prompt_logits(rgd, c2):
-    _last_logits(rgd, c2)
+def test_bf16_p8192_prompt_logits(rgd, p8192):
+    _last_logits(rgd, p8192)
 
 
-def test_bf16_c2_teacher_forced(rgd, c2):
-    _teacher_forced(rgd, c2, rows=2, steps=2, T=c2.w.temperature, p_min=c2.w.min_p)
+def test_bf16_p8192_teacher_forced(rgd, p8192):
+    _teacher_forced(rgd, p8192, rows=2, steps=2, T=p8192.w.temperature, p_min=p8192.w.min_p)
 
 
-def test_bf16_c2_full_size_properties(rgd, c2):
+def test_bf16_p8192_full_size_properties(rgd, p8192):
     """N=64 branches x 128 steps from the 8192-position prefix: deterministic,
     prefix untouched, and a gated miss (typical 0%-hit table) equals ungated."""
     t = torch()
-    w = c2.w
+    w = p8192.w
     N, S, k = w.n_branches, w.steps, w.probe_k
     seeds = seeds_tensor(synth.branch_seeds(1, N))
-    before = (c2.kv.prefix_k.clone(), c2.kv.prefix_v.clone())
+    before = (p8192.kv.prefix_k.clone(), p8192.kv.prefix_v.clone())
 
     def ungated():
-        c2.prefill(rgd)
+        p8192.prefill(rgd)
         out = t.full((1, N, S), -1, dtype=t.int32, device="cuda")
-        rgd.sample_continuations(c2.model, c2.kv, c2.last, [0], N, S, w.temperature, w.min_p, seeds, out)
+        rgd.sample_continuations(p8192.model, p8192.kv, p8192.last, [0], N, S, w.temperature, w.min_p, seeds, out)
         t.cuda.synchronize()
-        rgd.check_status(c2.model)
+        rgd.check_status(p8192.model)
         return out
 
     a, b = ungated(), ungated()
@@ -148,43 +148,43 @@ def test_bf16_c2_full_size_properties(rgd, c2):
     # gated: probe against the typical table, then the miss is sampled
     off, toks = synth.random_table(w)
     table = rgd.Table(off, toks)
-    c2.prefill(rgd)
+    p8192.prefill(rgd)
     ptok = t.empty(1, k, dtype=t.int32, device="cuda")
     plen = t.empty(1, dtype=t.int32, device="cuda")
     ev = t.empty(1, dtype=t.int32, device="cuda")
-    rgd.probe(c2.model, c2.kv, c2.last, table, 1, k, 3, -1, ptok, plen, ev)
-    dec, miss = rgd.gate(c2.kv, ev, 1)
+    rgd.probe(p8192.model, p8192.kv, p8192.last, table, 1, k, 3, -1, ptok, plen, ev)
+    dec, miss = rgd.gate(p8192.kv, ev, 1)
     assert dec[0] == 0 and list(miss) == [0]
     out = t.full((1, N, S), -1, dtype=t.int32, device="cuda")
-    rgd.sample_continuations(c2.model, c2.kv, c2.last, list(miss), N, S, w.temperature, w.min_p, seeds, out)
+    rgd.sample_continuations(p8192.model, p8192.kv, p8192.last, list(miss), N, S, w.temperature, w.min_p, seeds, out)
     t.cuda.synchronize()
     assert t.equal(out, a)
-    assert t.equal(before[0], c2.kv.prefix_k) and t.equal(before[1], c2.kv.prefix_v)
+    assert t.equal(before[0], p8192.kv.prefix_k) and t.equal(before[1], p8192.kv.prefix_v)
     # the probe's first token is the argmax of the prompt's last logits
-    assert int(ptok[0, 0]) == int(c2.last[0].argmax())
+    assert int(ptok[0, 0]) == int(p8192.last[0].argmax())
 
 
 @pytest.mark.parametrize("layer", [0, 1])
-def test_c1_residual_precheck_score(rgd, c1, layer):
+def test_p512_residual_precheck_score(rgd, p512, layer):
     """Residual-stream classifier pre-check (Appendix A) on the 8B-shaped layer:
     the score of the prefilled last token within the bf16 tolerance of the
     oracle's, and the prefill's logits unchanged by the readout."""
     t = torch()
-    d = c1.w.d_model
+    d = p512.w.d_model
     g = np.random.default_rng(11 + layer)
     w = (g.normal(size=d) / np.sqrt(d)).astype(np.float32)
     b = 0.1
     scores = t.empty(1, dtype=t.float32, device="cuda")
-    plain = c1.last.clone()
-    c1.prefill(rgd)
-    plain.copy_(c1.last)
-    c1.kv.set_prefix_len(0, c1.P)
-    rgd.prefill_kv_scored(c1.model, c1.kv, c1.tok, c1.P, c1.last, layer, t.from_numpy(w).cuda(), b, scores)
+    plain = p512.last.clone()
+    p512.prefill(rgd)
+    plain.copy_(p512.last)
+    p512.kv.set_prefix_len(0, p512.P)
+    rgd.prefill_kv_scored(p512.model, p512.kv, p512.tok, p512.P, p512.last, layer, t.from_numpy(w).cuda(), b, scores)
     t.cuda.synchronize()
-    assert t.equal(plain, c1.last)
+    assert t.equal(plain, p512.last)
     taps = {}
-    cache = KVCache.from_arrays([c1.kp[0]], [c1.vp[0]])
-    c1.dec.prefill([c1.last_tok], cache, start_pos=c1.P, taps=taps)
+    cache = KVCache.from_arrays([p512.kp[0]], [p512.vp[0]])
+    p512.dec.prefill([p512.last_tok], cache, start_pos=p512.P, taps=taps)
     from oracle import precheck
     ref = precheck.residual_score(taps[layer], w.astype(np.float64), b)
     got = float(scores.item())
