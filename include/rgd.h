@@ -190,6 +190,21 @@ int32_t rgd_probe(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_
                   int32_t B, int32_t k, int32_t c, int32_t eos_id, int32_t* probe_tokens,
                   int32_t* probe_len, int32_t* event, rgd_stream stream);
 
+/* Probe without the compatibility gate (Appendix B's fixed-probe ablation;
+ * with k = L, the naive greedy-then-high-temperature approach of Section 3):
+ * greedy decoding always runs to k tokens, or to eos_id when it is set, and
+ * the refusal detector (the table's compatibility predicate, tbl NULL = no
+ * refusal set, every probe passes) is applied to the finished probe: event
+ * INCOMPAT when the probe is incompatible with every entry (a miss), else
+ * STOP or MAXLEN (a hit).  By prefix closure the decision equals rgd_probe's;
+ * only the decoded tokens differ (k instead of stopping at the first
+ * incompatible one).  Arguments, outputs, page use and the c cadence (host
+ * polls after tokens 1..c and every c tokens, which only ends prompts that
+ * reached eos) as rgd_probe.  Synchronous. */
+int32_t rgd_probe_fixed(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_table* tbl,
+                        int32_t B, int32_t k, int32_t c, int32_t eos_id, int32_t* probe_tokens,
+                        int32_t* probe_len, int32_t* event, rgd_stream stream);
+
 /* Probe with the soft compatibility gate (Appendix C, the soft-gate
  * algorithm); arguments and outputs as rgd_probe.  Tokens 1..c are soft steps:
  * when the greedy token would make the probe incompatible, the topk most

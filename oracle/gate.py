@@ -77,6 +77,31 @@ def probe(first_logits, next_logits, table, k: int, eos: int = -1, min_match: in
         logits = next_logits(q)
 
 
+def fixed_probe(first_logits, next_logits, table, k: int, eos: int = -1, min_match: int = 2,
+                pick=None):
+    """Probe without the compatibility gate: greedy decoding runs to k tokens
+    (or to a stop token) whatever the tokens are, and the refusal detector is
+    applied once to the finished probe.  This is the fixed-probe ablation of
+    Appendix B (k = 32) and, with k equal to the full response budget L, the
+    naive greedy-then-high-temperature approach of Section 3 (a complete
+    greedy answer first, sampling only when it is not a refusal).  Returns
+    (q, event): INCOMPAT when C(q) fails (the prompt is sampled), otherwise
+    STOP if decoding ended on the stop token and MAXLEN if it reached k."""
+    if pick is None:
+        from .sampler import argmax as pick
+    q = []
+    logits = first_logits
+    while True:
+        y = int(pick(logits))
+        q.append(y)
+        if (eos >= 0 and y == eos) or len(q) >= k:
+            break
+        logits = next_logits(q)
+    if not compatible(q, table, min_match):
+        return q, INCOMPAT
+    return q, (STOP if eos >= 0 and q[-1] == eos else MAXLEN)
+
+
 def top_k(z, K: int):
     """The K most probable tokens of logits z, most probable first (equal logits:
     lower id first), with their probabilities under softmax(z) over the whole

@@ -56,6 +56,19 @@ def greedy_probe(model: Decoder, prefix: KVCache, last_logits, table, k: int, eo
     return gate.probe(last_logits, nxt, table, k, eos, min_match)
 
 
+def fixed_greedy_probe(model: Decoder, prefix: KVCache, last_logits, table, k: int, eos: int = -1,
+                       min_match: int = 2):
+    """The probe with no compatibility gate (greedy decoding to k tokens, the
+    detector applied once at the end) against the shared prompt cache: the
+    fixed-probe ablation (Appendix B) and the naive greedy answer (Section 3)."""
+    tail = KVCache(model.cfg.n_layers)
+
+    def nxt(q):
+        return model.decode(q[-1], prefix, tail)
+
+    return gate.fixed_probe(last_logits, nxt, table, k, eos, min_match)
+
+
 def soft_greedy_probe(model: Decoder, prefix: KVCache, last_logits, table, k: int, c: int, K: int,
                       rho: float, eos: int = -1, min_match: int = 2, steps: list | None = None):
     """The probe of the soft compatibility-gate variant (Appendix C) against the

@@ -11,7 +11,7 @@ import ctypes as C
 import os
 
 __all__ = [
-    "RGDError", "lib", "ModelConfig", "Model", "KV", "Table", "prefill_kv", "probe", "gate",
+    "RGDError", "lib", "ModelConfig", "Model", "KV", "Table", "prefill_kv", "probe", "probe_fixed", "gate",
     "sample_continuations", "sample_continuations_pless", "check_status", "kernel_attention", "kernel_lm_head", "kernel_argmax",
     "kernel_sample", "kernel_sample_pless", "sampler_workspace_bytes", "timing_enable", "timing_read", "TIMERS", "EVENT_INCOMPAT", "EVENT_STOP", "EVENT_MAXLEN",
     "DTYPE_F32", "DTYPE_BF16",
@@ -21,7 +21,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librgd.so")
 EXPORTS = (
     "rgd_version", "rgd_last_error", "rgd_model_create", "rgd_model_destroy", "rgd_kv_create",
     "rgd_kv_destroy", "rgd_kv_set_prefix_len", "rgd_table_create", "rgd_table_destroy",
-    "rgd_prefill_kv", "rgd_prefill_kv_scored", "rgd_probe", "rgd_probe_soft", "rgd_probe_adaptive", "rgd_gate", "rgd_sample_continuations", "rgd_sample_continuations_pless", "rgd_check_status",
+    "rgd_prefill_kv", "rgd_prefill_kv_scored", "rgd_probe", "rgd_probe_fixed", "rgd_probe_soft", "rgd_probe_adaptive", "rgd_gate", "rgd_sample_continuations", "rgd_sample_continuations_pless", "rgd_check_status",
     "rgd_kernel_attention", "rgd_kernel_lm_head", "rgd_sampler_workspace_bytes",
     "rgd_kernel_argmax", "rgd_kernel_sample", "rgd_kernel_sample_pless", "rgd_kernel_probe_step", "rgd_timing_enable", "rgd_timing_read",
 )
@@ -82,6 +82,7 @@ _sig("rgd_table_create", I32, I32P, I32P, I32, I32P, I32, C.POINTER(VP))
 _sig("rgd_table_destroy", None, VP)
 _sig("rgd_prefill_kv", I32, VP, VP, VP, I32, I32, I32, VP, VP)
 _sig("rgd_probe", I32, VP, VP, VP, VP, I32, I32, I32, I32, VP, VP, VP, VP)
+_sig("rgd_probe_fixed", I32, VP, VP, VP, VP, I32, I32, I32, I32, VP, VP, VP, VP)
 _sig("rgd_probe_soft", I32, VP, VP, VP, VP, I32, I32, I32, I32, I32, C.c_float, VP, VP, VP, VP)
 _sig("rgd_probe_adaptive", I32, VP, VP, VP, VP, I32, I32, I32, I32, I32, C.c_float, VP, C.c_float, VP, VP, VP, VP)
 _sig("rgd_prefill_kv_scored", I32, VP, VP, VP, I32, I32, I32, VP, I32, VP, C.c_float, VP, VP)
@@ -224,6 +225,13 @@ def probe(model, kv, last_logits, table, B, k, c, eos, probe_tokens, probe_len, 
     """table None: fixed-length probe (no refusal set)."""
     _check(lib.rgd_probe(model.h, kv.h, _ptr(last_logits), table.h if table is not None else None, B, k, c,
                          eos, _ptr(probe_tokens), _ptr(probe_len), _ptr(event), _stream()))
+
+
+def probe_fixed(model, kv, last_logits, table, B, k, c, eos, probe_tokens, probe_len, event):
+    """Probe with no early exit: k greedy tokens (or up to eos), then the table
+    judges the finished probe (table None: every probe is a hit)."""
+    _check(lib.rgd_probe_fixed(model.h, kv.h, _ptr(last_logits), table.h if table is not None else None, B, k,
+                               c, eos, _ptr(probe_tokens), _ptr(probe_len), _ptr(event), _stream()))
 
 
 def kernel_probe_step(model, logits, table, k, c, eos, topk, rho, probe_tokens, probe_len, event):

@@ -166,6 +166,11 @@ struct GateArgs {
   int eos;
   unsigned long long* best_reset;  // same as best (cleared after use)
   int all_compatible;              // no refusal table (fixed-length probe): every probe passes
+  // no early exit (fixed probe): a probe runs to k tokens or to eos whatever
+  // its tokens are; failed[b] remembers an incompatible token and the event is
+  // set only when the probe ends (INCOMPAT if it failed, else STOP / MAXLEN)
+  int no_early_exit;
+  int* failed;                     // [B], cleared by the probe's initialisation
 };
 hipError_t probe_update(const GateArgs& a, hipStream_t s);
 

@@ -43,17 +43,19 @@ int fail(int code, const char* fmt, ...) {
 
 inline long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
 
+constexpr int kMaxParts = 40;      // attention partials per row (prefix splits + tail chunks)
+constexpr int kVecSplit = 256;     // prefix positions per split of the fp32 attention
+
 // Positions per prefix split of the bf16 attention: a function of the KV
 // state's shape only (prompt capacity, prompts, KV heads), never of the rows
 // of a step, so the split boundaries a row sees do not depend on the other
 // rows.  Enough splits that the prompts' (split, KV head) pairs fill the
-// chip (about 256 workgroups), a multiple of 64 positions.
+// chip (about 256 workgroups), at most kMaxParts of them, a multiple of 64
+// positions.
 int prefix_split_len(int P, int prompts, int Hkv) {
-  const long long S = std::max<long long>(1, cdiv(256, (long long)std::max(prompts, 1) * Hkv));
+  const long long S = std::min<long long>(kMaxParts, std::max<long long>(1, cdiv(256, (long long)std::max(prompts, 1) * Hkv)));
   return (int)std::max<long long>(64, cdiv(cdiv(std::max(P, 1), S), 64) * 64);
 }
-
-constexpr int kMaxParts = 40;      // attention partials per row (prefix splits + tail chunks)
 constexpr int kSampleChunk = 4096; // logits per sampler workgroup
 constexpr int kTailChunk = 256;
 
@@ -119,6 +121,7 @@ struct rgd_model {
   int* cur_tok = nullptr;
   int* status = nullptr;
   int* row_map = nullptr;
+  int* probe_fail = nullptr;  // fixed probe: incompatible token seen, per prompt [R]
   unsigned long long* soft_keys = nullptr;  // soft gate: per-chunk top-K keys [R][nchunks][kMaxTopK]
   float* soft_cm = nullptr;                 // soft gate: chunk maxima and sums [2][R][nchunks]
   // per-call row arrays
@@ -337,8 +340,8 @@ int run_attention(rgd_model* m, const KVLayout& kvl, const Rows& rows, const Hos
     }
     a.splits = (int)cdiv(std::max(h.maxplen, 1), a.split_len);
   } else {
-    a.split_len = 256;
-    a.splits = (int)cdiv(std::max(h.maxplen, 1), 256);
+    a.split_len = kVecSplit;
+    a.splits = (int)cdiv(std::max(h.maxplen, 1), kVecSplit);
   }
   a.nparts = a.splits + a.tail_chunks;
   if (a.nparts > cap || a.splits < 1)
@@ -555,12 +558,13 @@ __global__ void argmax_finish_kernel(unsigned long long* best, int R, int* out, 
 // Probe state before token 1; with pre-check scores, a prompt scored <= theta
 // is decided at once (SKIPPED: sampled without any check token).
 __global__ void probe_init_kernel(int B, int k, int* tokens, int* len, int* event, const float* scores,
-                                  float theta) {
+                                  float theta, int* failed) {
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (i < B * k) tokens[i] = 0;
   if (i < B) {
     len[i] = 0;
     event[i] = (scores && scores[i] <= theta) ? 3 : -1;
+    failed[i] = 0;
   }
 }
 
@@ -723,6 +727,7 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
   A(&m->cur_tok, (size_t)R * 4);
   A(&m->status, 4);
   A(&m->row_map, (size_t)R * 4);
+  A(&m->probe_fail, (size_t)R * 4);
   A(&m->d_gate, (size_t)(2 * R + 1) * 4);
   A(&m->soft_keys, (size_t)R * m->nchunks * kMaxTopK * 8);
   A(&m->soft_cm, (size_t)2 * R * m->nchunks * 4);
@@ -802,6 +807,8 @@ int32_t rgd_kv_create(const rgd_model* m, int32_t max_prompts, int32_t max_prefi
     return fail(RGD_E_INVALID_ARG, "kv sizes out of range");
   if (max_prefix > m->cfg.max_pos) return fail(RGD_E_INVALID_ARG, "max_prefix exceeds the model's max_pos");
   if (m->bf16 && page_size % 16) return fail(RGD_E_UNSUPPORTED, "bf16 models need page_size % 16 == 0");
+  if (!m->bf16 && max_prefix > kMaxParts * kVecSplit)
+    return fail(RGD_E_UNSUPPORTED, "fp32 models hold at most %d prefix positions", kMaxParts * kVecSplit);
   rgd_kv* kv = new rgd_kv();
   kv->m = m;
   kv->max_prompts = max_prompts;
@@ -971,10 +978,11 @@ int32_t rgd_prefill_kv_scored(rgd_model* m, rgd_kv* kv, const int32_t* tokens, i
 namespace {
 
 // The probe loop shared by the hard and the soft gate (topk > 0: tokens 1..c
-// are soft steps).
+// are soft steps) and the fixed probe (fixed: no early exit, the table judges
+// the finished probe).
 int probe_impl(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_table* tbl, int B, int k, int c,
                int eos_id, int topk, float rho, const float* scores, float theta, int* probe_tokens, int* probe_len,
-               int* event, rgd_stream stream) {
+               int* event, rgd_stream stream, bool fixed = false) {
   if (!m || !kv || !last_logits || !probe_tokens || !probe_len || !event)
     return fail(RGD_E_INVALID_ARG, "null argument");
   if (kv->m != m) return fail(RGD_E_INVALID_ARG, "kv belongs to another model");
@@ -1018,7 +1026,7 @@ int probe_impl(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_tab
     }
   } release{kv, s};
   hipLaunchKernelGGL(probe_init_kernel, dim3((int)cdiv((long long)B * k, 256)), dim3(256), 0, s, B, k, probe_tokens,
-                     probe_len, event, scores, theta);
+                     probe_len, event, scores, theta, m->probe_fail);
   HIP_OK(hipGetLastError());
 
   GateArgs ga{};
@@ -1040,6 +1048,8 @@ int probe_impl(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_tab
     ga.all_compatible = 1;  // fixed-length probe
   }
   ga.eos = eos_id;
+  ga.no_early_exit = fixed ? 1 : 0;
+  ga.failed = m->probe_fail;
   SoftArgs sa{};
   sa.V = V;
   sa.chunk = kSampleChunk;
@@ -1132,6 +1142,14 @@ int32_t rgd_probe(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_
   g_err.clear();
   return probe_impl(m, kv, last_logits, tbl, B, k, c, eos_id, 0, 0.f, nullptr, 0.f, probe_tokens, probe_len, event,
                     stream);
+}
+
+int32_t rgd_probe_fixed(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_table* tbl, int32_t B,
+                        int32_t k, int32_t c, int32_t eos_id, int32_t* probe_tokens, int32_t* probe_len,
+                        int32_t* event, rgd_stream stream) {
+  g_err.clear();
+  return probe_impl(m, kv, last_logits, tbl, B, k, c, eos_id, 0, 0.f, nullptr, 0.f, probe_tokens, probe_len, event,
+                    stream, true);
 }
 
 int32_t rgd_probe_soft(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_table* tbl, int32_t B,

@@ -587,7 +587,16 @@ __global__ __launch_bounds__(64) void probe_update_kernel(GateArgs a) {
     a.probe_tokens[(long long)b * a.k + j] = tok;
     a.probe_len[b] = j + 1;
     if (a.cur_tok) a.cur_tok[r] = tok;
-    a.event[b] = !compat ? 0 : (a.eos >= 0 && tok == a.eos) ? 1 : (j + 1 >= a.k) ? 2 : -1;
+    const bool stop = a.eos >= 0 && tok == a.eos, full = j + 1 >= a.k;
+    if (a.no_early_exit) {
+      // the detector judges the finished probe: incompatibility is sticky
+      // (prefix closure), so one failed token decides it
+      const bool failed = a.failed[b] || !compat;
+      a.failed[b] = failed;
+      a.event[b] = !(stop || full) ? -1 : failed ? 0 : stop ? 1 : 2;
+    } else {
+      a.event[b] = !compat ? 0 : stop ? 1 : full ? 2 : -1;
+    }
   }
 }
 

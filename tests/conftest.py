@@ -27,3 +27,19 @@ def pytest_collection_modifyitems(config, items):
     for it in items:
         if "gpu" in it.keywords:
             it.add_marker(skip)
+
+
+def pytest_sessionfinish(session, exitstatus):
+    # margin cases of the judged draws (sampled tokens whose oracle CDF or
+    # min-p margin is below 1e-4), per test case
+    try:
+        from tests.gpu_common import MARGIN_REPORT
+    except Exception:  # pragma: no cover
+        return
+    if not MARGIN_REPORT:
+        return
+    import json
+    out = os.path.join(ROOT, "gpurun_out")
+    os.makedirs(out, exist_ok=True)
+    with open(os.path.join(out, "margin_cases.json"), "w") as f:
+        json.dump(MARGIN_REPORT, f, indent=1, sort_keys=True)

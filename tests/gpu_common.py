@@ -50,6 +50,31 @@ def argmax_gpu(rgd, z_np):
 
 MARGIN = 1e-4
 
+# judged draws per test case: {case: {"exact", "margin-equal", "margin-diff", "draws"}},
+# written to gpurun_out/margin_cases.json at the end of a session that judged any
+MARGIN_REPORT = {}
+
+
+class Tally:
+    """Verdict counts of the draws judged under one name.  close() records them
+    in MARGIN_REPORT, prints them and bounds the margin-diff draws (tokens that
+    differ from the oracle's in a margin case) to max(1, frac * draws)."""
+
+    def __init__(self, name):
+        self.name = name
+        self.c = {"exact": 0, "margin-equal": 0, "margin-diff": 0}
+
+    def add(self, verdict):
+        self.c[verdict] += 1
+        return verdict
+
+    def close(self, max_diff_frac=0.01):
+        n = sum(self.c.values())
+        MARGIN_REPORT[self.name] = dict(self.c, draws=n)
+        print(self.name, self.c)
+        assert self.c["margin-diff"] <= max(1, int(max_diff_frac * n)), (self.name, self.c)
+        return self.c
+
 
 def _robust(w, kept, amb, u, tok, margin):
     """True when the oracle's draw `tok` cannot change under any flip of the

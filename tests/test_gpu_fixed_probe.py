@@ -1,0 +1,232 @@
+"""The probe without the compatibility gate (rgd_probe_fixed): Appendix B's
+fixed-probe ablation (k greedy tokens, then the refusal detector once) and,
+with k = L, Section 3's naive greedy-then-high-temperature approach.
+
+Oracle parity on the tiny fp32 decoder (every prompt's k greedy tokens and
+event against oracle.gate.fixed_probe, exact outside argmax margin cases),
+and on the 8B-shaped layers the properties that fix the result: the decision
+equals the early-exit probe's, the probe holds exactly the k tokens the
+path's own greedy decoding produces, and a miss samples exactly what ungated
+sampling does."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import gate as ogate
+from oracle import rgd as orgd
+from oracle import sampler
+from oracle.model import Decoder, KVCache
+from tests.gpu_common import seeds_tensor, torch
+
+pytestmark = pytest.mark.gpu
+W0 = synth.TINY_FP32
+MARGIN = 1e-4
+
+
+@pytest.fixture(scope="module")
+def rgd():
+    import paper_2607_20791_amd as m
+    return m
+
+
+def _csr(tables):
+    offs, toks, own = [0], [], []
+    for b, ents in enumerate(tables):
+        for e in ents:
+            toks.extend(e)
+            offs.append(len(toks))
+            own.append(b)
+    return offs, toks, own
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    """Oracle greedy sequences of L = 32 tokens per prompt (with their argmax
+    margins) and per-prompt tables: even prompts seeded with their first 4
+    greedy tokens, prompt 1 with its first 12 (a hit only while k <= 12)."""
+    weights = synth.model_weights(W0)
+    dec = Decoder(weights)
+    prompts = synth.prompt_tokens(W0)
+    L = W0.steps
+    caches, last, greedy, margins = [], [], [], []
+    for b in range(W0.n_prompts):
+        c = KVCache(W0.n_layers)
+        lg = dec.prefill(prompts[b], c)
+        last.append(lg)
+        caches.append(c)
+        tail = KVCache(W0.n_layers)
+        seq, mg = [], []
+        while True:
+            seq.append(sampler.argmax(lg))
+            mg.append(sampler.logit_margin_argmax(lg))
+            if len(seq) == L:
+                break
+            lg = dec.decode(seq[-1], c, tail)
+        greedy.append(seq)
+        margins.append(mg)
+    tables = []
+    for b in range(W0.n_prompts):
+        off, tok = synth.random_table(W0, f"table{b}")
+        ents = ogate.table_entries(off, tok)
+        if b % 2 == 0:
+            ents[0] = greedy[b][:4]
+        if b == 1:
+            ents[0] = greedy[b][:12]
+        tables.append(ents)
+    return dict(weights=weights, dec=dec, prompts=prompts, caches=caches, last=last, greedy=greedy,
+                margins=margins, tables=tables)
+
+
+@pytest.mark.parametrize("k", [W0.probe_k, W0.steps])
+def test_fixed_probe_tiny_matches_oracle(rgd, tiny, k):
+    """k = 8: the fixed probe of the tiny workload's probe budget; k = 32 (its
+    whole response length): the naive greedy answer.  Tokens, lengths and
+    events equal the oracle's fixed probe wherever every argmax had a margin
+    >= 1e-4; the decisions equal the early-exit probe's on the same GPU."""
+    t = torch()
+    from paper_2607_20791_amd import session
+    B, V = W0.n_prompts, W0.vocab
+    m = session.build_model(tiny["weights"], max_rows=64, max_pos=128)
+    kv = session.alloc_kv(m, W0, max_prompts=B, max_prefix=W0.prompt_len, n_pages=B * 2 + 8)
+    last = t.empty(B, V, dtype=t.float32, device="cuda")
+    rgd.prefill_kv(m, kv, session.to_device(tiny["prompts"]), 0, last)
+    offs, toks, own = _csr(tiny["tables"])
+    table = rgd.Table(offs, toks, own, min_match=2)
+    ptok = t.full((B, k), -7, dtype=t.int32, device="cuda")
+    plen = t.empty(B, dtype=t.int32, device="cuda")
+    ev = t.empty(B, dtype=t.int32, device="cuda")
+    rgd.probe_fixed(m, kv, last, table, B, k, 3, -1, ptok, plen, ev)
+    dec_f, miss_f = rgd.gate(kv, ev, B)
+    ptok_h, plen_h, ev_h = ptok.cpu().numpy(), plen.cpu().numpy(), ev.cpu().numpy()
+    # the early-exit probe on the same GPU: same decisions
+    ptok2 = t.empty(B, k, dtype=t.int32, device="cuda")
+    plen2 = t.empty(B, dtype=t.int32, device="cuda")
+    ev2 = t.empty(B, dtype=t.int32, device="cuda")
+    rgd.probe(m, kv, last, table, B, k, 3, -1, ptok2, plen2, ev2)
+    dec_e, miss_e = rgd.gate(kv, ev2, B)
+    assert list(dec_f) == list(dec_e) and list(miss_f) == list(miss_e)
+    assert (plen_h == k).all()
+    plen2_h, ptok2_h = plen2.cpu().numpy(), ptok2.cpu().numpy()
+    clean_n = 0
+    for b in range(B):
+        assert np.array_equal(ptok2_h[b, :plen2_h[b]], ptok_h[b, :plen2_h[b]]), b
+        seq = tiny["greedy"][b][:k]
+        q, e = ogate.fixed_probe(_first(seq), _scripted_next(seq), tiny["tables"][b], k)
+        assert q == seq
+        if all(mg >= MARGIN for mg in tiny["margins"][b][:k]):
+            clean_n += 1
+            assert list(ptok_h[b]) == q, b
+            assert ev_h[b] == e and dec_f[b] == int(ogate.is_hit(e)), b
+    print(f"k={k}: {clean_n} of {B} prompts without argmax margin cases; decisions {list(dec_f)}")
+    assert clean_n >= B // 2
+    assert all(dec_f[b] == 1 for b in range(0, B, 2))          # seeded prompts hit
+    assert dec_f[1] == int(k <= 12)                            # 12-token entry: a hit only up to k = 12
+    # the oracle end to end on one prompt through its own decoder (not the scripted sequence)
+    q, e = orgd.fixed_greedy_probe(tiny["dec"], tiny["caches"][1], tiny["last"][1], tiny["tables"][1], k)
+    if all(mg >= MARGIN for mg in tiny["margins"][1][:k]):
+        assert list(ptok_h[1]) == q and ev_h[1] == e
+
+
+def _first(seq):
+    z = np.full(max(seq) + 1, -1.0)
+    z[seq[0]] = 1.0
+    return z
+
+
+def _scripted_next(seq):
+    def nxt(q):
+        z = np.full(max(seq) + 1, -1.0)
+        z[seq[len(q)]] = 1.0
+        return z
+    return nxt
+
+
+def test_fixed_probe_eos_ends_early(rgd, tiny):
+    """With a stop token that the greedy sequence reaches before k, the fixed
+    probe ends there: a hit (STOP) when still compatible, a miss otherwise."""
+    t = torch()
+    from paper_2607_20791_amd import session
+    B, V, k = W0.n_prompts, W0.vocab, 16
+    m = session.build_model(tiny["weights"], max_rows=64, max_pos=128)
+    kv = session.alloc_kv(m, W0, max_prompts=B, max_prefix=W0.prompt_len, n_pages=B * 2 + 8)
+    last = t.empty(B, V, dtype=t.float32, device="cuda")
+    rgd.prefill_kv(m, kv, session.to_device(tiny["prompts"]), 0, last)
+    b0 = 0                               # prompt 0 hits (seeded entry = its first 4 tokens)
+    eos = int(tiny["greedy"][b0][5])     # its 6th greedy token stops it
+    if not all(mg >= MARGIN for mg in tiny["margins"][b0][:6]):
+        pytest.skip("argmax margin case on prompt 0")
+    offs, toks, own = _csr(tiny["tables"])
+    table = rgd.Table(offs, toks, own, min_match=2)
+    ptok = t.empty(B, k, dtype=t.int32, device="cuda")
+    plen = t.empty(B, dtype=t.int32, device="cuda")
+    ev = t.empty(B, dtype=t.int32, device="cuda")
+    rgd.probe_fixed(m, kv, last, table, B, k, 3, eos, ptok, plen, ev)
+    dec, _ = rgd.gate(kv, ev, B)
+    seq = tiny["greedy"][b0]
+    q, e = ogate.fixed_probe(_first(seq), _scripted_next(seq), tiny["tables"][b0], k, eos=eos)
+    n = int(plen[b0])
+    assert n == len(q) and list(ptok[b0, :n].cpu().numpy()) == q
+    assert int(ev[b0]) == e == ogate.STOP and dec[b0] == 1
+
+
+@pytest.fixture(scope="module")
+def p8192(rgd):
+    from tests.test_gpu_path_bf16 import World
+    return World(rgd, synth.LAYER_P8192)
+
+
+def _greedy(rgd, wd, k):
+    t = torch()
+    wd.prefill(rgd)
+    g = t.full((1, 1, k), -1, dtype=t.int32, device="cuda")
+    rgd.sample_continuations(wd.model, wd.kv, wd.last, [0], 1, k, 0.0, 0.0,
+                             t.zeros(1, dtype=t.int64, device="cuda"), g)
+    return g[0, 0].cpu().numpy()
+
+
+@pytest.mark.parametrize("k", [32, 128])
+def test_fixed_probe_8b_layer(rgd, p8192, k):
+    """The 8192-position layer, as timed: k = 32 (Appendix B) and k = 128 (the
+    naive greedy answer).  Typical table: the same miss as the early-exit
+    probe after k tokens, and the miss then samples what ungated sampling does.
+    A table holding the first 15 greedy tokens then a different 16th: a
+    full-length miss for the early-exit probe at 16 tokens, a miss after k
+    here.  A table holding the first 4 greedy tokens: a hit returning k
+    tokens.  The probe tokens are the path's own greedy tokens."""
+    t = torch()
+    w = p8192.w
+    g = _greedy(rgd, p8192, k)
+    off, toks = synth.random_table(w)
+    cases = {"typical": (off, toks, 0),
+             "adversarial": (np.array([0, 16], np.int32),
+                             np.array(list(g[:15]) + [int((g[15] + 1) % w.vocab)], np.int32), 0),
+             "hit": (np.array([0, 4], np.int32), np.array(g[:4], np.int32), 1)}
+    ptok = t.empty(1, k, dtype=t.int32, device="cuda")
+    plen = t.empty(1, dtype=t.int32, device="cuda")
+    ev = t.empty(1, dtype=t.int32, device="cuda")
+    for name, (o, tk, want) in cases.items():
+        table = rgd.Table(o, tk)
+        p8192.prefill(rgd)
+        rgd.probe_fixed(p8192.model, p8192.kv, p8192.last, table, 1, k, 3, -1, ptok, plen, ev)
+        dec, miss = rgd.gate(p8192.kv, ev, 1)
+        assert int(plen[0]) == k, name
+        assert np.array_equal(ptok[0].cpu().numpy(), g), name
+        assert dec[0] == want and int(ev[0]) == (ogate.MAXLEN if want else ogate.INCOMPAT), name
+        ents = ogate.table_entries(o, tk)
+        assert ogate.is_hit(ogate.fixed_probe(_first(list(g)), _scripted_next(list(g)), ents, k)[1]) == bool(want)
+        rgd.probe(p8192.model, p8192.kv, p8192.last, table, 1, k, 3, -1, ptok, plen, ev)
+        dec_e, _ = rgd.gate(p8192.kv, ev, 1)
+        assert dec_e[0] == want, name
+    # a fixed-probe miss samples exactly what ungated sampling does
+    N, S = 8, 16
+    seeds = seeds_tensor(synth.branch_seeds(1, N))
+    p8192.prefill(rgd)
+    a = t.full((1, N, S), -1, dtype=t.int32, device="cuda")
+    rgd.sample_continuations(p8192.model, p8192.kv, p8192.last, [0], N, S, w.temperature, w.min_p, seeds, a)
+    table = rgd.Table(off, toks)
+    rgd.probe_fixed(p8192.model, p8192.kv, p8192.last, table, 1, k, 3, -1, ptok, plen, ev)
+    _, miss = rgd.gate(p8192.kv, ev, 1)
+    b = t.full((1, N, S), -1, dtype=t.int32, device="cuda")
+    rgd.sample_continuations(p8192.model, p8192.kv, p8192.last, list(miss), N, S, w.temperature, w.min_p, seeds, b)
+    t.cuda.synchronize()
+    assert list(miss) == [0] and t.equal(a, b)

@@ -14,7 +14,7 @@ import synth
 from oracle import philox
 from oracle import rgd as orgd
 from oracle.model import Decoder, KVCache
-from tests.gpu_common import judge_draw, judge_draw_pless, rel_err, seeds_tensor, torch
+from tests.gpu_common import Tally, judge_draw, judge_draw_pless, rel_err, seeds_tensor, torch
 
 pytestmark = pytest.mark.gpu
 TOL = 2e-2
@@ -27,17 +27,20 @@ def rgd():
 
 
 class World:
-    def __init__(self, rgd, w):
+    """One 8B-shaped layer over a synthetic prefix: device model and KV state
+    (row capacity max_rows) and the oracle decoder with the prompt's logits."""
+
+    def __init__(self, rgd, w, max_rows=64, weights=None):
         from paper_2607_20791_amd import session
         t = torch()
         self.w = w
-        self.weights = synth.model_weights(w)
+        self.weights = synth.model_weights(w) if weights is None else weights
         self.P = w.synthetic_prefix
         self.kp, self.vp = synth.synthetic_prefix_kv(w, 0)
         self.last_tok = int(synth.prompt_tokens(w)[0, 0])
-        self.model = session.build_model(self.weights, max_rows=64, max_pos=self.P + 256)
+        self.model = session.build_model(self.weights, max_rows=max_rows, max_pos=self.P + 256)
         self.kv = session.alloc_kv(self.model, w, max_prompts=1, max_prefix=self.P + 1,
-                                   n_pages=64 * 8 + 24)
+                                   n_pages=max_rows * 8 + 24)
         session.fill_prefix(self.kv, 0, self.kp, self.vp)
         self.last = t.empty(1, w.vocab, dtype=t.float32, device="cuda")
         self.tok = t.tensor([[self.last_tok]], dtype=t.int32, device="cuda")
@@ -88,6 +91,7 @@ def _teacher_forced(rgd, wd, rows, steps, T, p_min, pless=False):
     rgd.check_status(wd.model)
     tap_h, got = tap.cpu().numpy(), out.cpu().numpy()[0]
     worst = 0.0
+    tally = Tally(f"{w.name} teacher-forced{' p-less' if pless else ''}, {rows} rows x {steps} tokens")
     for r in range(rows):
         br = orgd.sample_branch(wd.dec, wd.cache, wd.ref_last, int(seeds[r]), steps, T, p_min,
                                 forced=forced[r], keep_logits=True, truncation="pless" if pless else "minp")
@@ -97,10 +101,11 @@ def _teacher_forced(rgd, wd, rows, steps, T, p_min, pless=False):
         for s in range(steps):   # the sampler on the GPU's own logits
             u = float(philox.uniform(int(seeds[r]), s))
             if pless:
-                judge_draw_pless(tap_h[s, r], T, u, int(got[r, s]))
+                tally.add(judge_draw_pless(tap_h[s, r], T, u, int(got[r, s])))
             else:
-                judge_draw(tap_h[s, r], T, p_min, u, int(got[r, s]))
+                tally.add(judge_draw(tap_h[s, r], T, p_min, u, int(got[r, s])))
     print(w.name, "teacher-forced logits rel err (worst)", worst)
+    tally.close()
 
 
 def test_bf16_p512_prompt_logits(rgd, p512):

@@ -9,7 +9,7 @@ import synth
 from oracle import gate as ogate
 from oracle import philox, rgd as orgd, sampler
 from oracle.model import Decoder, KVCache
-from tests.gpu_common import judge_draw, rel_err, seeds_tensor, torch
+from tests.gpu_common import Tally, judge_draw, rel_err, seeds_tensor, torch
 
 pytestmark = pytest.mark.gpu
 W0 = synth.TINY_FP32
@@ -132,18 +132,19 @@ def test_fp32_path_end_to_end(rgd, world):
     rgd.check_status(m)
     got = out.cpu().numpy()
     assert t.equal(before[0], kv.prefix_k) and t.equal(before[1], kv.prefix_v)
-    counts = {"exact": 0, "margin-equal": 0, "margin-diff": 0}
+    tally = Tally("tiny fp32 decoder free-running, every miss x 32 tokens")
     for i, b in enumerate(miss):
         br = orgd.sample_branch(world["dec"], world["caches"][b], world["last"][b], int(b), S,
                                 W0.temperature, W0.min_p, keep_logits=True)
         for s in range(S):
             u = float(philox.uniform(int(b), s))
-            verdict = judge_draw(br.logits[s], W0.temperature, W0.min_p, u, int(got[i, 0, s]))
-            counts[verdict] += 1
+            verdict = tally.add(judge_draw(br.logits[s], W0.temperature, W0.min_p, u, int(got[i, 0, s])))
             if verdict == "margin-diff":
                 break       # the histories differ from here on
-    print("sampled tokens:", counts, "of", len(miss) * S)
-    assert counts["exact"] + counts["margin-equal"] >= len(miss) * S // 2
+    # at V = 8192, T = 2 nearly every draw is a margin case (CDF intervals of
+    # ~1e-4 of the kept weight); each branch is judged draw by draw until its
+    # first margin-diff draw, and at most one branch may diverge
+    tally.close(max_diff_frac=0.0)
 
     # ungated sampling from a fresh KV (no probe ever ran) gives the same tokens
     kv2 = session.alloc_kv(m, W0, max_prompts=B, max_prefix=W0.prompt_len, n_pages=96)
@@ -175,6 +176,7 @@ def test_fp32_teacher_forced_logits(rgd, world):
                              forced=session.to_device(forced), logits_tap=tap)
     t.cuda.synchronize()
     tap_h, got = tap.cpu().numpy(), out.cpu().numpy().reshape(-1, S)
+    tally = Tally("tiny fp32 decoder teacher-forced, 4 branches x 12 tokens")
     for r in range(len(prompts) * N):
         b = prompts[r // N]
         br = orgd.sample_branch(world["dec"], world["caches"][b], world["last"][b], int(seeds[r]), S,
@@ -182,4 +184,5 @@ def test_fp32_teacher_forced_logits(rgd, world):
         err = rel_err(tap_h[:, r], np.stack(br.logits))
         assert err.max() <= 1e-5, (r, err.max())
         for s in range(S):
-            judge_draw(br.logits[s], 1.5, 0.05, float(philox.uniform(int(seeds[r]), s)), int(got[r, s]))
+            tally.add(judge_draw(br.logits[s], 1.5, 0.05, float(philox.uniform(int(seeds[r]), s)), int(got[r, s])))
+    tally.close()

@@ -10,7 +10,7 @@ import synth
 from oracle import philox, pless
 from oracle import rgd as orgd
 from oracle.model import Decoder, KVCache
-from tests.gpu_common import judge_draw_pless, rel_err, seeds_tensor, torch
+from tests.gpu_common import Tally, judge_draw_pless, rel_err, seeds_tensor, torch
 
 pytestmark = pytest.mark.gpu
 MARGIN = 1e-4
@@ -44,26 +44,24 @@ def test_pless_single_draw_every_temperature(rgd, z, T):
     rows = z[:48]
     seeds = np.arange(48, dtype=np.uint64) + 500
     got = sample_pless_gpu(rgd, rows, T, seeds, ctr=3)[:, 0]
-    counts = {"exact": 0, "margin-equal": 0, "margin-diff": 0}
+    tally = Tally(f"p-less, sampler sweep, 48 rows, T={T}")
     for r in range(48):
-        counts[judge_draw_pless(rows[r], T, float(philox.uniform(int(seeds[r]), 3, 0)), int(got[r]))] += 1
-    print(f"T={T}: {counts}")
+        tally.add(judge_draw_pless(rows[r], T, float(philox.uniform(int(seeds[r]), 3, 0)), int(got[r])))
     # every draw was judged above (exact outside margin cases); from T = 2 on the
     # threshold falls inside the dense N(0, 1) tail, so most rows are margin
     # cases, nearly all of which still give the oracle's token
-    assert counts["margin-diff"] <= 5
+    tally.close()
 
 
 def test_pless_all_rows_and_further_draws(rgd, z):
     seeds = np.arange(256, dtype=np.uint64) * 7 + 1
     got = sample_pless_gpu(rgd, z, 2.0, seeds, ctr=9, stream0=4, draws=2)
-    counts = {"exact": 0, "margin-equal": 0, "margin-diff": 0}
+    tally = Tally("p-less, sampler sweep, 256 rows x 2 draws, T=2")
     for r in range(256):
         for d in range(2):
             u = float(philox.uniform(int(seeds[r]), 9, 4 + d))
-            counts[judge_draw_pless(z[r], 2.0, u, int(got[r, d]))] += 1
-    print(counts)
-    assert counts["margin-diff"] <= 0.05 * 512
+            tally.add(judge_draw_pless(z[r], 2.0, u, int(got[r, d])))
+    tally.close()
 
 
 def test_pless_thousand_draws_follow_the_kept_distribution(rgd, z):
@@ -142,18 +140,19 @@ def test_pless_decode_path_free_running(rgd, tiny):
     t.cuda.synchronize()
     rgd.check_status(m)
     got = out.cpu().numpy().reshape(-1, S)
-    counts = {"exact": 0, "margin-equal": 0, "margin-diff": 0}
+    tally = Tally("p-less, tiny fp32 decoder free-running, 8 branches x 24 tokens")
     for r in range(len(prompts) * N):
         b = prompts[r // N]
         br = orgd.sample_branch(tiny["dec"], tiny["caches"][b], tiny["last"][b], int(seeds[r]), S, T, 0.0,
                                 keep_logits=True, truncation="pless")
         for s in range(S):
-            v = judge_draw_pless(br.logits[s], T, float(philox.uniform(int(seeds[r]), s)), int(got[r, s]))
-            counts[v] += 1
+            v = tally.add(judge_draw_pless(br.logits[s], T, float(philox.uniform(int(seeds[r]), s)),
+                                           int(got[r, s])))
             if v == "margin-diff":
                 break       # the histories differ from here on
-    print("p-less decode path:", counts)
-    assert counts["exact"] + counts["margin-equal"] >= len(prompts) * N * S // 2
+    # a branch is compared draw by draw until its first margin-diff draw (its
+    # history then differs from the oracle's); at most one branch may diverge
+    tally.close(max_diff_frac=0.0)
     # deterministic: the same call gives the same tokens
     out2 = t.full_like(out, -1)
     rgd.sample_continuations_pless(m, kv, last, prompts, N, S, T, seeds_tensor(seeds), out2)

@@ -77,6 +77,69 @@ def test_early_exit_decision_equals_full_probe(seed):
         assert not gate.compatible(q, table) and gate.compatible(q[:-1], table) or len(q) == 1
 
 
+def _counting(seq):
+    """Scripted logits plus a counter of the decode steps asked for."""
+    first, nxt = _scripted(seq)
+    calls = []
+
+    def counted(q):
+        calls.append(len(q))
+        return nxt(q)
+    return first, counted, calls
+
+
+def test_fixed_probe_decodes_k_tokens_then_applies_the_detector():
+    """Appendix B: the probe always runs k greedy tokens, then the detector
+    decides once; Section 3's naive approach is the same with k = L."""
+    table = [[1, 2, 3]]
+    seq = [1, 5, 3, 4, 6, 7, 8, 2, 2]
+    first, nxt, calls = _counting(seq)
+    assert gate.fixed_probe(first, nxt, table, k=6) == (seq[:6], gate.INCOMPAT)
+    assert calls == [1, 2, 3, 4, 5]            # k - 1 decode steps after the prompt's own logits
+    # the early-exit probe stops at the second token with the same decision
+    first, nxt, calls = _counting(seq)
+    assert gate.probe(first, nxt, table, k=6) == ([1, 5], gate.INCOMPAT)
+    assert calls == [1]
+    first, nxt, calls = _counting([1, 2, 3, 4, 5, 6, 7])
+    assert gate.fixed_probe(first, nxt, table, k=6) == ([1, 2, 3, 4, 5, 6], gate.MAXLEN)
+    # a stop token ends decoding; compatible -> STOP (a greedy refusal), else INCOMPAT
+    first, nxt, calls = _counting([1, 2, 3, 9, 4])
+    assert gate.fixed_probe(first, nxt, table, k=6, eos=9) == ([1, 2, 3, 9], gate.STOP)
+    assert calls == [1, 2, 3]
+    first, nxt, _ = _counting([1, 2, 9, 4])
+    assert gate.fixed_probe(first, nxt, table, k=6, eos=9) == ([1, 2, 9], gate.INCOMPAT)
+    # an empty table never matches; no table at all (None) always does
+    first, nxt, _ = _counting([7, 7, 7, 7])
+    assert gate.fixed_probe(first, nxt, [], k=3) == ([7, 7, 7], gate.INCOMPAT)
+    first, nxt, _ = _counting([7, 7, 7, 7])
+    assert gate.fixed_probe(first, nxt, None, k=3) == ([7, 7, 7], gate.MAXLEN)
+    # k = 1: the prompt's logits alone
+    first, nxt, calls = _counting([1, 5])
+    assert gate.fixed_probe(first, nxt, table, k=1) == ([1], gate.MAXLEN) and calls == []
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_fixed_probe_same_decision_as_early_exit(seed):
+    """Prefix closure: the fixed probe and the gated probe decide alike on every
+    prompt; the gated probe's tokens are a prefix of the fixed probe's, which
+    always has k tokens unless a stop token came first."""
+    g = np.random.default_rng(300 + seed)
+    table = [list(g.integers(0, 3, size=g.integers(2, 5))) for _ in range(3)]
+    seq = list(g.integers(0, 4, size=14))
+    eos = int(g.integers(-1, 4))
+    k = int(g.integers(1, 12))
+    first, nxt = _scripted(seq)
+    qe, ee = gate.probe(first, nxt, table, k=k, eos=eos)
+    first, nxt = _scripted(seq)
+    qf, ef = gate.fixed_probe(first, nxt, table, k=k, eos=eos)
+    assert gate.is_hit(ee) == gate.is_hit(ef)
+    if gate.is_hit(ef):
+        assert qe == qf and ee == ef
+    assert qf[:len(qe)] == qe
+    stop = [i for i, y in enumerate(seq[:k]) if y == eos]
+    assert len(qf) == (stop[0] + 1 if stop else k)
+
+
 def test_table_entries_csr():
     assert gate.table_entries(np.array([0, 2, 5]), np.array([4, 5, 6, 7, 8])) == [[4, 5], [6, 7, 8]]
 
