@@ -43,7 +43,9 @@ def _csr(tables):
 def tiny():
     """Oracle greedy sequences of L = 32 tokens per prompt (with their argmax
     margins) and per-prompt tables: even prompts seeded with their first 4
-    greedy tokens, prompt 1 with its first 12 (a hit only while k <= 12)."""
+    greedy tokens; prompt 1 with its first 12 (a hit at every k: a shorter
+    probe is a prefix of the entry, a longer one passes it); prompt 3 with its
+    first 9 and a different 10th (a hit only while k <= 9)."""
     weights = synth.model_weights(W0)
     dec = Decoder(weights)
     prompts = synth.prompt_tokens(W0)
@@ -72,6 +74,8 @@ def tiny():
             ents[0] = greedy[b][:4]
         if b == 1:
             ents[0] = greedy[b][:12]
+        if b == 3:
+            ents[0] = greedy[b][:9] + [(greedy[b][9] + 1) % W0.vocab]
         tables.append(ents)
     return dict(weights=weights, dec=dec, prompts=prompts, caches=caches, last=last, greedy=greedy,
                 margins=margins, tables=tables)
@@ -120,7 +124,8 @@ def test_fixed_probe_tiny_matches_oracle(rgd, tiny, k):
     print(f"k={k}: {clean_n} of {B} prompts without argmax margin cases; decisions {list(dec_f)}")
     assert clean_n >= B // 2
     assert all(dec_f[b] == 1 for b in range(0, B, 2))          # seeded prompts hit
-    assert dec_f[1] == int(k <= 12)                            # 12-token entry: a hit only up to k = 12
+    assert dec_f[1] == 1                                       # 12-token entry: a hit at every k
+    assert dec_f[3] == int(k <= 9)                             # differs from the greedy answer at token 10
     # the oracle end to end on one prompt through its own decoder (not the scripted sequence)
     q, e = orgd.fixed_greedy_probe(tiny["dec"], tiny["caches"][1], tiny["last"][1], tiny["tables"][1], k)
     if all(mg >= MARGIN for mg in tiny["margins"][1][:k]):
