@@ -348,6 +348,22 @@ int32_t rgd_kernel_sample(const float* z, int32_t R, int32_t V, float T, float m
                           const uint64_t* seeds, uint32_t ctr, uint32_t stream0, int32_t draws,
                           void* workspace, int32_t* out, rgd_stream stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the draws of
+ * rgd_kernel_sample, same arguments without the workspace, which is taken from
+ * a fixed array of RGD_NOALLOC_SCRATCH_BYTES the library holds on each device
+ * it runs on until the process ends.  Allocates nothing.  Calls with
+ * rgd_sampler_workspace_bytes(R, V) > RGD_NOALLOC_SCRATCH_BYTES are rejected
+ * (RGD_E_INVALID_ARG) before any HIP call.  Every call on one device shares
+ * that array: calls that overlap on one device (several streams or threads)
+ * race and must be serialised by the caller.  The first call on a device
+ * looks up the array's device address (hipGetSymbolAddress) with that device
+ * current.  Asynchronous. */
+#define RGD_NOALLOC_SCRATCH_BYTES 1048576
+int32_t rgd_kernel_sample_noalloc(const float* z, int32_t R, int32_t V, float T, float min_p,
+                                  const uint64_t* seeds, uint32_t ctr, uint32_t stream0, int32_t draws,
+                                  int32_t* out, rgd_stream stream);
+
 /* p-less draws on z dev fp32 [R][V] (keep p_i >= sum_j p_j^2 of softmax(z/T),
  * see rgd_sample_continuations_pless; V a multiple of 4, V <= 1048576,
  * T > 0); seeds, counters, workspace and out as for rgd_kernel_sample.

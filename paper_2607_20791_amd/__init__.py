@@ -13,7 +13,7 @@ import os
 __all__ = [
     "RGDError", "lib", "ModelConfig", "Model", "KV", "Table", "prefill_kv", "probe", "probe_fixed", "gate",
     "sample_continuations", "sample_continuations_pless", "check_status", "kernel_attention", "kernel_lm_head", "kernel_argmax",
-    "kernel_sample", "kernel_sample_pless", "sampler_workspace_bytes", "timing_enable", "timing_read", "TIMERS", "EVENT_INCOMPAT", "EVENT_STOP", "EVENT_MAXLEN",
+    "kernel_sample", "kernel_sample_noalloc", "kernel_sample_pless", "sampler_workspace_bytes", "timing_enable", "timing_read", "TIMERS", "EVENT_INCOMPAT", "EVENT_STOP", "EVENT_MAXLEN",
     "DTYPE_F32", "DTYPE_BF16",
 ]
 
@@ -23,7 +23,7 @@ EXPORTS = (
     "rgd_kv_destroy", "rgd_kv_set_prefix_len", "rgd_table_create", "rgd_table_destroy",
     "rgd_prefill_kv", "rgd_prefill_kv_scored", "rgd_probe", "rgd_probe_fixed", "rgd_probe_soft", "rgd_probe_adaptive", "rgd_gate", "rgd_sample_continuations", "rgd_sample_continuations_pless", "rgd_check_status",
     "rgd_kernel_attention", "rgd_kernel_lm_head", "rgd_sampler_workspace_bytes",
-    "rgd_kernel_argmax", "rgd_kernel_sample", "rgd_kernel_sample_pless", "rgd_kernel_probe_step", "rgd_timing_enable", "rgd_timing_read",
+    "rgd_kernel_argmax", "rgd_kernel_sample", "rgd_kernel_sample_noalloc", "rgd_kernel_sample_pless", "rgd_kernel_probe_step", "rgd_timing_enable", "rgd_timing_read",
 )
 
 DTYPE_F32, DTYPE_BF16 = 0, 1
@@ -97,6 +97,7 @@ _sig("rgd_kernel_lm_head", I32, VP, VP, I32, VP, VP)
 _sig("rgd_sampler_workspace_bytes", U64, I32, I32)
 _sig("rgd_kernel_argmax", I32, VP, I32, I32, VP, VP, VP)
 _sig("rgd_kernel_sample", I32, VP, I32, I32, F32, F32, VP, U32, U32, I32, VP, VP, VP)
+_sig("rgd_kernel_sample_noalloc", I32, VP, I32, I32, F32, F32, VP, U32, U32, I32, VP, VP)
 _sig("rgd_kernel_sample_pless", I32, VP, I32, I32, F32, VP, U32, U32, I32, VP, VP, VP)
 _sig("rgd_timing_enable", I32, VP, I32)
 _sig("rgd_timing_read", I32, VP, C.POINTER(C.c_double), C.POINTER(C.c_int64))
@@ -334,6 +335,17 @@ def kernel_sample(z, T, min_p, seeds, ctr, stream0, draws, workspace, out):
     R, V = z.shape
     _check(lib.rgd_kernel_sample(_ptr(z), R, V, T, min_p, _ptr(seeds), ctr, stream0, draws,
                                  _ptr(workspace), _ptr(out), _stream()))
+
+
+NOALLOC_SCRATCH_BYTES = 1 << 20
+
+
+def kernel_sample_noalloc(z, T, min_p, seeds, ctr, stream0, draws, out):
+    """rgd_kernel_sample without a workspace: the library's fixed device scratch
+    (RGD_NOALLOC_SCRATCH_BYTES) is used; nothing is allocated."""
+    R, V = z.shape
+    _check(lib.rgd_kernel_sample_noalloc(_ptr(z), R, V, T, min_p, _ptr(seeds), ctr, stream0, draws, _ptr(out),
+                                         _stream()))
 
 
 def kernel_sample_pless(z, T, seeds, ctr, stream0, draws, workspace, out):

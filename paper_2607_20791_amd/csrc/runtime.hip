@@ -9,6 +9,7 @@
 #include <string>
 #include <vector>
 
+#include "entry.hpp"
 #include "kernels.hpp"
 #include "rgd.h"
 
@@ -1512,7 +1513,9 @@ int32_t rgd_kernel_argmax(const float* z, int32_t R, int32_t V, void* workspace,
 
 }  // extern "C"
 
-namespace {
+namespace rgd {
+
+int32_t set_error(int32_t code, const char* msg) { return fail(code, "%s", msg); }
 
 int32_t kernel_sample(const float* z, int32_t R, int32_t V, float T, float min_p, bool pless,
                       const uint64_t* seeds, uint32_t ctr, uint32_t stream0, int32_t draws, void* workspace,
@@ -1559,7 +1562,7 @@ int32_t kernel_sample(const float* z, int32_t R, int32_t V, float T, float min_p
   return RGD_OK;
 }
 
-}  // namespace
+}  // namespace rgd
 
 extern "C" {
 

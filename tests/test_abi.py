@@ -108,3 +108,15 @@ def test_kernel_sampler_validation(rgd):
     assert rgd.lib.rgd_kernel_argmax(fake, 0, 8, fake, fake, None) == 1
     assert rgd.lib.rgd_sampler_workspace_bytes(4, 152064) >= 8 * 4 + 4 * 4 + 16 * 4 * 38
     assert rgd.lib.rgd_sampler_workspace_bytes(0, 8) == 0
+
+
+def test_noalloc_sampler_rejects_before_any_hip_call(rgd):
+    """The no-allocation sampler validates sizes (against its fixed scratch)
+    and arguments before touching the GPU, so this runs without one."""
+    fake = C.c_void_p(0x1000)
+    assert _code(rgd.lib.rgd_kernel_sample_noalloc(None, 4, 8, 1.0, 0.1, fake, 0, 0, 1, fake, None)) == 1
+    assert _code(rgd.lib.rgd_kernel_sample_noalloc(fake, 4096, 152064, 1.0, 0.1, fake, 0, 0, 1, fake, None)) == 1
+    assert b"scratch" in rgd.lib.rgd_last_error()
+    assert _code(rgd.lib.rgd_kernel_sample_noalloc(fake, 4, 8, 0.0, 0.1, fake, 0, 0, 1, fake, None)) == 1
+    assert _code(rgd.lib.rgd_kernel_sample_noalloc(fake, 4, 8, 1.0, 1.5, fake, 0, 0, 1, fake, None)) == 1
+    assert rgd.sampler_workspace_bytes(160, 152064) <= rgd.NOALLOC_SCRATCH_BYTES
