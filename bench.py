@@ -28,9 +28,19 @@ sys.path.insert(0, ROOT)
 METRIC = "gated decode tokens/sec (probe+N branches) + % HBM roofline, attn & sampler"
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
-# the library times every unit of decode steps 1, 1+P, 1+2P, ... of each
-# sampling call (P = TIMING_PERIOD); the other steps run without event records
-TIMING_PERIOD = 8
+# the library times decode steps 1, 1+P, 1+2P, ... of each sampling call
+# (P = TIMING_PERIOD), one unit per timed step in turn (LM head, attention
+# stage, prefix attention kernel, sampler, whole step); the other steps run
+# without event records
+TIMING_PERIOD = 4
+TIMER_UNITS = ("lm_head", "attention", "attn_prefix", "sampler", "step")
+
+
+def timed_steps(n_decode, unit):
+    """Indices i (decode step i + 1) of the steps of one sampling call on which
+    the library timed `unit`."""
+    u = TIMER_UNITS.index(unit)
+    return [i for i in range(n_decode) if i % TIMING_PERIOD == 0 and (i // TIMING_PERIOD) % len(TIMER_UNITS) == u]
 
 
 def log(*a):
@@ -602,7 +612,7 @@ def main():
         st_ms, st_n = tim["step"]
         lm_avg = lm_ms / lm_n
         lm_gbs = lm_b / (lm_avg * 1e-3) / 1e9
-        timed = [i for i in range(len(att_b)) if i % TIMING_PERIOD == 0]  # decode step i+1
+        timed = timed_steps(len(att_b), "attention")  # decode step i+1
         att_total_b = sum(att_b[i] for i in timed) * n_miss_steps
         att_gbs = att_total_b / (at_ms * 1e-3) / 1e9
         attp_total_b = (2 * Pp * w.n_kv_heads * w.head_dim * 2) * ap_n

@@ -294,14 +294,17 @@ enum rgd_timer {
 };
 
 /* period >= 1: from now on the model records HIP events on the work stream
- * around each timed unit: inside rgd_sample_continuations, for every unit of
- * decode steps 1, 1 + period, 1 + 2 period, ... (the draw from the prompt's
- * logits is not timed when period > 1); elsewhere, every launch.  At most
- * 8192 timed launches per unit between reads; later launches are not timed.
- * A period above 1 keeps most steps free of event records, which otherwise
- * leave small idle gaps on the stream.  period == 0 stops recording; negative
- * is RGD_E_INVALID_ARG.  Events are created on the first enable, not on the
- * decode path. */
+ * around timed units.  Inside rgd_sample_continuations, decode step s (s >= 1)
+ * is timed when (s - 1) % period == 0, and only one unit is timed in such a
+ * step: unit ((s - 1) / period) % RGD_TIMER_COUNT (LM head, attention stage,
+ * shared-prefix attention kernel, sampler, whole step, in turn), so that no
+ * unit's measurement holds another unit's event records; the draw from the
+ * prompt's logits is never timed.  Elsewhere every launch of every unit is
+ * timed (the prefix kernel's events then sit inside the attention stage's).
+ * At most 8192 timed launches per unit between reads; later launches are not
+ * timed.  Each event record leaves a small idle gap on the stream.  period == 0
+ * stops recording; negative is RGD_E_INVALID_ARG.  Events are created on the
+ * first enable, not on the decode path. */
 int32_t rgd_timing_enable(rgd_model* m, int32_t period);
 
 /* Waits for the recorded events and returns, per timed unit, the summed

@@ -16,6 +16,8 @@
 //
 // fp32 path: vector kernels of the same structure (prefix splits, then tail
 // plus merge).
+#include <type_traits>
+
 #include "kernels.hpp"
 
 namespace rgd {
@@ -46,6 +48,9 @@ constexpr float kNoRef = -3.0e38f;
 
 #ifndef RGD_ATTN_NW
 #define RGD_ATTN_NW 8
+#endif
+#ifndef RGD_ATTN_RING
+#define RGD_ATTN_RING 3
 #endif
 
 // K tiles sit in LDS as unpadded 256-byte rows whose 16-byte chunks are
@@ -94,7 +99,7 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
     vok[nt] = v < nq;
     vrow[nt] = r0 + (vok[nt] ? v / G : 0);
     vhead[nt] = g * G + (vok[nt] ? v % G : 0);
-    vend[nt] = vok[nt] ? min(a.rows.plen[vrow[nt]], hi) : lo;
+    vend[nt] = vok[nt] ? min(prefix_part_end(a.rows.plen[vrow[nt]], a.split_len), hi) : lo;
     const bf16_t* qp = (const bf16_t*)a.q + ((long long)vrow[nt] * a.Hq + vhead[nt]) * D + grp * 8;
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks)
@@ -133,20 +138,25 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
   constexpr int KSEG = TP * 16 / NT, VSEG = D * (TP / 8) / NT;  // 16-byte segments per thread
   u32x4 kreg[KSEG], vreg[VSEG];
   int vt0 = 0;
+  // A whole tile (all 64 positions inside the split) takes the unpredicated
+  // loads and stores; only a split's ragged last tile is masked (the branch
+  // is uniform over the workgroup).
   auto load_tile = [&](int t0) {
     vt0 = t0;
+    const bool whole = t0 + TP <= hi;
+    const bf16_t* vblk = vbase + (long long)(t0 / TP) * D * TP;
 #pragma unroll
     for (int i = 0; i < KSEG; ++i) {
       const int seg = threadIdx.x + i * NT;
       const int pos = t0 + (seg >> 4);
-      kreg[i] = pos < hi ? *(const u32x4*)(kbase + (long long)pos * D + (seg & 15) * 8) : u32x4{0u, 0u, 0u, 0u};
+      const u32x4* src = (const u32x4*)(kbase + (long long)pos * D + (seg & 15) * 8);
+      kreg[i] = (whole || pos < hi) ? *src : u32x4{0u, 0u, 0u, 0u};
     }
 #pragma unroll
     for (int i = 0; i < VSEG; ++i) {
       const int seg = threadIdx.x + i * NT;
-      const int d = seg >> 3, p0 = t0 + (seg & 7) * 8;
-      vreg[i] = p0 < hi ? *(const u32x4*)(vbase + ((long long)(t0 / TP) * D + d) * TP + (seg & 7) * 8)
-                        : u32x4{0u, 0u, 0u, 0u};
+      const u32x4* src = (const u32x4*)(vblk + (seg >> 3) * TP + (seg & 7) * 8);
+      vreg[i] = (whole || t0 + (seg & 7) * 8 < hi) ? *src : u32x4{0u, 0u, 0u, 0u};
     }
   };
   auto store_tile = [&](int buf) {
@@ -156,14 +166,22 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
       const int row = seg >> 4;
       *(u32x4*)&k_lds[buf][row * D + (((seg & 15) ^ kswz(row)) * 8)] = kreg[i];
     }
+    if (vt0 + TP <= hi) {
 #pragma unroll
-    for (int i = 0; i < VSEG; ++i) {
-      const int seg = threadIdx.x + i * NT;
-      const int nv = hi - (vt0 + (seg & 7) * 8);  // valid positions of this segment
-      u32x4 vv = vreg[i];
+      for (int i = 0; i < VSEG; ++i) {
+        const int seg = threadIdx.x + i * NT;
+        *(u32x4*)&v_lds[buf][seg >> 3][(seg & 7) * 8] = vreg[i];
+      }
+    } else {
 #pragma unroll
-      for (int w = 0; w < 4; ++w) vv[w] &= nv >= 2 * w + 2 ? 0xFFFFFFFFu : (nv == 2 * w + 1 ? 0xFFFFu : 0u);
-      *(u32x4*)&v_lds[buf][seg >> 3][(seg & 7) * 8] = vv;
+      for (int i = 0; i < VSEG; ++i) {
+        const int seg = threadIdx.x + i * NT;
+        const int nv = hi - (vt0 + (seg & 7) * 8);  // valid positions of this segment
+        u32x4 vv = vreg[i];
+#pragma unroll
+        for (int w = 0; w < 4; ++w) vv[w] &= nv >= 2 * w + 2 ? 0xFFFFFFFFu : (nv == 2 * w + 1 ? 0xFFFFu : 0u);
+        *(u32x4*)&v_lds[buf][seg >> 3][(seg & 7) * 8] = vv;
+      }
     }
   };
 
@@ -261,18 +279,20 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
   // One straight-line stream per half: the scores of the following half
   // (buffer kb, half kh, into nxt), the exponentials of this half (cur)
   // interleaved with them, then this half's P V product (buffer vb, half vh).
-  // 16 fragment reads go through a 3-slot register ring, NQ MFMAs each.  After
+  // 16 fragment reads go through a register ring of RGD_ATTN_RING slots, NQ
+  // MFMAs each.  After
   // the last half kb holds stale data and nxt is simply not used.
   auto stream = [&](int kb, int kh, int vb, int vh, f32x4 (&cur)[2][NQ], f32x4 (&nxt)[2][NQ]) {
     auto frag = [&](int f) -> u32x4 { return f < 8 ? k_frag(kb, kh, f >> 2, f & 3) : v_frag(vb, f - 8, vh); };
-    u32x4 ring[3];
-    ring[0] = frag(0);
-    ring[1] = frag(1);
+    constexpr int RD = RGD_ATTN_RING;  // fragment reads in flight + 1
+    u32x4 ring[RD];
+#pragma unroll
+    for (int f = 0; f + 1 < RD; ++f) ring[f] = frag(f);
     float plo[NQ];
     uint32_t pw[NQ][4];  // packed weights, word 2e + (i >> 1)
 #pragma unroll
     for (int f = 0; f < 16; ++f) {
-      if (f + 2 < 16) ring[(f + 2) % 3] = frag(f + 2);
+      if (f + RD - 1 < 16) ring[(f + RD - 1) % RD] = frag(f + RD - 1);
       if (f < 8) {
         const int e = f >> 2, ks = f & 3;
         if (ks == 0) {
@@ -280,7 +300,7 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
           for (int nt = 0; nt < NQ; ++nt) nxt[e][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
 #pragma unroll
-        for (int nt = 0; nt < NQ; ++nt) nxt[e][nt] = mfma16x16x32(ring[f % 3], qf[nt][ks], nxt[e][nt]);
+        for (int nt = 0; nt < NQ; ++nt) nxt[e][nt] = mfma16x16x32(ring[f % RD], qf[nt][ks], nxt[e][nt]);
         // step f handles value i = f & 3 of block e = f >> 2; pairs are packed
         // to bf16 as soon as both halves exist
 #pragma unroll
@@ -293,7 +313,7 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
         const int dt = f - 8;
 #pragma unroll
         for (int nt = 0; nt < NQ; ++nt)
-          o[dt][nt] = mfma16x16x32(ring[f % 3], u32x4{pw[nt][0], pw[nt][1], pw[nt][2], pw[nt][3]}, o[dt][nt]);
+          o[dt][nt] = mfma16x16x32(ring[f % RD], u32x4{pw[nt][0], pw[nt][1], pw[nt][2], pw[nt][3]}, o[dt][nt]);
         if (dt == 7) {
 #pragma unroll
           for (int n2 = 0; n2 < NQ; ++n2)
@@ -314,8 +334,11 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
     __syncthreads();
     f32x4 sa[2][NQ], sb[2][NQ];
     if (wave_active) scores(0, 0, sa);
-    for (int t = 0; t < ntile; ++t) {
-      const int t0 = lo + t * TP, cb = t % NB, nb = (t + 1) % NB;
+    // tile t uses ring buffer t % NB; the loop is unrolled by NB so that every
+    // buffer index is a constant (LDS offsets fold into the instructions)
+    auto tile = [&](int t, auto cbc) {
+      constexpr int cb = decltype(cbc)::value, nb = (cb + 1) % NB;
+      const int t0 = lo + t * TP;
       if (t + 1 < ntile) {  // publish tile t+1
         store_tile(nb);
         if (t + 2 < ntile) load_tile(t0 + 2 * TP);
@@ -327,6 +350,12 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
         prepare(t0 + 32, sb);
         stream(nb, 0, cb, 1, sb, sa);
       }
+    };
+    static_assert(NB == 3, "the tile loop is unrolled by the ring depth");
+    for (int t = 0; t < ntile; t += NB) {
+      tile(t, std::integral_constant<int, 0>{});
+      if (t + 1 < ntile) tile(t + 1, std::integral_constant<int, 1>{});
+      if (t + 2 < ntile) tile(t + 2, std::integral_constant<int, 2>{});
     }
   }
 
@@ -642,28 +671,46 @@ __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t
   f32x4 o[8];
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // the row's own positions: first its prefix positions the split kernel left
+  // (fewer than 64 past a split boundary, read in place from the shared
+  // prefix), then its paged tail; 32-position tiles of either, dealt to the
+  // four waves in turn
   const int n = a.tail_len;
   const int* pages = n > 0 ? a.rows.pages + (long long)r * a.rows.max_pages : nullptr;
-  for (int tb = wave * TT; tb < n; tb += 4 * TT) {
+  const int plen = a.rows.plen[r];
+  const int pe = prefix_part_end(plen, a.split_len);
+  const int n_ovt = (plen - pe + TT - 1) / TT, n_all = n_ovt + (n + TT - 1) / TT;
+  const long long bg = (long long)a.rows.prompt[r] * a.Hkv + g;
+  const bf16_t* pk = (const bf16_t*)a.kv.prefix_k + bg * a.kv.P * D;
+  const bf16_t* pv = (const bf16_t*)a.kv.prefix_v + bg * a.kv.VP * D;
+  for (int vt = wave; vt < n_all; vt += 4) {
+    const bool ov = vt < n_ovt;
+    const int tb = ov ? pe + vt * TT : (vt - n_ovt) * TT;  // first position of the tile
+    const int lim = ov ? plen : n;                          // positions < lim exist
     u32x4 ka[2][4], va[8];
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
       const int pos = tb + k_gather_row(0, e, l16);
-      const bool ok = pos < n;
-      const int pp = ok ? pos : 0;
-      const bf16_t* kr = (const bf16_t*)a.kv.pool_k +
-                         (((long long)pages[pp / ps] * a.Hkv + g) * ps + pp % ps) * D + grp * 8;
+      const bool ok = pos < lim;
+      const int pp = ok ? pos : tb;
+      const bf16_t* kr = ov ? pk + (long long)pp * D + grp * 8
+                            : (const bf16_t*)a.kv.pool_k +
+                                  (((long long)pages[pp / ps] * a.Hkv + g) * ps + pp % ps) * D + grp * 8;
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) ka[e][ks] = ok ? *(const u32x4*)(kr + ks * 32) : u32x4{0u, 0u, 0u, 0u};
     }
-    const int p0 = tb + grp * 8;  // this lane's eight positions p0 .. p0+7 (one page: ps % 8 == 0)
-    const int nv = n - p0;
+    // this lane's eight positions p0 .. p0+7 lie in one page (ps % 8 == 0) or
+    // one 64-position block of the prefix V layout (p0 % 8 == 0)
+    const int p0 = tb + grp * 8;
+    const int nv = lim - p0;
     {
-      const int pp = nv > 0 ? p0 : 0;
-      const bf16_t* vr = (const bf16_t*)a.kv.pool_v +
-                         (((long long)pages[pp / ps] * a.Hkv + g) * D + l16) * ps + pp % ps;
+      const int pp = nv > 0 ? p0 : tb;
+      const bf16_t* vr = ov ? pv + ((long long)(pp / 64) * D + l16) * 64 + pp % 64
+                            : (const bf16_t*)a.kv.pool_v +
+                                  (((long long)pages[pp / ps] * a.Hkv + g) * D + l16) * ps + pp % ps;
+      const long long vstep = ov ? 16LL * 64 : 16LL * ps;  // 16 head-dim rows
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt) va[dt] = nv > 0 ? *(const u32x4*)(vr + (long long)dt * 16 * ps) : u32x4{0u, 0u, 0u, 0u};
+      for (int dt = 0; dt < 8; ++dt) va[dt] = nv > 0 ? *(const u32x4*)(vr + dt * vstep) : u32x4{0u, 0u, 0u, 0u};
     }
     f32x4 sc[2];
 #pragma unroll
@@ -677,7 +724,7 @@ __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t
     for (int e = 0; e < 2; ++e)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        if (p0 + e * 4 + i >= n) sc[e][i] = -INFINITY;
+        if (p0 + e * 4 + i >= lim) sc[e][i] = -INFINITY;
         x = fmaxf(x, sc[e][i]);
       }
     x = fmaxf(x, __shfl_xor(x, 16, 64));
@@ -699,7 +746,7 @@ __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t
 #pragma unroll
     for (int i = 0; i < 8; ++i) lsum += p[i];
     const u32x4 pb = {pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]), pack2(p[6], p[7])};
-    if (nv < 8) {  // V past the tail end is arbitrary (unwritten page slots): zero it
+    if (nv < 8) {  // V past the row's end is arbitrary (unwritten slots): zero it
 #pragma unroll
       for (int dt = 0; dt < 8; ++dt)
 #pragma unroll

@@ -65,6 +65,17 @@ struct KVLayout {
 
 inline int v_stride(int P) { return (P + 63) / 64 * 64; }
 
+// bf16 attention: the prefix positions of a row attended by the prefix-split
+// kernel are [0, end); when a row's prefix passes a split boundary by fewer
+// than 64 positions, those last positions [end, plen) are attended by the
+// tail kernel instead (read in place from the prefix), so that no split holds
+// a nearly empty 64-position tile.  A function of the row's own length and the
+// KV state's split length only.
+__host__ __device__ inline int prefix_part_end(int plen, int split_len) {
+  const int rem = plen % split_len;
+  return (plen >= split_len && rem < 64) ? plen - rem : plen;
+}
+
 // ------------------------------------------------------------ elementwise ----
 // x[r] = E[tok[i * tok_stride]] with i = tok_map[r] (tok_map null: i = r), ids
 // clamped to [0, V); xn[r] = rmsnorm(x[r]) * g

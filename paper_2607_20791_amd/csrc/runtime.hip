@@ -50,12 +50,15 @@ constexpr int kVecSplit = 256;     // prefix positions per split of the fp32 att
 // Positions per prefix split of the bf16 attention: a function of the KV
 // state's shape only (prompt capacity, prompts, KV heads), never of the rows
 // of a step, so the split boundaries a row sees do not depend on the other
-// rows.  Enough splits that the prompts' (split, KV head) pairs fill the
-// chip (about 256 workgroups), at most kMaxParts of them, a multiple of 64
-// positions.
+// rows.  About 256 workgroups for the prompts' (split, KV head) pairs (one per
+// CU), at most kMaxParts splits: S* splits share the whole 64-position tiles
+// of the capacity evenly, and a row's positions past a split boundary by fewer
+// than 64 go to the tail kernel (prefix_part_end), so a row never needs more
+// than S* splits (an 8193-position prefix: 32 splits of 256, the last position
+// with the tail).
 int prefix_split_len(int P, int prompts, int Hkv) {
   const long long S = std::min<long long>(kMaxParts, std::max<long long>(1, cdiv(256, (long long)std::max(prompts, 1) * Hkv)));
-  return (int)std::max<long long>(64, cdiv(cdiv(std::max(P, 1), S), 64) * 64);
+  return (int)(64 * cdiv(std::max(P / 64, 1), S));
 }
 constexpr int kSampleChunk = 4096; // logits per sampler workgroup
 constexpr int kTailChunk = 256;
@@ -144,6 +147,10 @@ struct rgd_model {
   // the sampling loop tstep is 0 and every launch is timed
   int tstep = 0;
   int tperiod = 1;
+  // inside the sampling loop one unit is timed per timed step, in turn (unit
+  // (tstep / tperiod) % RGD_TIMER_COUNT), so no unit's events sit inside
+  // another's timed region
+  bool tloop = false;
   ~rgd_model() {
     for (auto& v : tev)
       for (hipEvent_t e : v) (void)hipEventDestroy(e);
@@ -208,7 +215,9 @@ struct TimeScope {
   hipStream_t s;
   bool on;
   TimeScope(rgd_model* m_, int unit_, hipStream_t s_) : m(m_), unit(unit_), s(s_) {
-    on = m->timing && m->tstep % m->tperiod == 0 && m->tused[unit] < (int)m->tev[unit].size() / 2;
+    on = m->timing && m->tstep % m->tperiod == 0 &&
+         (!m->tloop || (m->tstep / m->tperiod) % RGD_TIMER_COUNT == unit) &&
+         m->tused[unit] < (int)m->tev[unit].size() / 2;
     if (on) (void)hipEventRecord(m->tev[unit][2 * m->tused[unit]], s);
   }
   ~TimeScope() {
@@ -339,7 +348,12 @@ int run_attention(rgd_model* m, const KVLayout& kvl, const Rows& rows, const Hos
     } else {
       a.split_len = kvl.split_len;
     }
-    a.splits = (int)cdiv(std::max(h.maxplen, 1), a.split_len);
+    // splits up to the longest row's prefix-kernel part (the rest of a row's
+    // prefix, fewer than 64 positions past a split boundary, is attended with
+    // its tail)
+    int pe = 1;
+    for (int p : h.plen) pe = std::max(pe, prefix_part_end(p, a.split_len));
+    a.splits = (int)cdiv(pe, a.split_len);
   } else {
     a.split_len = kVecSplit;
     a.splits = (int)cdiv(std::max(h.maxplen, 1), kVecSplit);
@@ -1281,9 +1295,13 @@ int32_t sample_continuations(rgd_model* m, rgd_kv* kv, const float* last_logits,
   if (T > 0.f && !pless) HIP_OK(chunk_max(z0, V, R, V, kSampleChunk, m->tilemax, s));
   struct StepIndex {  // restores the timing step index on every exit
     rgd_model* m;
-    ~StepIndex() { m->tstep = 0; }
+    ~StepIndex() {
+      m->tstep = 0;
+      m->tloop = false;
+    }
   } step_index{m};
   m->tstep = -1;  // the first draw (prompt logits) is not timed
+  m->tloop = true;
   // the sampler writes the next step's input rows itself unless tokens are
   // forced (teacher forcing feeds other tokens) or no step follows
   bool embedded = false;
