@@ -4,7 +4,7 @@
 // prompt.  bf16 path: the shared part is split over (prefix split, KV head,
 // row block); a workgroup streams 64-position K/V tiles of its split through
 // LDS once and all query vectors of the row block (rows x the G query heads of
-// the KV head, up to 256) consume them with MFMA.  Scores are computed
+// the KV head, up to RGD_ATTN_QV) consume them with MFMA.  Scores are computed
 // transposed, S^T = K Q^T, with the K rows gathered so that each lane ends up
 // holding eight consecutive positions of one query vector; those feed
 // O^T += V^T P^T directly as the B operand, and the V cache is kept
@@ -68,7 +68,10 @@ RGD_DEV int kswz(int r) { return (r & 3) | ((r >> 1) & 12); }
 RGD_DEV int k_gather_row(int h, int e, int l16) { return h * 32 + (l16 >> 2) * 8 + e * 4 + (l16 & 3); }
 
 // Shared-prefix attention: one workgroup per (prefix split, KV head, block of
-// up to 256 query vectors of one prompt).  NW waves each own NQ MFMA column
+// up to RGD_ATTN_QV query vectors of one prompt).  The row blocks of one
+// (split, KV head) are Hkv * splits workgroups apart in dispatch order, a
+// multiple of the 8 XCDs the dispatcher deals workgroups to in turn, so they
+// share one XCD's L2 for their common tiles.  NW waves each own NQ MFMA column
 // tiles of 16 query vectors, so each K / V^T fragment read from LDS feeds NQ
 // MFMAs and each 64-position tile is fetched from HBM once for all rows of the
 // prompt.  The tile loop is software-pipelined: tiles are fetched into
@@ -78,9 +81,13 @@ RGD_DEV int k_gather_row(int h, int e, int l16) { return h * 32 + (l16 >> 2) * 8
 template <int NW, int NQ>
 __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
   constexpr int D = 128, TP = 64, NT = NW * 64, NB = 3;
-  static_assert(NW * NQ * 16 == 256, "a workgroup covers 256 query vectors");
+  static_assert(NW * NQ * 16 == RGD_ATTN_QV, "a workgroup covers RGD_ATTN_QV query vectors");
   const int s = blockIdx.x, g = blockIdx.y;
-  const int4 rb = blockIdx.z == 0 ? a.rblock0 : a.rblocks[blockIdx.z];
+  // the first row blocks come with the arguments (scalar loads, no dependent
+  // memory round trip); further ones from the row-block table
+  const int z = blockIdx.z;
+  const int4 rb = z == 0 ? a.rblk[0] : z == 1 ? a.rblk[1] : z == 2 ? a.rblk[2] : z == 3 ? a.rblk[3]
+                                                                                      : a.rblocks[z];
   const int r0 = rb.x, nr = rb.y, b = rb.z, maxplen = rb.w;
   const int lo = s * a.split_len;
   const int hi = min(lo + a.split_len, maxplen);
@@ -831,9 +838,9 @@ __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t
 }  // namespace
 
 hipError_t attn_prefix_bf16(const AttnArgs& a, hipStream_t s) {
-  if (a.D != 128 || a.Hq / a.Hkv > 256 || a.split_len % 64 || a.kv.VP % 64) return hipErrorInvalidValue;
+  if (a.D != 128 || a.Hq / a.Hkv > RGD_ATTN_QV || a.split_len % 64 || a.kv.VP % 64) return hipErrorInvalidValue;
   if (a.splits <= 0 || a.nrblocks <= 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_prefix_kernel<RGD_ATTN_NW, 16 / RGD_ATTN_NW>), dim3(a.splits, a.Hkv, a.nrblocks),
+  hipLaunchKernelGGL((attn_prefix_kernel<RGD_ATTN_NW, RGD_ATTN_QV / 16 / RGD_ATTN_NW>), dim3(a.splits, a.Hkv, a.nrblocks),
                      dim3(RGD_ATTN_NW * 64), 0, s, a);
   return hipGetLastError();
 }

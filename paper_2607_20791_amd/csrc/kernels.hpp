@@ -101,6 +101,20 @@ hipError_t residual_readout(const float* x, long long row0, long long stride, in
                             float b, float* out, hipStream_t s);
 
 // -------------------------------------------------------------- attention ----
+// Query vectors (rows x the G query heads of one KV head) per workgroup of the
+// bf16 shared-prefix attention, and the number of (prefix split, KV head)
+// pairs its split length is sized for.  128 query vectors (32 rows of a GQA
+// group of 4) and 128 pairs: a 64-row decode step runs 256 workgroups, two
+// row blocks per 512-position split of an 8193-position prefix, which halves
+// the split partials that 256-vector blocks over 256-position splits write and
+// merge.
+#ifndef RGD_ATTN_QV
+#define RGD_ATTN_QV 128
+#endif
+#ifndef RGD_ATTN_WGS
+#define RGD_ATTN_WGS 128
+#endif
+constexpr int kAttnInlineBlocks = 4;
 struct AttnArgs {
   const void* q;            // [R][Hq][D]
   Rows rows;
@@ -111,14 +125,14 @@ struct AttnArgs {
   int nparts;
   // prefix (shared) part
   const int4* rblocks; int nrblocks;  // (r0, nr, prompt, maxplen) row blocks for the MFMA path
-  int4 rblock0;                       // rblocks[0], passed by value (no dependent load)
+  int4 rblk[kAttnInlineBlocks];       // rblocks[0..3] passed by value (no dependent load)
   int splits; int split_len;          // prefix splits (part index 0..splits-1)
   // tail part
   int tail_len;             // visible tail positions (decode), 0 for prefill
   int tail_chunk; int tail_chunks;    // part index splits .. splits+tail_chunks-1
 };
 // bf16, head_dim 128: prefix-split partials 0 .. splits-1 on MFMA, row blocks
-// of up to 256 query vectors of one prompt
+// of up to RGD_ATTN_QV query vectors of one prompt
 hipError_t attn_prefix_bf16(const AttnArgs& a, hipStream_t s);
 // bf16, head_dim 128, G <= 16: each row's paged tail on MFMA, merged with the
 // prefix-split partials into the final output
@@ -152,6 +166,10 @@ struct SampleArgs {
   const float* gain; float eps; float* x; void* xn;
   // optional [R] per-row threshold on w (p-less); null: p_min for every row
   const float* row_thr;
+  // optional [R][nchunks * 16] kept sums of the 256-logit sub-chunks (decode
+  // path, nchunks * 16 <= 1024): written by the sum pass, located by one wave
+  // of the draw, which then rescans one sub-chunk instead of a whole chunk
+  float* sub_sums;
 };
 hipError_t minp_sample(const SampleArgs& a, hipStream_t s);
 // rows without producer maxima: chunk maxima into cmax [R][nchunks] and the

@@ -50,14 +50,14 @@ constexpr int kVecSplit = 256;     // prefix positions per split of the fp32 att
 // Positions per prefix split of the bf16 attention: a function of the KV
 // state's shape only (prompt capacity, prompts, KV heads), never of the rows
 // of a step, so the split boundaries a row sees do not depend on the other
-// rows.  About 256 workgroups for the prompts' (split, KV head) pairs (one per
-// CU), at most kMaxParts splits: S* splits share the whole 64-position tiles
+// rows.  About RGD_ATTN_WGS (split, KV head) pairs over the prompts (each with
+// one workgroup per row block), at most kMaxParts splits: S* splits share the whole 64-position tiles
 // of the capacity evenly, and a row's positions past a split boundary by fewer
 // than 64 go to the tail kernel (prefix_part_end), so a row never needs more
-// than S* splits (an 8193-position prefix: 32 splits of 256, the last position
+// than S* splits (an 8193-position prefix: 16 splits of 512, the last position
 // with the tail).
 int prefix_split_len(int P, int prompts, int Hkv) {
-  const long long S = std::min<long long>(kMaxParts, std::max<long long>(1, cdiv(256, (long long)std::max(prompts, 1) * Hkv)));
+  const long long S = std::min<long long>(kMaxParts, std::max<long long>(1, cdiv(RGD_ATTN_WGS, (long long)std::max(prompts, 1) * Hkv)));
   return (int)(64 * cdiv(std::max(P / 64, 1), S));
 }
 constexpr int kSampleChunk = 4096; // logits per sampler workgroup
@@ -119,6 +119,7 @@ struct rgd_model {
   float* logits = nullptr;
   float* tilemax = nullptr;
   float* chunk_sums = nullptr;
+  float* sub_sums = nullptr;  // [R][nchunks * 16] kept sums of 256-logit sub-chunks
   float* pl_stats = nullptr;  // p-less: chunk maxima, sums of w and w^2 [3][R][nchunks]
   float* pl_thr = nullptr;    // p-less: per-row threshold on w [R]
   unsigned long long* best = nullptr;
@@ -261,11 +262,11 @@ struct HostRows {
   int maxplen = 0;
 };
 
-// Row blocks of one prompt for the shared-prefix attention kernel: up to 256
-// query vectors (rows x G query heads) per block.
+// Row blocks of one prompt for the shared-prefix attention kernel: up to
+// RGD_ATTN_QV query vectors (rows x G query heads) per block.
 void build_blocks(const rgd_model* m, HostRows& h) {
   const int G = m->cfg.n_heads / m->cfg.n_kv_heads;
-  const int per = std::max(1, (m->bf16 ? 256 : 64) / G);
+  const int per = std::max(1, (m->bf16 ? RGD_ATTN_QV : 64) / G);
   h.blocks.clear();
   h.maxplen = 0;
   const int R = (int)h.prompt.size();
@@ -335,7 +336,7 @@ int run_attention(rgd_model* m, const KVLayout& kvl, const Rows& rows, const Hos
   a.part_lse = m->part_lse;
   a.rblocks = m->d_rblocks;
   a.nrblocks = (int)h.blocks.size();
-  if (!h.blocks.empty()) a.rblock0 = h.blocks[0];
+  for (int i = 0; i < kAttnInlineBlocks && i < (int)h.blocks.size(); ++i) a.rblk[i] = h.blocks[i];
   a.tail_len = tail_len;
   a.tail_chunk = kTailChunk;
   a.tail_chunks = 0;  // tails are attended inside the merge kernel
@@ -543,6 +544,7 @@ SampleArgs sample_args(rgd_model* m, const float* z, long long ldz, int R, int V
   a.chunk = kSampleChunk;
   a.nchunks = (int)cdiv(V, kSampleChunk);
   a.chunk_sums = m->chunk_sums;
+  if (a.nchunks * 16 <= 1024) a.sub_sums = m->sub_sums;
   a.seeds = seeds;
   a.ctr = ctr;
   a.stream = 0;
@@ -736,6 +738,7 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
   A(&m->logits, (size_t)R * cfg->vocab * 4);
   A(&m->tilemax, (size_t)R * m->ntiles * 4);
   A(&m->chunk_sums, (size_t)R * m->nchunks * 4);
+  A(&m->sub_sums, (size_t)R * m->nchunks * 16 * 4);
   A(&m->pl_stats, (size_t)3 * R * m->nchunks * 4);
   A(&m->pl_thr, (size_t)R * 4);
   A(&m->best, (size_t)R * 8);

@@ -243,6 +243,29 @@ RGD_DEV int select_token(const SampleArgs& a, int r, float mx, float u, float mi
   return fb != 0x7FFFFFFF ? fb : lb;
 }
 
+// Kept sums of chunk c of row r from each thread's four float4 partials
+// (part[k]: logits (threadIdx.x + 256 k) * 4 .. +3 of the chunk).  With
+// sub_sums, the 16 sub-chunks of 256 logits: wave w's partials at step k cover
+// sub-chunk 4k + w exactly, so each is one wave reduction (no barrier);
+// otherwise the chunk's sum.
+RGD_DEV void store_kept_sums(const SampleArgs& a, int r, int c, const float (&part)[4], float* red) {
+  if (a.sub_sums) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    float* dst = a.sub_sums + ((long long)r * a.nchunks + c) * 16 + w;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const float t = wave_sum(part[k]);
+      if (lane == 0) dst[4 * k] = t;
+    }
+  } else {
+    float sum = 0.f;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) sum += part[k];
+    sum = block_sum(sum, red);
+    if (threadIdx.x == 0) a.chunk_sums[(long long)r * a.nchunks + c] = sum;
+  }
+}
+
 __global__ __launch_bounds__(256) void minp_sum_kernel(SampleArgs a) {
   __shared__ float red[4];
   const int c = blockIdx.x, r = blockIdx.y;
@@ -258,18 +281,15 @@ __global__ __launch_bounds__(256) void minp_sum_kernel(SampleArgs a) {
   }
   const float mx = row_max_from_partials(a.pmax, a.npmax, r, red);
   const float kT = kLog2e / a.T;
-  float sum = 0.f;
+  float part[4];
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const float w0 = kept_weight(v[k].x, mx, kT, a.p_min), w1 = kept_weight(v[k].y, mx, kT, a.p_min);
     const float w2 = kept_weight(v[k].z, mx, kT, a.p_min), w3 = kept_weight(v[k].w, mx, kT, a.p_min);
-    sum += (w0 > 0.f ? w0 : 0.f) + (w1 > 0.f ? w1 : 0.f) + (w2 > 0.f ? w2 : 0.f) + (w3 > 0.f ? w3 : 0.f);
+    part[k] = (w0 > 0.f ? w0 : 0.f) + (w1 > 0.f ? w1 : 0.f) + (w2 > 0.f ? w2 : 0.f) + (w3 > 0.f ? w3 : 0.f);
   }
-  sum = block_sum(sum, red);
-  if (threadIdx.x == 0) {
-    a.chunk_sums[(long long)r * a.nchunks + c] = sum;
-    if (c == 0 && a.status && !(mx > -INFINITY && mx < INFINITY)) atomicOr(a.status, 1);
-  }
+  store_kept_sums(a, r, c, part, red);
+  if (threadIdx.x == 0 && c == 0 && a.status && !(mx > -INFINITY && mx < INFINITY)) atomicOr(a.status, 1);
 }
 
 // Standalone rows (no partial maxima from a producer): one read of the
@@ -515,7 +535,7 @@ __global__ __launch_bounds__(256) void pless_sum_kernel(SampleArgs a, const floa
     thr_out[r] = thr;
     if (a.status && !(m > -INFINITY && m < INFINITY)) atomicOr(a.status, 1);
   }
-  float sum = 0.f;
+  float part[4] = {0.f, 0.f, 0.f, 0.f};
   if (kept_weight(cmax[r0 + c], m, kT, thr) >= 0.f) {  // uniform: one value per workgroup
     const float* zr = a.z + r * a.ldz;
     const int lo = c * a.chunk, hi = min(a.V, lo + a.chunk);
@@ -529,11 +549,127 @@ __global__ __launch_bounds__(256) void pless_sum_kernel(SampleArgs a, const floa
     for (int k = 0; k < 4; ++k) {
       const float w0 = kept_weight(v[k].x, m, kT, thr), w1 = kept_weight(v[k].y, m, kT, thr);
       const float w2 = kept_weight(v[k].z, m, kT, thr), w3 = kept_weight(v[k].w, m, kT, thr);
-      sum += (w0 > 0.f ? w0 : 0.f) + (w1 > 0.f ? w1 : 0.f) + (w2 > 0.f ? w2 : 0.f) + (w3 > 0.f ? w3 : 0.f);
+      part[k] = (w0 > 0.f ? w0 : 0.f) + (w1 > 0.f ? w1 : 0.f) + (w2 > 0.f ? w2 : 0.f) + (w3 > 0.f ? w3 : 0.f);
     }
-    sum = block_sum(sum, red);
   }
-  if (t == 0) a.chunk_sums[r0 + c] = sum;
+  store_kept_sums(a, r, c, part, red);
+}
+
+// The draw from sub-chunk kept sums (decode path): wave 0 makes the draw in
+// two dependent reads and no barrier.  Each lane takes SP = nsub / 64
+// consecutive sub-chunk sums (a lane-local running sum, then a wave scan of
+// the lane totals gives every sub-chunk's running sum in id order); the first
+// sub-chunk whose running sum exceeds u * W is rescanned, four logits per
+// lane, with a second wave scan.  The token (the smallest kept id whose
+// running sum exceeds u * W; else the sub-chunk's last kept id) then goes
+// through LDS to all four waves for the next step's embedding row and
+// RMSNorm.
+__global__ __launch_bounds__(256) void minp_select_sub_kernel(SampleArgs a) {
+  constexpr int kMaxSP = 16;
+  __shared__ int sh_tok;
+  const int r = blockIdx.x;
+  const int lane = threadIdx.x & 63;
+  if (threadIdx.x < 64) {
+    const int nsub = a.nchunks * 16;
+    const int SP = (nsub + 63) / 64;
+    const float* ss = a.sub_sums + (long long)r * nsub;
+    float loc[kMaxSP];
+#pragma unroll
+    for (int i = 0; i < kMaxSP; ++i) {
+      const int j = lane * SP + i;
+      loc[i] = (i < SP && j < nsub) ? ss[j] : 0.f;
+    }
+    const float* pm = a.pmax + (long long)r * a.npmax;
+    float mx = -INFINITY;
+    for (int i = lane; i < a.npmax; i += 64) mx = fmaxf(mx, pm[i]);
+    const float u = philox_uniform(a.seeds[r], a.ctr, a.stream);
+    const float thr = a.row_thr ? a.row_thr[r] : a.p_min;
+    mx = wave_max(mx);
+#pragma unroll
+    for (int i = 1; i < kMaxSP; ++i) loc[i] += loc[i - 1];
+    const float tl = loc[kMaxSP - 1];
+    float incl = tl;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const float t = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += t;
+    }
+    float excl = __shfl_up(incl, 1, 64);
+    if (lane == 0) excl = 0.f;
+    const float W = __shfl(incl, 63, 64);
+    const float target = u * W;
+    // first sub-chunk whose running sum passes the target; the last non-empty one
+    int jf = 0x7FFFFFFF, jl = -1;
+    float prev = excl;
+#pragma unroll
+    for (int i = 0; i < kMaxSP; ++i) {
+      const int j = lane * SP + i;
+      if (i < SP && j < nsub) {
+        const float run = excl + loc[i];
+        if (run > prev) jl = j;
+        if (jf == 0x7FFFFFFF && run > target) jf = j;
+        prev = run;
+      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      jf = min(jf, __shfl_xor(jf, o, 64));
+      jl = max(jl, __shfl_xor(jl, o, 64));
+    }
+    const int js = jf != 0x7FFFFFFF ? jf : max(jl, 0);
+    // running sum before sub-chunk js, from the lane that holds it
+    const int ow = js / SP, oi = js - ow * SP;
+    float b = excl;
+#pragma unroll
+    for (int i = 1; i < kMaxSP; ++i)
+      if (i == oi) b = excl + loc[i - 1];
+    const float base = __shfl(b, ow, 64);
+    // rescan: lane l holds logits js * 256 + 4 l .. +3 (V is a multiple of 4)
+    const int e0 = js * 256 + lane * 4;
+    const float* zr = a.z + r * a.ldz;
+    const float4 zv = e0 < a.V ? *(const float4*)(zr + e0) : float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+    const float kT = kLog2e / a.T;
+    float wv[4] = {kept_weight(zv.x, mx, kT, thr), kept_weight(zv.y, mx, kT, thr), kept_weight(zv.z, mx, kT, thr),
+                   kept_weight(zv.w, mx, kT, thr)};
+    if (e0 >= a.V) wv[0] = wv[1] = wv[2] = wv[3] = -1.f;
+    const float ts = (wv[0] > 0.f ? wv[0] : 0.f) + (wv[1] > 0.f ? wv[1] : 0.f) + (wv[2] > 0.f ? wv[2] : 0.f) +
+                     (wv[3] > 0.f ? wv[3] : 0.f);
+    float inc2 = ts;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const float t = __shfl_up(inc2, o, 64);
+      if (lane >= o) inc2 += t;
+    }
+    float run = base + (inc2 - ts);
+    int found = 0x7FFFFFFF, last = -1;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (wv[i] >= 0.f) {
+        run += wv[i];
+        last = e0 + i;
+        if (found == 0x7FFFFFFF && run > target) found = e0 + i;
+      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      found = min(found, __shfl_xor(found, o, 64));
+      last = max(last, __shfl_xor(last, o, 64));
+    }
+    const int tok = found != 0x7FFFFFFF ? found : (last >= 0 ? last : js * 256);
+    if (lane == 0) {
+      sh_tok = tok;
+      a.out[r * a.out_stride + a.out_col] = tok;
+      if (a.cur_tok) a.cur_tok[r] = tok;
+    }
+  }
+  if (!a.embed) return;
+  __syncthreads();
+  const int tok = sh_tok;
+  float* x = a.x + (long long)r * a.d;
+  if (a.embed_bf16)
+    embed_norm_row(tok, (const bf16_t*)a.embed, a.d, a.vocab, a.gain, a.eps, x, (bf16_t*)a.xn + (long long)r * a.d);
+  else
+    embed_norm_row(tok, (const float*)a.embed, a.d, a.vocab, a.gain, a.eps, x, (float*)a.xn + (long long)r * a.d);
 }
 
 __global__ __launch_bounds__(256) void minp_select_kernel(SampleArgs a) {
@@ -642,8 +778,12 @@ hipError_t minp_sample(const SampleArgs& a, hipStream_t s) {
   if (a.chunk % 1024 || a.chunk > 4096 || a.V % 4 || a.nchunks > 256 ||
       a.nchunks * a.chunk < a.V || !(a.T > 0.f))
     return hipErrorInvalidValue;
+  if (a.sub_sums && a.nchunks * 16 > 1024) return hipErrorInvalidValue;
   hipLaunchKernelGGL(minp_sum_kernel, dim3(a.nchunks, a.R), dim3(256), 0, s, a);
-  hipLaunchKernelGGL(minp_select_kernel, dim3(a.R), dim3(256), 0, s, a);
+  if (a.sub_sums)
+    hipLaunchKernelGGL(minp_select_sub_kernel, dim3(a.R), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(minp_select_kernel, dim3(a.R), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -674,8 +814,12 @@ hipError_t pless_sample(const SampleArgs& a0, float* stats, float* thr, hipStrea
   a.npmax = a.nchunks;
   a.row_thr = thr;
   hipLaunchKernelGGL(pless_stats_kernel, dim3(a.nchunks, a.R), dim3(256), 0, s, a, cmax, stats + n, stats + 2 * n);
+  if (a.sub_sums && a.nchunks * 16 > 1024) return hipErrorInvalidValue;
   hipLaunchKernelGGL(pless_sum_kernel, dim3(a.nchunks, a.R), dim3(256), 0, s, a, cmax, stats + n, stats + 2 * n, thr);
-  hipLaunchKernelGGL(minp_select_kernel, dim3(a.R), dim3(256), 0, s, a);
+  if (a.sub_sums)
+    hipLaunchKernelGGL(minp_select_sub_kernel, dim3(a.R), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(minp_select_kernel, dim3(a.R), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -81,8 +81,8 @@ def oracle_rows(name, wd, tap, got, forced, seeds, T, p_min, check):
 
 def test_64_row_steps_8192_prefix(rgd, p8192):
     """The benchmarked step: 64 branches over the 8192-position prefix (the
-    64-row GEMM tiles, split-K QKV/O/down, fused SwiGLU, one attention row
-    block of 256 query vectors)."""
+    64-row GEMM tiles, split-K QKV/O/down, fused SwiGLU, two attention row
+    blocks of 128 query vectors)."""
     w = p8192.w
     rows, steps = 64, 2
     forced = synth.forced_history(w, rows, steps, name="forced64")
@@ -96,8 +96,8 @@ def test_64_row_steps_8192_prefix(rgd, p8192):
 @pytest.mark.parametrize("rows,check", [(128, (0, 77, 127)), (256, (0, 129, 255))])
 def test_wide_steps_512_prefix(rgd, p512_wide, rows, check):
     """128- and 256-row steps (the 8-layer workload's gated and ungated
-    batches): 128-row GEMM blocks, two per weight panel at 256 rows, and one
-    or two attention row blocks."""
+    batches): 128-row GEMM blocks, two per weight panel at 256 rows, and four
+    or eight attention row blocks (more than the four passed by value)."""
     w = p512_wide.w
     steps = 2
     forced = synth.forced_history(w, rows, steps, name=f"forced{rows}")
