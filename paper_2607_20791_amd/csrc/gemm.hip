@@ -211,33 +211,55 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
               Y[(long long)m * a.ldy + ncol[j]] = f32_to_bf16(silu(acc[mt][j][i]) * u);
           }
     }
-  } else {  // GEMM_LOGITS: logits plus one maximum per (row, workgroup)
+  } else {  // GEMM_LOGITS: logits plus one maximum (and argmax key) per (row, workgroup)
     float* Y = (float*)a.y;
     __shared__ float red[NW][MT * 16];
+    __shared__ unsigned long long redk[NW][MT * 16];
+    const bool keys = a.tilekey != nullptr;  // uniform
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int m = m0 + mt * 16 + rq + i;
         float v = -INFINITY;
+        unsigned long long kb = 0ull;
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
           const bool ok = m < a.M && ncol[j] < a.N;
           if (ok) Y[(long long)m * a.ldy + ncol[j]] = acc[mt][j][i];
           v = fmaxf(v, ok ? acc[mt][j][i] : -INFINITY);
+          if (ok) {
+            const unsigned long long kj = ((unsigned long long)ordered_u32(acc[mt][j][i]) << 32) |
+                                          (unsigned long long)(0xFFFFFFFFu - uint32_t(ncol[j]));
+            kb = kj > kb ? kj : kb;
+          }
         }
-        v = fmaxf(v, __shfl_xor(v, 1, 64));
-        v = fmaxf(v, __shfl_xor(v, 2, 64));
-        v = fmaxf(v, __shfl_xor(v, 4, 64));
-        v = fmaxf(v, __shfl_xor(v, 8, 64));
-        if (col16 == 0) red[wave][mt * 16 + rq + i] = v;
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) {
+          v = fmaxf(v, __shfl_xor(v, o, 64));
+          if (keys) {
+            const unsigned long long ko = __shfl_xor(kb, o, 64);
+            kb = ko > kb ? ko : kb;
+          }
+        }
+        if (col16 == 0) {
+          red[wave][mt * 16 + rq + i] = v;
+          redk[wave][mt * 16 + rq + i] = kb;
+        }
       }
     __syncthreads();
     for (int t = threadIdx.x; t < MT * 16; t += NTH) {
       float v = red[0][t];
-      for (int w = 1; w < NW; ++w) v = fmaxf(v, red[w][t]);
+      unsigned long long kb = redk[0][t];
+      for (int w = 1; w < NW; ++w) {
+        v = fmaxf(v, red[w][t]);
+        kb = redk[w][t] > kb ? redk[w][t] : kb;
+      }
       const int m = m0 + t;
-      if (m < a.M) a.tilemax[(long long)m * a.ntiles + gx] = v;
+      if (m < a.M) {
+        a.tilemax[(long long)m * a.ntiles + gx] = v;
+        if (keys) a.tilekey[(long long)m * a.ntiles + gx] = kb;
+      }
     }
   }
 }

@@ -26,6 +26,9 @@ struct GemmArgs {
   void* y; int ldy;       // output (fp32, or T for GEMM_SILU)
   long long split_stride; // elements between split partials
   float* tilemax; int ntiles;  // GEMM_LOGITS: [M][ntiles]
+  // GEMM_LOGITS, optional [M][ntiles]: per workgroup tile the packed argmax
+  // key (ordered value << 32 | ~index: larger value, then lower index, wins)
+  unsigned long long* tilekey;
   int mode;
 };
 
@@ -200,6 +203,14 @@ struct GateArgs {
   // set only when the probe ends (INCOMPAT if it failed, else STOP / MAXLEN)
   int no_early_exit;
   int* failed;                     // [B], cleared by the probe's initialisation
+  // optional: the argmax keys come as [R][ntiles] tile keys from the LM-head
+  // epilogue (best unused); the row's key is their maximum
+  const unsigned long long* tilekeys; int ntiles;
+  // optional: the next step's input row of each row, x = E[t] (fp32 [R][d])
+  // and xn = RMSNorm(x) * gain, for t = probe_tokens[prompt][feed_col] read
+  // after this step's update (what the next step feeds); d % 4 == 0, d <= 4096
+  const void* embed; int embed_bf16; int d; int vocab; int feed_col;
+  const float* gain; float eps; float* x; void* xn;
 };
 hipError_t probe_update(const GateArgs& a, hipStream_t s);
 

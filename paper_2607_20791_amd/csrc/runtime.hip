@@ -118,6 +118,7 @@ struct rgd_model {
   float* down_part = nullptr;
   float* logits = nullptr;
   float* tilemax = nullptr;
+  unsigned long long* tilekey = nullptr;  // [R][ntiles] LM-head argmax keys (bf16 models)
   float* chunk_sums = nullptr;
   float* sub_sums = nullptr;  // [R][nchunks * 16] kept sums of 256-logit sub-chunks
   float* pl_stats = nullptr;  // p-less: chunk maxima, sums of w and w^2 [3][R][nchunks]
@@ -396,6 +397,7 @@ int lm_head(rgd_model* m, const void* x, int ldx, int R, float* logits, hipStrea
   g.y = logits;
   g.ldy = m->cfg.vocab;
   g.tilemax = m->tilemax;
+  g.tilekey = m->bf16 ? m->tilekey : nullptr;
   g.ntiles = m->ntiles;
   g.mode = GEMM_LOGITS;
   TimeScope ts(m, RGD_TIMER_LM_HEAD, s);
@@ -737,6 +739,7 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
   A(&m->down_part, PR * d * 4);
   A(&m->logits, (size_t)R * cfg->vocab * 4);
   A(&m->tilemax, (size_t)R * m->ntiles * 4);
+  A(&m->tilekey, (size_t)R * m->ntiles * 8);
   A(&m->chunk_sums, (size_t)R * m->nchunks * 4);
   A(&m->sub_sums, (size_t)R * m->nchunks * 16 * 4);
   A(&m->pl_stats, (size_t)3 * R * m->nchunks * 4);
@@ -1080,16 +1083,43 @@ int probe_impl(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_tab
   sa.soft_steps = c;
   // one probe step on logits z (row r of the alive set at z + r * V): soft
   // for tokens 1..c when a soft gate is asked for, hard otherwise
-  auto step = [&](const float* z, int R, int token) -> int {
+  // The hard steps of a bf16 model take the argmax from the LM head's tile
+  // keys (no pass over the logits; token 1 comes from the prompt logits) and
+  // write the next step's input rows (embedding + first RMSNorm) for the
+  // current row set: `embedded` tells the next forward pass whether they are
+  // there (a soft step, or a change of the row set, leaves them out).
+  const int dm = m->cfg.d_model;
+  const bool fuse = m->bf16 && dm % 4 == 0 && dm <= 4096;
+  bool embedded = false;
+  auto step = [&](const float* z, int R, int token, bool lm_keys) -> int {
     ga.R = R;
+    embedded = false;
     if (topk > 0 && token <= c) {
       sa.g = ga;
       sa.z = z;
       sa.ldz = V;
       HIP_OK(probe_update_soft(sa, s));
     } else {
-      HIP_OK(argmax_rows(z, V, R, V, m->best, s));
-      HIP_OK(probe_update(ga, s));
+      GateArgs g2 = ga;
+      if (lm_keys && fuse) {
+        g2.tilekeys = m->tilekey;
+        g2.ntiles = m->ntiles;
+      } else {
+        HIP_OK(argmax_rows(z, V, R, V, m->best, s));
+      }
+      if (fuse && token < k) {
+        g2.embed = m->embed;
+        g2.embed_bf16 = 1;
+        g2.d = dm;
+        g2.vocab = V;
+        g2.feed_col = token - 1;
+        g2.gain = (const float*)m->layers[0].attn_norm;
+        g2.eps = m->cfg.rms_eps;
+        g2.x = m->x;
+        g2.xn = m->xn;
+        embedded = true;
+      }
+      HIP_OK(probe_update(g2, s));
     }
     return RGD_OK;
   };
@@ -1123,7 +1153,7 @@ int probe_impl(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_tab
   std::vector<int> pages;
   RGD_TRY(set_rows(h, pages));
   // token 1 from the prompt logits (rows are prompts 0..B-1 here)
-  RGD_TRY(step(last_logits, B, 1));
+  RGD_TRY(step(last_logits, B, 1, false));
   for (int j = 2;; ++j) {
     const int done_tokens = j - 1;
     const bool check = done_tokens <= c || done_tokens % c == 0 || done_tokens >= k;
@@ -1137,15 +1167,16 @@ int probe_impl(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_tab
       if (still.size() != alive.size()) {
         alive.swap(still);
         RGD_TRY(set_rows(h, pages));
+        embedded = false;  // the rows were renumbered
       }
     }
     if (j > k) break;  // cannot happen: every prompt is decided after k tokens
     const int R = (int)alive.size();
     // row r feeds token j-1 of its prompt's probe (probe_tokens[prompt[r]][j-2])
     Rows rows = device_rows(m, kv, R, j - 2, false);
-    RGD_TRY(forward_rows(m, kv, rows, h, probe_tokens + (j - 2), k, s, false, nullptr, m->d_prompt));
+    RGD_TRY(forward_rows(m, kv, rows, h, probe_tokens + (j - 2), k, s, embedded, nullptr, m->d_prompt));
     RGD_TRY(lm_head(m, m->xn, m->cfg.d_model, R, m->logits, s));
-    RGD_TRY(step(m->logits, R, j));
+    RGD_TRY(step(m->logits, R, j, true));
   }
   HIP_OK(hipStreamSynchronize(s));
   release.ok = true;

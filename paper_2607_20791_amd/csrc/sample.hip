@@ -706,13 +706,30 @@ __global__ __launch_bounds__(256) void minp_multi_kernel(SampleArgs a, unsigned 
 }
 
 // ------------------------------------------------------------------ gate ----
-__global__ __launch_bounds__(64) void probe_update_kernel(GateArgs a) {
-  const int r = blockIdx.x;
+// One probe step of row r (prompt b): the greedy token (the argmax key of the
+// row, from the argmax pass or the LM head's tile keys), the compatibility of
+// the probe extended by it against every table entry, the event.  Wave 0 does
+// the update; with a.embed all four waves then write the next step's input
+// row (embedding of the token the next step feeds, RMSNorm).
+// Returns the token appended (every lane of the wave), or -1 when the row's
+// prompt was already decided.
+RGD_DEV int probe_update_row(const GateArgs& a, int r) {
   const int b = a.row_prompt[r];
-  const unsigned long long key = a.best[r];
-  __syncthreads();
-  if (threadIdx.x == 0) a.best_reset[r] = 0ull;
-  if (a.event[b] != -1) return;
+  unsigned long long key;
+  if (a.tilekeys) {
+    key = 0ull;
+    const unsigned long long* tk = a.tilekeys + (long long)r * a.ntiles;
+    for (int i = threadIdx.x; i < a.ntiles; i += 64) key = tk[i] > key ? tk[i] : key;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const unsigned long long ko = __shfl_xor(key, o, 64);
+      key = ko > key ? ko : key;
+    }
+  } else {
+    key = a.best[r];
+    if (threadIdx.x == 0) a.best_reset[r] = 0ull;
+  }
+  if (a.event[b] != -1) return -1;
   const int tok = int(0xFFFFFFFFu - uint32_t(key & 0xFFFFFFFFull));
   const int j = a.probe_len[b];
   const int* q = a.probe_tokens + (long long)b * a.k;
@@ -734,6 +751,27 @@ __global__ __launch_bounds__(64) void probe_update_kernel(GateArgs a) {
       a.event[b] = !compat ? 0 : stop ? 1 : full ? 2 : -1;
     }
   }
+  return tok;
+}
+
+__global__ __launch_bounds__(256) void probe_update_kernel(GateArgs a) {
+  __shared__ int sh_tok;
+  const int r = blockIdx.x;
+  if (threadIdx.x < 64) {
+    const int t = probe_update_row(a, r);
+    if (threadIdx.x == 0) sh_tok = t;
+  }
+  if (!a.embed) return;
+  __syncthreads();
+  // the token the next step feeds: the one just appended (column feed_col),
+  // or for a prompt decided earlier what its probe holds there
+  const int b = a.row_prompt[r];
+  const int tok = sh_tok >= 0 ? sh_tok : a.probe_tokens[(long long)b * a.k + a.feed_col];
+  float* x = a.x + (long long)r * a.d;
+  if (a.embed_bf16)
+    embed_norm_row(tok, (const bf16_t*)a.embed, a.d, a.vocab, a.gain, a.eps, x, (bf16_t*)a.xn + (long long)r * a.d);
+  else
+    embed_norm_row(tok, (const float*)a.embed, a.d, a.vocab, a.gain, a.eps, x, (float*)a.xn + (long long)r * a.d);
 }
 
 __global__ void gate_decide_kernel(const int* event, int B, int* decision, int* n_miss, int* miss_idx) {
@@ -831,7 +869,8 @@ hipError_t minp_multi_draw(const SampleArgs& a, int draws, unsigned int stream0,
 
 hipError_t probe_update(const GateArgs& a, hipStream_t s) {
   if (a.R <= 0) return hipSuccess;
-  hipLaunchKernelGGL(probe_update_kernel, dim3(a.R), dim3(64), 0, s, a);
+  if (a.embed && (a.d % 4 || a.d > 4096)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(probe_update_kernel, dim3(a.R), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
