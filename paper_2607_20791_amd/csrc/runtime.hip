@@ -138,6 +138,7 @@ struct rgd_model {
   int* h_stage = nullptr;  // pinned staging for uploads
   size_t stage_ints = 0;
   hipEvent_t stage_done = nullptr;
+  hipEvent_t poll_done = nullptr;  // a probe poll's copy of the events reached host memory
   int* h_events = nullptr;  // pinned host copies: probe events, gate results [2 * max_rows + 1]
   int* d_gate = nullptr;    // gate results on the device: decision [R], n_miss, miss list [R]
   // in-situ timing: event pairs per timed unit
@@ -160,6 +161,7 @@ struct rgd_model {
     if (h_stage) (void)hipHostFree(h_stage);
     if (h_events) (void)hipHostFree(h_events);
     if (stage_done) (void)hipEventDestroy(stage_done);
+    if (poll_done) (void)hipEventDestroy(poll_done);
   }
   template <typename P>
   int alloc(P** out, size_t bytes) {
@@ -803,6 +805,7 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
   if (hipHostMalloc((void**)&m->h_stage, m->stage_ints * sizeof(int), hipHostMallocDefault) != hipSuccess ||
       hipHostMalloc((void**)&m->h_events, (size_t)(2 * R + 1) * sizeof(int), hipHostMallocDefault) != hipSuccess ||
       hipEventCreateWithFlags(&m->stage_done, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&m->poll_done, hipEventDisableTiming) != hipSuccess ||
       hipEventRecord(m->stage_done, nullptr) != hipSuccess) {
     delete m;
     return fail(RGD_E_HIP, "pinned staging allocation failed");
@@ -1154,21 +1157,43 @@ int probe_impl(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_tab
   RGD_TRY(set_rows(h, pages));
   // token 1 from the prompt logits (rows are prompts 0..B-1 here)
   RGD_TRY(step(last_logits, B, 1, false));
+  // Polls: after each of the first c tokens and after token k the host waits
+  // for the events (the first c checks of Algorithm 1, and the end).  The
+  // checks every c tokens in between are pipelined: the copy of the events is
+  // enqueued after token j-1 and read once the next step has been launched,
+  // so the GPU never waits for the host; a probe that ended there has decoded
+  // one more token, which leaves its events and tokens as they were (decided
+  // rows are not updated) and only costs that step's time.
+  bool done = false;
+  auto apply_poll = [&]() -> int {
+    std::vector<int> still;
+    for (int b : alive)
+      if (pinned_ev[b] == -1) still.push_back(b);
+    if (still.empty()) {
+      done = true;
+      return RGD_OK;
+    }
+    if (still.size() != alive.size()) {
+      alive.swap(still);
+      RGD_TRY(set_rows(h, pages));
+      embedded = false;  // the rows were renumbered
+    }
+    return RGD_OK;
+  };
   for (int j = 2;; ++j) {
     const int done_tokens = j - 1;
-    const bool check = done_tokens <= c || done_tokens % c == 0 || done_tokens >= k;
-    if (check) {
+    const bool first = done_tokens <= c, last = done_tokens >= k;
+    const bool check = first || done_tokens % c == 0 || last;
+    const bool pipelined = check && !first && !last;
+    if (check && !pipelined) {
       HIP_OK(hipMemcpyAsync(pinned_ev, event, (size_t)B * 4, hipMemcpyDeviceToHost, s));
       HIP_OK(hipStreamSynchronize(s));
-      std::vector<int> still;
-      for (int b : alive)
-        if (pinned_ev[b] == -1) still.push_back(b);
-      if (still.empty()) break;
-      if (still.size() != alive.size()) {
-        alive.swap(still);
-        RGD_TRY(set_rows(h, pages));
-        embedded = false;  // the rows were renumbered
-      }
+      RGD_TRY(apply_poll());
+      if (done) break;
+    }
+    if (pipelined) {
+      HIP_OK(hipMemcpyAsync(pinned_ev, event, (size_t)B * 4, hipMemcpyDeviceToHost, s));
+      HIP_OK(hipEventRecord(m->poll_done, s));
     }
     if (j > k) break;  // cannot happen: every prompt is decided after k tokens
     const int R = (int)alive.size();
@@ -1177,6 +1202,11 @@ int probe_impl(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_tab
     RGD_TRY(forward_rows(m, kv, rows, h, probe_tokens + (j - 2), k, s, embedded, nullptr, m->d_prompt));
     RGD_TRY(lm_head(m, m->xn, m->cfg.d_model, R, m->logits, s));
     RGD_TRY(step(m->logits, R, j, true));
+    if (pipelined) {
+      HIP_OK(hipEventSynchronize(m->poll_done));
+      RGD_TRY(apply_poll());
+      if (done) break;
+    }
   }
   HIP_OK(hipStreamSynchronize(s));
   release.ok = true;
