@@ -16,6 +16,7 @@
 //
 // fp32 path: vector kernels of the same structure (prefix splits, then tail
 // plus merge).
+#include <algorithm>
 #include <type_traits>
 
 #include "kernels.hpp"
@@ -83,11 +84,8 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
   constexpr int D = 128, TP = 64, NT = NW * 64, NB = 3;
   static_assert(NW * NQ * 16 == RGD_ATTN_QV, "a workgroup covers RGD_ATTN_QV query vectors");
   const int s = blockIdx.x, g = blockIdx.y;
-  // the first row blocks come with the arguments (scalar loads, no dependent
-  // memory round trip); further ones from the row-block table
-  const int z = blockIdx.z;
-  const int4 rb = z == 0 ? a.rblk[0] : z == 1 ? a.rblk[1] : z == 2 ? a.rblk[2] : z == 3 ? a.rblk[3]
-                                                                                      : a.rblocks[z];
+  // the row block comes with the arguments
+  const int4 rb = a.rblk[blockIdx.z];
   const int r0 = rb.x, nr = rb.y, b = rb.z, maxplen = rb.w;
   const int lo = s * a.split_len;
   const int hi = min(lo + a.split_len, maxplen);
@@ -100,18 +98,32 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
   u32x4 qf[NQ][4];
   bool vok[NQ];
   int vrow[NQ], vhead[NQ], vend[NQ];
+  // Q fragments first (unconditional loads: a query vector past the block
+  // reads row r0 and is zeroed), then the visible ends, whose loads then do
+  // not hold up the Q loads
+  int pl[NQ];
 #pragma unroll
   for (int nt = 0; nt < NQ; ++nt) {
     const int v = wave * NQ * 16 + nt * 16 + l16;
     vok[nt] = v < nq;
     vrow[nt] = r0 + (vok[nt] ? v / G : 0);
     vhead[nt] = g * G + (vok[nt] ? v % G : 0);
-    vend[nt] = vok[nt] ? min(prefix_part_end(a.rows.plen[vrow[nt]], a.split_len), hi) : lo;
     const bf16_t* qp = (const bf16_t*)a.q + ((long long)vrow[nt] * a.Hq + vhead[nt]) * D + grp * 8;
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
-      qf[nt][ks] = vok[nt] ? *(const u32x4*)(qp + ks * 32) : u32x4{0u, 0u, 0u, 0u};
+    for (int ks = 0; ks < 4; ++ks) qf[nt][ks] = *(const u32x4*)(qp + ks * 32);
+    pl[nt] = a.rows.plen[vrow[nt]];
   }
+  // the visible ends are formed after the prologue's barrier (their loads are
+  // long back by then; waiting for them here would hold up the first tile)
+  auto set_vend = [&]() {
+#pragma unroll
+    for (int nt = 0; nt < NQ; ++nt) {
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+        if (!vok[nt]) qf[nt][ks] = u32x4{0u, 0u, 0u, 0u};
+      vend[nt] = vok[nt] ? min(prefix_part_end(pl[nt], a.split_len), hi) : lo;
+    }
+  };
   const bool wave_active = (wave * NQ * 16) < nq;
 
   __shared__ __attribute__((aligned(16))) bf16_t k_lds[NB][TP * D];
@@ -145,25 +157,23 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
   constexpr int KSEG = TP * 16 / NT, VSEG = D * (TP / 8) / NT;  // 16-byte segments per thread
   u32x4 kreg[KSEG], vreg[VSEG];
   int vt0 = 0;
-  // A whole tile (all 64 positions inside the split) takes the unpredicated
-  // loads and stores; only a split's ragged last tile is masked (the branch
-  // is uniform over the workgroup).
+  // The loads are unconditional (a predicated load makes the compiler wait
+  // for it where the branches join): K rows past the range read row hi - 1
+  // (their scores are masked), V of the tile's 64-position block is in the
+  // padded cache and is zeroed past the range at the store.
   auto load_tile = [&](int t0) {
     vt0 = t0;
-    const bool whole = t0 + TP <= hi;
     const bf16_t* vblk = vbase + (long long)(t0 / TP) * D * TP;
 #pragma unroll
     for (int i = 0; i < KSEG; ++i) {
       const int seg = threadIdx.x + i * NT;
-      const int pos = t0 + (seg >> 4);
-      const u32x4* src = (const u32x4*)(kbase + (long long)pos * D + (seg & 15) * 8);
-      kreg[i] = (whole || pos < hi) ? *src : u32x4{0u, 0u, 0u, 0u};
+      const int pos = min(t0 + (seg >> 4), hi - 1);
+      kreg[i] = *(const u32x4*)(kbase + (long long)pos * D + (seg & 15) * 8);
     }
 #pragma unroll
     for (int i = 0; i < VSEG; ++i) {
       const int seg = threadIdx.x + i * NT;
-      const u32x4* src = (const u32x4*)(vblk + (seg >> 3) * TP + (seg & 7) * 8);
-      vreg[i] = (whole || t0 + (seg & 7) * 8 < hi) ? *src : u32x4{0u, 0u, 0u, 0u};
+      vreg[i] = *(const u32x4*)(vblk + (seg >> 3) * TP + (seg & 7) * 8);
     }
   };
   auto store_tile = [&](int buf) {
@@ -339,6 +349,7 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
     store_tile(0);
     if (ntile > 1) load_tile(lo + TP);
     __syncthreads();
+    set_vend();
     f32x4 sa[2][NQ], sb[2][NQ];
     if (wave_active) scores(0, 0, sa);
     // tile t uses ring buffer t % NB; the loop is unrolled by NB so that every
@@ -657,14 +668,18 @@ __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t
   const int S = a.splits;
   constexpr int kPrefetch = 32;
   const long long pstep = R * a.Hq * D;
+  // (Loads in this kernel are unconditional, from clamped addresses, and
+  // masked afterwards: a predicated load makes the compiler wait for it where
+  // the branches join, one memory round trip each.)
   uint32_t pre[kPrefetch];  // bf16 pairs
   float pre_lse = -INFINITY;
   if (wave < G) {
     const int head = g * G + wave;
     const bf16_t* po = (const bf16_t*)a.part_o + ((long long)r * a.Hq + head) * D + 2 * lane;
 #pragma unroll
-    for (int k = 0; k < kPrefetch; ++k) pre[k] = k < S ? *(const uint32_t*)(po + k * pstep) : 0u;
-    if (lane < S) pre_lse = a.part_lse[((long long)lane * R + r) * a.Hq + head];
+    for (int k = 0; k < kPrefetch; ++k) pre[k] = *(const uint32_t*)(po + min(k, S - 1) * pstep);
+    const float ls = a.part_lse[((long long)min(lane, S - 1) * R + r) * a.Hq + head];
+    pre_lse = lane < S ? ls : -INFINITY;
   }
 
   u32x4 qf[4];
@@ -672,7 +687,10 @@ __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t
     const bool ok = l16 < G;
     const bf16_t* qp = (const bf16_t*)a.q + ((long long)r * a.Hq + g * G + (ok ? l16 : 0)) * D + grp * 8;
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) qf[ks] = ok ? *(const u32x4*)(qp + ks * 32) : u32x4{0u, 0u, 0u, 0u};
+    for (int ks = 0; ks < 4; ++ks) {
+      const u32x4 x = *(const u32x4*)(qp + ks * 32);
+      qf[ks] = ok ? x : u32x4{0u, 0u, 0u, 0u};
+    }
   }
   float m = -INFINITY, lsum = 0.f;
   f32x4 o[8];
@@ -704,7 +722,7 @@ __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t
                             : (const bf16_t*)a.kv.pool_k +
                                   (((long long)pages[pp / ps] * a.Hkv + g) * ps + pp % ps) * D + grp * 8;
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) ka[e][ks] = ok ? *(const u32x4*)(kr + ks * 32) : u32x4{0u, 0u, 0u, 0u};
+      for (int ks = 0; ks < 4; ++ks) ka[e][ks] = *(const u32x4*)(kr + ks * 32);  // past the end: masked scores
     }
     // this lane's eight positions p0 .. p0+7 lie in one page (ps % 8 == 0) or
     // one 64-position block of the prefix V layout (p0 % 8 == 0)
@@ -717,7 +735,7 @@ __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t
                                   (((long long)pages[pp / ps] * a.Hkv + g) * D + l16) * ps + pp % ps;
       const long long vstep = ov ? 16LL * 64 : 16LL * ps;  // 16 head-dim rows
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt) va[dt] = nv > 0 ? *(const u32x4*)(vr + dt * vstep) : u32x4{0u, 0u, 0u, 0u};
+      for (int dt = 0; dt < 8; ++dt) va[dt] = *(const u32x4*)(vr + dt * vstep);  // past the end: zeroed below
     }
     f32x4 sc[2];
 #pragma unroll
@@ -840,9 +858,18 @@ __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t
 hipError_t attn_prefix_bf16(const AttnArgs& a, hipStream_t s) {
   if (a.D != 128 || a.Hq / a.Hkv > RGD_ATTN_QV || a.split_len % 64 || a.kv.VP % 64) return hipErrorInvalidValue;
   if (a.splits <= 0 || a.nrblocks <= 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_prefix_kernel<RGD_ATTN_NW, RGD_ATTN_QV / 16 / RGD_ATTN_NW>), dim3(a.splits, a.Hkv, a.nrblocks),
-                     dim3(RGD_ATTN_NW * 64), 0, s, a);
-  return hipGetLastError();
+  if (!a.rblocks) return hipErrorInvalidValue;
+  // one launch per kAttnInlineBlocks row blocks
+  for (int c0 = 0; c0 < a.nrblocks; c0 += kAttnInlineBlocks) {
+    AttnArgs b = a;
+    const int n = std::min(kAttnInlineBlocks, a.nrblocks - c0);
+    for (int i = 0; i < n; ++i) b.rblk[i] = a.rblocks[c0 + i];
+    hipLaunchKernelGGL((attn_prefix_kernel<RGD_ATTN_NW, RGD_ATTN_QV / 16 / RGD_ATTN_NW>), dim3(a.splits, a.Hkv, n),
+                       dim3(RGD_ATTN_NW * 64), 0, s, b);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 template <typename T>

@@ -55,7 +55,11 @@ template <int MT, int NT, int NW, int SW, int MODE, int XS>
 __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
   constexpr int NTH = NW * 64, XSEG = MT * 16 * 8 * XS, XPT = (XSEG + NTH - 1) / NTH;
   static_assert(XS % SW == 0 || SW % XS == 0, "ring slots must stay static within an X stage");
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, col16 = lane & 15;
+  // wave index as a scalar: the panel and weight segment it selects are then
+  // scalar too (a per-lane index into the arguments becomes a vector load of
+  // the argument segment and a full memory round trip before the first weight
+  // request)
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), col16 = lane & 15;
   // Workgroups are handed out in linear order (x fastest), round-robin over
   // the chip's 8 XCDs, each with its own L2.  With several row blocks, the
   // work is reordered so that the row blocks of one column group are 8 apart

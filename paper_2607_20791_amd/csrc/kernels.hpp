@@ -117,7 +117,7 @@ hipError_t residual_readout(const float* x, long long row0, long long stride, in
 #ifndef RGD_ATTN_WGS
 #define RGD_ATTN_WGS 128
 #endif
-constexpr int kAttnInlineBlocks = 4;
+constexpr int kAttnInlineBlocks = 64;
 struct AttnArgs {
   const void* q;            // [R][Hq][D]
   Rows rows;
@@ -127,8 +127,11 @@ struct AttnArgs {
   float* part_lse;          // [nparts][R][Hq]
   int nparts;
   // prefix (shared) part
-  const int4* rblocks; int nrblocks;  // (r0, nr, prompt, maxplen) row blocks for the MFMA path
-  int4 rblk[kAttnInlineBlocks];       // rblocks[0..3] passed by value (no dependent load)
+  // (r0, nr, prompt, maxplen) row blocks of the MFMA path: a host array; the
+  // launcher passes them by value, kAttnInlineBlocks per launch (scalar loads
+  // of the arguments, no memory round trip before the first Q load)
+  const int4* rblocks; int nrblocks;
+  int4 rblk[kAttnInlineBlocks];
   int splits; int split_len;          // prefix splits (part index 0..splits-1)
   // tail part
   int tail_len;             // visible tail positions (decode), 0 for prefill

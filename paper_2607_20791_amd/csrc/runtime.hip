@@ -134,7 +134,6 @@ struct rgd_model {
   int* d_prompt = nullptr;
   int* d_base = nullptr;
   int* d_plen = nullptr;
-  int4* d_rblocks = nullptr;
   int* h_stage = nullptr;  // pinned staging for uploads
   size_t stage_ints = 0;
   hipEvent_t stage_done = nullptr;
@@ -290,8 +289,7 @@ int upload_rows(rgd_model* m, const HostRows& h, hipStream_t s) {
   return upload(m,
                 {{m->d_prompt, h.prompt.data(), R},
                  {m->d_base, h.base.data(), R},
-                 {m->d_plen, h.plen.data(), R},
-                 {(int*)m->d_rblocks, (const int*)h.blocks.data(), h.blocks.size() * 4}},
+                 {m->d_plen, h.plen.data(), R}},
                 s);
 }
 
@@ -337,9 +335,8 @@ int run_attention(rgd_model* m, const KVLayout& kvl, const Rows& rows, const Hos
   a.D = c.head_dim;
   a.part_o = m->part_o;
   a.part_lse = m->part_lse;
-  a.rblocks = m->d_rblocks;
+  a.rblocks = h.blocks.data();
   a.nrblocks = (int)h.blocks.size();
-  for (int i = 0; i < kAttnInlineBlocks && i < (int)h.blocks.size(); ++i) a.rblk[i] = h.blocks[i];
   a.tail_len = tail_len;
   a.tail_chunk = kTailChunk;
   a.tail_chunks = 0;  // tails are attended inside the merge kernel
@@ -757,7 +754,6 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
   A(&m->d_prompt, (size_t)R * 4);
   A(&m->d_base, (size_t)R * 4);
   A(&m->d_plen, (size_t)R * 4);
-  A(&m->d_rblocks, (size_t)R * 16);
   // RoPE rotations: angle pos * theta^(-2j/D) in fp64, rounded to fp32 once
   const int half = D / 2;
   const size_t ncs = ((size_t)cfg->max_pos + 1) * half;
@@ -1148,7 +1144,6 @@ int probe_impl(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_tab
                   {{m->d_prompt, h.prompt.data(), h.prompt.size()},
                    {m->d_base, h.base.data(), h.base.size()},
                    {m->d_plen, h.plen.data(), h.plen.size()},
-                   {(int*)m->d_rblocks, (const int*)h.blocks.data(), h.blocks.size() * 4},
                    {kv->d_pages, pages.data(), pages.size()}},
                   s);
   };
@@ -1346,7 +1341,6 @@ int32_t sample_continuations(rgd_model* m, rgd_kv* kv, const float* last_logits,
                  {{m->d_prompt, h.prompt.data(), (size_t)R},
                   {m->d_base, h.base.data(), (size_t)R},
                   {m->d_plen, h.plen.data(), (size_t)R},
-                  {(int*)m->d_rblocks, (const int*)h.blocks.data(), h.blocks.size() * 4},
                   {kv->d_pages, pages.data(), pages.size()},
                   {m->row_map, map.data(), (size_t)R}},
                  s));

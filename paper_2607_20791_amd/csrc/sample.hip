@@ -128,12 +128,15 @@ RGD_DEV float row_max_from_partials(const float* pmax, int npmax, int r, float* 
   const float* p = pmax + (long long)r * npmax;
   float mx = -INFINITY;
   const int n4 = npmax & ~3;
-  if ((((uintptr_t)p) & 15) == 0) {
-    for (int i = threadIdx.x * 4; i < n4; i += 1024) {
-      const float4 v = *(const float4*)(p + i);
-      mx = fmaxf(mx, fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w)));
-    }
-    for (int i = n4 + threadIdx.x; i < npmax; i += 256) mx = fmaxf(mx, p[i]);
+  if ((((uintptr_t)p) & 15) == 0 && npmax <= 1024 && n4 >= 4) {
+    // one float4 and one scalar per thread, loaded unconditionally from
+    // clamped indices and masked afterwards (a predicated load makes the
+    // compiler wait for it where the branches join)
+    const int i = threadIdx.x * 4, j = n4 + threadIdx.x;
+    const float4 v = *(const float4*)(p + min(i, n4 - 4));
+    const float t = p[min(j, npmax - 1)];
+    if (i < n4) mx = fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w));
+    if (j < npmax) mx = fmaxf(mx, t);
   } else {
     for (int i = threadIdx.x; i < npmax; i += 256) mx = fmaxf(mx, p[i]);
   }
@@ -573,15 +576,22 @@ __global__ __launch_bounds__(256) void minp_select_sub_kernel(SampleArgs a) {
     const int nsub = a.nchunks * 16;
     const int SP = (nsub + 63) / 64;
     const float* ss = a.sub_sums + (long long)r * nsub;
+    // Every load is issued unconditionally from a clamped index and its
+    // value is used on every path: a load whose value is only used under a
+    // condition is sunk into a branch by the compiler, which then waits for
+    // it where the branches join, one memory round trip per load.
     float loc[kMaxSP];
 #pragma unroll
     for (int i = 0; i < kMaxSP; ++i) {
       const int j = lane * SP + i;
-      loc[i] = (i < SP && j < nsub) ? ss[j] : 0.f;
+      // sub-chunk sums are finite and non-negative, so a 0/1 factor masks them
+      loc[i] = ss[min(j, nsub - 1)] * ((i < SP && j < nsub) ? 1.f : 0.f);
     }
     const float* pm = a.pmax + (long long)r * a.npmax;
     float mx = -INFINITY;
-    for (int i = lane; i < a.npmax; i += 64) mx = fmaxf(mx, pm[i]);
+#pragma unroll
+    for (int i = 0; i < 16; ++i)  // npmax <= 1024 (checked by the launcher)
+      mx = fmaxf(mx, pm[min(lane + 64 * i, a.npmax - 1)]);  // a repeated entry leaves the maximum unchanged
     const float u = philox_uniform(a.seeds[r], a.ctr, a.stream);
     const float thr = a.row_thr ? a.row_thr[r] : a.p_min;
     mx = wave_max(mx);
@@ -719,7 +729,15 @@ RGD_DEV int probe_update_row(const GateArgs& a, int r) {
   if (a.tilekeys) {
     key = 0ull;
     const unsigned long long* tk = a.tilekeys + (long long)r * a.ntiles;
-    for (int i = threadIdx.x; i < a.ntiles; i += 64) key = tk[i] > key ? tk[i] : key;
+    // four unconditional loads per lane and round (clamped indices, masked)
+    for (int i0 = 0; i0 < a.ntiles; i0 += 256) {
+      unsigned long long v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = tk[min(i0 + (int)threadIdx.x + 64 * u, a.ntiles - 1)];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (i0 + (int)threadIdx.x + 64 * u < a.ntiles) key = v[u] > key ? v[u] : key;
+    }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
       const unsigned long long ko = __shfl_xor(key, o, 64);
@@ -816,7 +834,7 @@ hipError_t minp_sample(const SampleArgs& a, hipStream_t s) {
   if (a.chunk % 1024 || a.chunk > 4096 || a.V % 4 || a.nchunks > 256 ||
       a.nchunks * a.chunk < a.V || !(a.T > 0.f))
     return hipErrorInvalidValue;
-  if (a.sub_sums && a.nchunks * 16 > 1024) return hipErrorInvalidValue;
+  if (a.sub_sums && (a.nchunks * 16 > 1024 || a.npmax > 1024)) return hipErrorInvalidValue;
   hipLaunchKernelGGL(minp_sum_kernel, dim3(a.nchunks, a.R), dim3(256), 0, s, a);
   if (a.sub_sums)
     hipLaunchKernelGGL(minp_select_sub_kernel, dim3(a.R), dim3(256), 0, s, a);
@@ -852,7 +870,7 @@ hipError_t pless_sample(const SampleArgs& a0, float* stats, float* thr, hipStrea
   a.npmax = a.nchunks;
   a.row_thr = thr;
   hipLaunchKernelGGL(pless_stats_kernel, dim3(a.nchunks, a.R), dim3(256), 0, s, a, cmax, stats + n, stats + 2 * n);
-  if (a.sub_sums && a.nchunks * 16 > 1024) return hipErrorInvalidValue;
+  if (a.sub_sums && (a.nchunks * 16 > 1024 || a.nchunks > 1024)) return hipErrorInvalidValue;
   hipLaunchKernelGGL(pless_sum_kernel, dim3(a.nchunks, a.R), dim3(256), 0, s, a, cmax, stats + n, stats + 2 * n, thr);
   if (a.sub_sums)
     hipLaunchKernelGGL(minp_select_sub_kernel, dim3(a.R), dim3(256), 0, s, a);
