@@ -662,6 +662,20 @@ __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t
   __shared__ float w_m[4][16], w_l[4][16];
   __shared__ __attribute__((aligned(16))) float w_o[4][16][D + 4];  // [wave][query][dim]
 
+  // First requests: the row's visible prefix length and its first 64 tail
+  // page numbers (lane i holds page i), so that tile addresses need no
+  // further dependent load.  Without tail pages a valid int array stands in.
+  const int n = a.tail_len;
+  const int* prow = n > 0 ? a.rows.pages + (long long)r * a.rows.max_pages : a.rows.plen;
+  const int plen = a.rows.plen[r];
+  const int pg_reg = prow[n > 0 ? min(lane, a.rows.max_pages - 1) : 0];
+  const int ps_ = a.kv.page_size;
+  const bool pg_in_regs = (n + ps_ - 1) / ps_ <= 64;  // uniform
+  auto page_at = [&](int pi) -> int {
+    return pg_in_regs ? __shfl(pg_reg, pi, 64) : prow[min(pi, a.rows.max_pages - 1)];
+  };
+  const int prompt = a.rows.prompt[r];
+
   // The prefix-split partials and log-sum-exps do not depend on the tail:
   // request those of this wave's first head now so their latency overlaps the
   // tail attention (splits beyond kPrefetch are loaded in the merge).
@@ -671,10 +685,11 @@ __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t
   // (Loads in this kernel are unconditional, from clamped addresses, and
   // masked afterwards: a predicated load makes the compiler wait for it where
   // the branches join, one memory round trip each.)
+  // (a wave past the G heads loads head G-1's and does not use them)
   uint32_t pre[kPrefetch];  // bf16 pairs
-  float pre_lse = -INFINITY;
-  if (wave < G) {
-    const int head = g * G + wave;
+  float pre_lse;
+  {
+    const int head = g * G + min(wave, G - 1);
     const bf16_t* po = (const bf16_t*)a.part_o + ((long long)r * a.Hq + head) * D + 2 * lane;
 #pragma unroll
     for (int k = 0; k < kPrefetch; ++k) pre[k] = *(const uint32_t*)(po + min(k, S - 1) * pstep);
@@ -700,43 +715,47 @@ __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t
   // (fewer than 64 past a split boundary, read in place from the shared
   // prefix), then its paged tail; 32-position tiles of either, dealt to the
   // four waves in turn
-  const int n = a.tail_len;
-  const int* pages = n > 0 ? a.rows.pages + (long long)r * a.rows.max_pages : nullptr;
-  const int plen = a.rows.plen[r];
   const int pe = prefix_part_end(plen, a.split_len);
   const int n_ovt = (plen - pe + TT - 1) / TT, n_all = n_ovt + (n + TT - 1) / TT;
-  const long long bg = (long long)a.rows.prompt[r] * a.Hkv + g;
+  const long long bg = (long long)prompt * a.Hkv + g;
   const bf16_t* pk = (const bf16_t*)a.kv.prefix_k + bg * a.kv.P * D;
   const bf16_t* pv = (const bf16_t*)a.kv.prefix_v + bg * a.kv.VP * D;
   for (int vt = wave; vt < n_all; vt += 4) {
     const bool ov = vt < n_ovt;
     const int tb = ov ? pe + vt * TT : (vt - n_ovt) * TT;  // first position of the tile
     const int lim = ov ? plen : n;                          // positions < lim exist
-    u32x4 ka[2][4], va[8];
+    // every address of the tile first (page numbers come from registers),
+    // then all its loads back to back
+    int kp[2];
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
       const int pos = tb + k_gather_row(0, e, l16);
-      const bool ok = pos < lim;
-      const int pp = ok ? pos : tb;
-      const bf16_t* kr = ov ? pk + (long long)pp * D + grp * 8
-                            : (const bf16_t*)a.kv.pool_k +
-                                  (((long long)pages[pp / ps] * a.Hkv + g) * ps + pp % ps) * D + grp * 8;
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) ka[e][ks] = *(const u32x4*)(kr + ks * 32);  // past the end: masked scores
+      kp[e] = pos < lim ? pos : tb;
     }
     // this lane's eight positions p0 .. p0+7 lie in one page (ps % 8 == 0) or
     // one 64-position block of the prefix V layout (p0 % 8 == 0)
     const int p0 = tb + grp * 8;
     const int nv = lim - p0;
-    {
-      const int pp = nv > 0 ? p0 : tb;
-      const bf16_t* vr = ov ? pv + ((long long)(pp / 64) * D + l16) * 64 + pp % 64
-                            : (const bf16_t*)a.kv.pool_v +
-                                  (((long long)pages[pp / ps] * a.Hkv + g) * D + l16) * ps + pp % ps;
-      const long long vstep = ov ? 16LL * 64 : 16LL * ps;  // 16 head-dim rows
+    const int vp = nv > 0 ? p0 : tb;
+    const int kpg0 = page_at(ov ? 0 : kp[0] / ps), kpg1 = page_at(ov ? 0 : kp[1] / ps);
+    const int vpg = page_at(ov ? 0 : vp / ps);
+    const bf16_t* kr[2];
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt) va[dt] = *(const u32x4*)(vr + dt * vstep);  // past the end: zeroed below
+    for (int e = 0; e < 2; ++e) {
+      const int pg = e ? kpg1 : kpg0;
+      kr[e] = ov ? pk + (long long)kp[e] * D + grp * 8
+                 : (const bf16_t*)a.kv.pool_k + (((long long)pg * a.Hkv + g) * ps + kp[e] % ps) * D + grp * 8;
     }
+    const bf16_t* vr = ov ? pv + ((long long)(vp / 64) * D + l16) * 64 + vp % 64
+                          : (const bf16_t*)a.kv.pool_v + (((long long)vpg * a.Hkv + g) * D + l16) * ps + vp % ps;
+    const long long vstep = ov ? 16LL * 64 : 16LL * ps;  // 16 head-dim rows
+    u32x4 ka[2][4], va[8];
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) ka[e][ks] = *(const u32x4*)(kr[e] + ks * 32);  // past the end: masked scores
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) va[dt] = *(const u32x4*)(vr + dt * vstep);  // past the end: zeroed below
     f32x4 sc[2];
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
