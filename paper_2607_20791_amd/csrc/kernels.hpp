@@ -32,9 +32,12 @@ struct GemmArgs {
   int mode;
 };
 
-// bf16 weights are used in the packed panel layout (see gemm.hip).
-hipError_t pack_panels(const void* w, int N, int K, void* out, hipStream_t s);
-size_t packed_elems(int N, int K);
+// bf16 weights are used in the packed panel layout (see gemm.hip); the LM
+// head's panels are interleaved step by step in groups of kHeadGroup (the
+// panels one wave of its GEMM owns), the other matrices' are not (group 1).
+constexpr int kHeadGroup = 4;
+hipError_t pack_panels(const void* w, int N, int K, int group, void* out, hipStream_t s);
+size_t packed_elems(int N, int K, int group);
 int gemm_groups(int mode, int N);   // workgroups along N for a mode
 hipError_t gemm_bf16(const GemmArgs& a, hipStream_t s);
 hipError_t gemm_f32(const GemmArgs& a, hipStream_t s);

@@ -773,10 +773,10 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
   }
   // bf16: repack every matrix into the GEMM panel layout
   if (rc == RGD_OK && m->bf16) {
-    auto pack = [&](const void* src, int N, int K, void** dst) {
+    auto pack = [&](const void* src, int N, int K, void** dst, int group = 1) {
       if (rc != RGD_OK) return;
-      rc = m->alloc(dst, packed_elems(N, K) * 2);
-      if (rc == RGD_OK && pack_panels(src, N, K, *dst, nullptr) != hipSuccess)
+      rc = m->alloc(dst, packed_elems(N, K, group) * 2);
+      if (rc == RGD_OK && pack_panels(src, N, K, group, *dst, nullptr) != hipSuccess)
         rc = fail(RGD_E_HIP, "weight packing failed");
     };
     m->packed.resize(cfg->n_layers);
@@ -791,7 +791,7 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
       pack(L.w_up, cfg->ffn_dim, d, &P.w_up);
       pack(L.w_down, d, cfg->ffn_dim, &P.w_down);
     }
-    pack(m->lm_head, cfg->vocab, d, &m->lm_head_packed);
+    pack(m->lm_head, cfg->vocab, d, &m->lm_head_packed, kHeadGroup);
   }
   if (rc != RGD_OK) {
     delete m;
