@@ -2,6 +2,7 @@
 // per-row tails, the decode step, and the probe, gate and sampling loops of
 // refusal-gated decoding (Algorithm 1).
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -138,6 +139,7 @@ struct rgd_model {
   size_t stage_ints = 0;
   hipEvent_t stage_done = nullptr;
   hipEvent_t poll_done = nullptr;  // a probe poll's copy of the events reached host memory
+  hipEvent_t sync_done = nullptr;  // marks the end of the queued work for spin_sync
   int* h_events = nullptr;  // pinned host copies: probe events, gate results [2 * max_rows + 1]
   int* d_gate = nullptr;    // gate results on the device: decision [R], n_miss, miss list [R]
   // in-situ timing: event pairs per timed unit
@@ -161,6 +163,7 @@ struct rgd_model {
     if (h_events) (void)hipHostFree(h_events);
     if (stage_done) (void)hipEventDestroy(stage_done);
     if (poll_done) (void)hipEventDestroy(poll_done);
+    if (sync_done) (void)hipEventDestroy(sync_done);
   }
   template <typename P>
   int alloc(P** out, size_t bytes) {
@@ -208,6 +211,26 @@ struct rgd_kv {
 };
 
 namespace {
+
+// ------------------------------------------------------------- host waits --
+// Waits for an event by polling it from this thread.  A blocking wait wakes
+// the host some tens of microseconds after the GPU is done, and on the probe's
+// polls (the host reads the events, then launches the next step) that time is
+// GPU idle time.  Falls back to a blocking wait after a second.
+hipError_t spin_wait(hipEvent_t ev) {
+  const auto t0 = std::chrono::steady_clock::now();
+  for (;;) {
+    const hipError_t e = hipEventQuery(ev);
+    if (e != hipErrorNotReady) return e;
+    if (std::chrono::steady_clock::now() - t0 > std::chrono::seconds(1)) return hipEventSynchronize(ev);
+  }
+}
+
+// everything queued on s so far is done
+hipError_t spin_sync(rgd_model* m, hipStream_t s) {
+  const hipError_t e = hipEventRecord(m->sync_done, s);
+  return e != hipSuccess ? e : spin_wait(m->sync_done);
+}
 
 // ------------------------------------------------------------ timing hooks --
 constexpr int kTimerPairs = 8192;  // timed launches kept per unit between reads
@@ -802,6 +825,7 @@ int32_t rgd_model_create(const rgd_model_config* cfg, const rgd_weights* w, int3
       hipHostMalloc((void**)&m->h_events, (size_t)(2 * R + 1) * sizeof(int), hipHostMallocDefault) != hipSuccess ||
       hipEventCreateWithFlags(&m->stage_done, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&m->poll_done, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&m->sync_done, hipEventDisableTiming) != hipSuccess ||
       hipEventRecord(m->stage_done, nullptr) != hipSuccess) {
     delete m;
     return fail(RGD_E_HIP, "pinned staging allocation failed");
@@ -1182,7 +1206,7 @@ int probe_impl(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_tab
     const bool pipelined = check && !first && !last;
     if (check && !pipelined) {
       HIP_OK(hipMemcpyAsync(pinned_ev, event, (size_t)B * 4, hipMemcpyDeviceToHost, s));
-      HIP_OK(hipStreamSynchronize(s));
+      HIP_OK(spin_sync(m, s));
       RGD_TRY(apply_poll());
       if (done) break;
     }
@@ -1198,12 +1222,12 @@ int probe_impl(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_tab
     RGD_TRY(lm_head(m, m->xn, m->cfg.d_model, R, m->logits, s));
     RGD_TRY(step(m->logits, R, j, true));
     if (pipelined) {
-      HIP_OK(hipEventSynchronize(m->poll_done));
+      HIP_OK(spin_wait(m->poll_done));
       RGD_TRY(apply_poll());
       if (done) break;
     }
   }
-  HIP_OK(hipStreamSynchronize(s));
+  HIP_OK(spin_sync(m, s));
   release.ok = true;
   return RGD_OK;
 }
@@ -1267,7 +1291,7 @@ int32_t rgd_gate(rgd_kv* kv, const int32_t* event, int32_t B, int32_t* decision_
   int* d_miss = d_nmiss + 1;
   HIP_OK(gate_decide(event, B, d_dec, d_nmiss, d_miss, s));
   HIP_OK(hipMemcpyAsync(m->h_events, d_dec, (2 * (size_t)B + 1) * 4, hipMemcpyDeviceToHost, s));
-  HIP_OK(hipStreamSynchronize(s));
+  HIP_OK(spin_sync(m, s));
   const int nm = m->h_events[B];
   std::memcpy(decision_host, m->h_events, (size_t)B * 4);
   *n_miss_host = nm;
