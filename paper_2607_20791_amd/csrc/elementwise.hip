@@ -67,7 +67,12 @@ __global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(float* x
 // One workgroup per (row, group of 8 heads of the fused q|k|v output).  The
 // rotation of position pos, pair j is (cos, sin) = rope_cs[pos][j] (a table
 // computed once on the host in fp64).
-template <typename T>
+// NP >= nparts: the loads of all NP split partials (clamped to the last one,
+// masked by a 0/1 factor) and of the rotation are issued before any of them is
+// used, so the kernel waits for memory once (a partial or a table load used
+// only under a condition is moved into a branch by the compiler, which then
+// waits for it where the branches join, one memory round trip each).
+template <typename T, int NP>
 __global__ __launch_bounds__(1024) void qkv_rope_kernel(const float* parts, int nparts, long long part_stride,
                                                        Rows rows, int Hq, int Hkv, int D, const float2* rope_cs,
                                                        int max_pos, T* q, KVLayout kv) {
@@ -78,12 +83,24 @@ __global__ __launch_bounds__(1024) void qkv_rope_kernel(const float* parts, int 
   const float2* cs = rope_cs + (long long)pos * half;
   const int nqkv = (Hq + 2 * Hkv) * D;
   const float* pr = parts + (long long)r * nqkv;
-  auto col = [&](int c) {
-    float v = pr[c];
+  // columns c and c + D/2, summed over the splits in split order (split-K
+  // partials are finite, so the 0/1 factor masks them exactly)
+  auto cols = [&](int c, float& v1, float& v2) {
+    float a1[NP], a2[NP];
 #pragma unroll
-    for (int p = 1; p < kMaxSplitK; ++p)
-      if (p < nparts) v += pr[p * part_stride + c];
-    return v;
+    for (int p = 0; p < NP; ++p) {
+      const float* pp = pr + min(p, nparts - 1) * part_stride;
+      a1[p] = pp[c];
+      a2[p] = pp[c + half];
+    }
+    v1 = a1[0];
+    v2 = a2[0];
+#pragma unroll
+    for (int p = 1; p < NP; ++p) {
+      const float f = p < nparts ? 1.f : 0.f;
+      v1 += a1[p] * f;
+      v2 += a2[p] * f;
+    }
   };
   const int b = rows.prompt[r];
   // destinations: K of head h at kd + h * kstride; V of head h, dim d at
@@ -111,18 +128,22 @@ __global__ __launch_bounds__(1024) void qkv_rope_kernel(const float* parts, int 
   for (int i = threadIdx.x; i < nh * half; i += blockDim.x) {
     const int h = h0 + i / half, j = i % half;
     const int base = h * D;
-    if (h < Hq + Hkv) {  // rotated q or k pair (j, j + D/2)
-      const float x1 = col(base + j), x2 = col(base + j + half);
-      const float2 cj = cs[j];
-      const float y1 = x1 * cj.x - x2 * cj.y;
-      const float y2 = x2 * cj.x + x1 * cj.y;
+    float x1, x2;
+    cols(base + j, x1, x2);
+    // q and k pairs (j, j + D/2) are rotated, v passes through (cos 1, sin 0)
+    const float2 cj = cs[j];
+    const float kq = h < Hq + Hkv ? 1.f : 0.f;
+    const float c = cj.x * kq + (1.f - kq), sn = cj.y * kq;
+    const float y1 = x1 * c - x2 * sn;
+    const float y2 = x2 * c + x1 * sn;
+    if (h < Hq + Hkv) {
       T* dst = h < Hq ? q + ((long long)r * Hq + h) * D : kd + (long long)(h - Hq) * kstride;
       store_f(dst + j, y1);
       store_f(dst + j + half, y2);
     } else {             // v: dims j and j + D/2 of head h - Hq - Hkv
       const int hv = h - Hq - Hkv;
-      store_f(vd + hv * vhstride + (long long)j * vdstride, col(base + j));
-      store_f(vd + hv * vhstride + (long long)(j + half) * vdstride, col(base + j + half));
+      store_f(vd + hv * vhstride + (long long)j * vdstride, y1);
+      store_f(vd + hv * vhstride + (long long)(j + half) * vdstride, y2);
     }
   }
 }
@@ -161,8 +182,16 @@ hipError_t qkv_rope_store(const float* parts, int nparts, long long part_stride,
   if (D > 256 || (D & 1) || nparts < 1 || nparts > kMaxSplitK) return hipErrorInvalidValue;
   // one thread per (head of the group of 8, rotation pair)
   const int threads = std::max(64, 8 * (D / 2));
-  hipLaunchKernelGGL(qkv_rope_kernel<T>, dim3(rows.R, (Hq + 2 * Hkv + 7) / 8), dim3(threads), 0, s, parts, nparts,
-                     part_stride, rows, Hq, Hkv, D, (const float2*)rope_cs, max_pos, q, kv);
+  const dim3 grid(rows.R, (Hq + 2 * Hkv + 7) / 8);
+  if (nparts <= 4)
+    hipLaunchKernelGGL((qkv_rope_kernel<T, 4>), grid, dim3(threads), 0, s, parts, nparts, part_stride, rows, Hq, Hkv,
+                       D, (const float2*)rope_cs, max_pos, q, kv);
+  else if (nparts <= 8)
+    hipLaunchKernelGGL((qkv_rope_kernel<T, 8>), grid, dim3(threads), 0, s, parts, nparts, part_stride, rows, Hq, Hkv,
+                       D, (const float2*)rope_cs, max_pos, q, kv);
+  else
+    hipLaunchKernelGGL((qkv_rope_kernel<T, kMaxSplitK>), grid, dim3(threads), 0, s, parts, nparts, part_stride, rows,
+                       Hq, Hkv, D, (const float2*)rope_cs, max_pos, q, kv);
   return hipGetLastError();
 }
 
