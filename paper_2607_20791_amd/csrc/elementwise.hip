@@ -43,6 +43,7 @@ __global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(float* x
 #pragma unroll
   for (int c = 0; c < kChunks; ++c) {
     const int i = (threadIdx.x + c * blockDim.x) * 4;
+    v[c] = gg[c] = float4{0.f, 0.f, 0.f, 0.f};
     if (i < d) {
       float4 q[kMaxSplitK];
 #pragma unroll

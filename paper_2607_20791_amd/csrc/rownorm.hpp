@@ -26,10 +26,13 @@ template <typename T>
 RGD_DEV void norm_store(const float4 (&v)[kChunks], const float4 (&gg)[kChunks], int d, float eps, T* xn) {
   __shared__ float red[16];
   float ss = 0.f;
+  // chunks past d do not count (a per-lane select, not a branch: a value used
+  // only inside a branch makes the compiler move its load there and wait)
 #pragma unroll
   for (int c = 0; c < kChunks; ++c) {
     const int i = (threadIdx.x + c * blockDim.x) * 4;
-    if (i < d) ss += v[c].x * v[c].x + v[c].y * v[c].y + v[c].z * v[c].z + v[c].w * v[c].w;
+    const float q = v[c].x * v[c].x + v[c].y * v[c].y + v[c].z * v[c].z + v[c].w * v[c].w;
+    ss += i < d ? q : 0.f;
   }
   ss = block_sum(ss, red);
   const float inv = rsqrtf(ss / float(d) + eps);
@@ -49,13 +52,13 @@ template <typename T>
 RGD_DEV void embed_norm_row(int tok, const T* E, int d, int V, const float* g, float eps, float* x, T* xn) {
   const long long t = min(max(tok, 0), V - 1);
   float4 v[kChunks], gg[kChunks];
+  // unconditional loads from clamped addresses (chunks past d are left out
+  // of the norm and not stored)
 #pragma unroll
   for (int c = 0; c < kChunks; ++c) {
-    const int i = (threadIdx.x + c * blockDim.x) * 4;
-    if (i < d) {
-      v[c] = load4(E + t * d + i);
-      gg[c] = load4(g + i);
-    }
+    const int i = min((int)(threadIdx.x + c * blockDim.x) * 4, d - 4);
+    v[c] = load4(E + t * d + i);
+    gg[c] = load4(g + i);
   }
 #pragma unroll
   for (int c = 0; c < kChunks; ++c) {

@@ -773,18 +773,22 @@ RGD_DEV int probe_update_row(const GateArgs& a, int r) {
 }
 
 __global__ __launch_bounds__(256) void probe_update_kernel(GateArgs a) {
-  __shared__ int sh_tok;
+  __shared__ int sh_tok, sh_held;
   const int r = blockIdx.x;
   if (threadIdx.x < 64) {
     const int t = probe_update_row(a, r);
     if (threadIdx.x == 0) sh_tok = t;
+  } else if (threadIdx.x == 64) {
+    // meanwhile, the token the row's probe holds at feed_col (what a prompt
+    // decided earlier feeds; both loads are in range whatever feed_col)
+    const int b = a.row_prompt[r];
+    sh_held = a.probe_tokens[(long long)b * a.k + min(max(a.feed_col, 0), a.k - 1)];
   }
   if (!a.embed) return;
   __syncthreads();
   // the token the next step feeds: the one just appended (column feed_col),
   // or for a prompt decided earlier what its probe holds there
-  const int b = a.row_prompt[r];
-  const int tok = sh_tok >= 0 ? sh_tok : a.probe_tokens[(long long)b * a.k + a.feed_col];
+  const int tok = sh_tok >= 0 ? sh_tok : sh_held;
   float* x = a.x + (long long)r * a.d;
   if (a.embed_bf16)
     embed_norm_row(tok, (const bf16_t*)a.embed, a.d, a.vocab, a.gain, a.eps, x, (bf16_t*)a.xn + (long long)r * a.d);
