@@ -1176,13 +1176,14 @@ int probe_impl(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_tab
   RGD_TRY(set_rows(h, pages));
   // token 1 from the prompt logits (rows are prompts 0..B-1 here)
   RGD_TRY(step(last_logits, B, 1, false));
-  // Polls: after each of the first c tokens and after token k the host waits
-  // for the events (the first c checks of Algorithm 1, and the end).  The
-  // checks every c tokens in between are pipelined: the copy of the events is
-  // enqueued after token j-1 and read once the next step has been launched,
-  // so the GPU never waits for the host; a probe that ended there has decoded
-  // one more token, which leaves its events and tokens as they were (decided
-  // rows are not updated) and only costs that step's time.
+  // Polls: after each of the first c tokens and every c tokens after that
+  // (the checks of Algorithm 1), and after token k.  After token 1 (which
+  // needs no decode step) and after token k the host waits for the events;
+  // the other checks are pipelined: the copy of the events is enqueued after
+  // token j-1 and read once the next step has been launched, so the GPU never
+  // waits for the host; a probe that ended there has decoded one more token,
+  // which leaves its events and tokens as they were (decided rows are not
+  // updated) and only costs that step's time.
   bool done = false;
   auto apply_poll = [&]() -> int {
     std::vector<int> still;
@@ -1203,7 +1204,7 @@ int probe_impl(rgd_model* m, rgd_kv* kv, const float* last_logits, const rgd_tab
     const int done_tokens = j - 1;
     const bool first = done_tokens <= c, last = done_tokens >= k;
     const bool check = first || done_tokens % c == 0 || last;
-    const bool pipelined = check && !first && !last;
+    const bool pipelined = check && done_tokens > 1 && !last;
     if (check && !pipelined) {
       HIP_OK(hipMemcpyAsync(pinned_ev, event, (size_t)B * 4, hipMemcpyDeviceToHost, s));
       HIP_OK(spin_sync(m, s));
