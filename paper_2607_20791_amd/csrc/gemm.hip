@@ -128,7 +128,19 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[mt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  u32x4 wb[SW][NT][2], xr[XPT];
+  // One 16-row tile (M <= 16, the probe's one-row steps): the A fragments come
+  // straight from X in global memory (a few KiB, cache-resident) through a
+  // register ring beside the weights' ring, with no LDS staging and no
+  // barrier per stage.  Each lane reads the same row and k values it would
+  // read from LDS, so the arithmetic is that of the staged path.
+  constexpr bool XG = (MT == 1);
+  const int kq = (lane >> 4) * 16;
+  u32x4 wb[SW][NT][2], xr[XPT], xa[SW][2];
+  const bf16_t* xrow = (const bf16_t*)a.x + (long long)min(m0 + col16, a.M - 1) * a.ldx + kq;
+  auto loadxa = [&](int st, int slot) {
+    xa[slot][0] = *(const u32x4*)(xrow + (long long)st * kStep);
+    xa[slot][1] = *(const u32x4*)(xrow + (long long)st * kStep + 8);
+  };
   auto loadw = [&](int st, int slot) {
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
@@ -160,9 +172,11 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
 
 #pragma unroll
   for (int j = 0; j < SW; ++j)
-    if (st0 + j < st1) loadw(st0 + j, j);
-  if (st0 < st1) loadx(st0);
-  const int kq = (lane >> 4) * 16;
+    if (st0 + j < st1) {
+      loadw(st0 + j, j);
+      if (XG) loadxa(st0 + j, j);
+    }
+  if (!XG && st0 < st1) loadx(st0);
   // W ring: step st lives in slot (st - st0) % SW; X stage g covers steps
   // [st0 + g*XS, st0 + (g+1)*XS)
   constexpr int UN = XS > SW ? XS : SW;  // steps per unrolled block
@@ -173,7 +187,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
       if (st < st1) {
         const int g = (st - st0) / XS, kk = ((st - st0) % XS) * kStep;
         const int xsl = g & 1;
-        if (kk == 0) {  // first step of a stage: publish it, fetch the next
+        if (!XG && kk == 0) {  // first step of a stage: publish it, fetch the next
           storex(xsl);
           if (st + XS < st1) loadx(st + XS);
           __syncthreads();
@@ -182,11 +196,14 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
         for (int h = 0; h < 2; ++h)
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) {
-            const u32x4 av = *(const u32x4*)&xs[xsl][mt * 16 + col16][kk + kq + h * 8];
+            const u32x4 av = XG ? xa[j % SW][h] : *(const u32x4*)&xs[xsl][mt * 16 + col16][kk + kq + h * 8];
 #pragma unroll
             for (int jj = 0; jj < NT; ++jj) acc[mt][jj] = mfma16x16x32(av, wb[j % SW][jj][h], acc[mt][jj]);
           }
-        if (st + SW < st1) loadw(st + SW, j % SW);
+        if (st + SW < st1) {
+          loadw(st + SW, j % SW);
+          if (XG) loadxa(st + SW, j % SW);
+        }
       }
     }
   }
