@@ -296,34 +296,43 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
   // One straight-line stream per half: the scores of the following half
   // (buffer kb, half kh, into nxt), the exponentials of this half (cur)
   // interleaved with them, then this half's P V product (buffer vb, half vh).
-  // 16 fragment reads go through a register ring of RGD_ATTN_RING slots, NQ
-  // MFMAs each.  After
-  // the last half kb holds stale data and nxt is simply not used.
-  auto stream = [&](int kb, int kh, int vb, int vh, f32x4 (&cur)[2][NQ], f32x4 (&nxt)[2][NQ]) {
-    auto frag = [&](int f) -> u32x4 { return f < 8 ? k_frag(kb, kh, f >> 2, f & 3) : v_frag(vb, f - 8, vh); };
-    constexpr int RD = RGD_ATTN_RING;  // fragment reads in flight + 1
-    u32x4 ring[RD];
+  // The 16 fragment reads go through a register ring of RD slots, NQ MFMAs
+  // each; the caller primes the ring before the half's softmax preparation so
+  // that those reads overlap it, and every step ends in a scheduling barrier,
+  // so that the reads stay RD - 1 steps ahead of their MFMAs as written (left
+  // alone, the scheduler moves each read next to its use and the MFMAs wait
+  // for LDS).  The two score blocks alternate, so consecutive score MFMAs are
+  // independent.  After the last half kb holds stale data and nxt is simply
+  // not used.
+  constexpr int RD = RGD_ATTN_RING;  // fragment reads in flight + 1
+  auto frag = [&](int kb, int kh, int vb, int vh, int f) -> u32x4 {
+    return f < 8 ? k_frag(kb, kh, f & 1, f >> 1) : v_frag(vb, f - 8, vh);
+  };
+  auto prime = [&](int kb, int kh, int vb, int vh, u32x4 (&ring)[RD]) {
 #pragma unroll
-    for (int f = 0; f + 1 < RD; ++f) ring[f] = frag(f);
+    for (int f = 0; f + 1 < RD; ++f) ring[f] = frag(kb, kh, vb, vh, f);
+  };
+  auto stream = [&](int kb, int kh, int vb, int vh, f32x4 (&cur)[2][NQ], f32x4 (&nxt)[2][NQ], u32x4 (&ring)[RD]) {
     float plo[NQ];
     uint32_t pw[NQ][4];  // packed weights, word 2e + (i >> 1)
 #pragma unroll
     for (int f = 0; f < 16; ++f) {
-      if (f + RD - 1 < 16) ring[(f + RD - 1) % RD] = frag(f + RD - 1);
+      if (f + RD - 1 < 16) ring[(f + RD - 1) % RD] = frag(kb, kh, vb, vh, f + RD - 1);
       if (f < 8) {
-        const int e = f >> 2, ks = f & 3;
+        const int e = f & 1, ks = f >> 1;
         if (ks == 0) {
 #pragma unroll
           for (int nt = 0; nt < NQ; ++nt) nxt[e][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
 #pragma unroll
         for (int nt = 0; nt < NQ; ++nt) nxt[e][nt] = mfma16x16x32(ring[f % RD], qf[nt][ks], nxt[e][nt]);
-        // step f handles value i = f & 3 of block e = f >> 2; pairs are packed
-        // to bf16 as soon as both halves exist
+        // step f exponentiates value i = f & 3 of block ce = f >> 2 of this
+        // half; pairs are packed to bf16 as soon as both halves exist
+        const int ce = f >> 2, i = f & 3;
 #pragma unroll
         for (int nt = 0; nt < NQ; ++nt) {
-          const float x = exp2_raw(cur[e][nt][ks]);
-          if (ks & 1) pw[nt][e * 2 + (ks >> 1)] = pack2(plo[nt], x);
+          const float x = exp2_raw(cur[ce][nt][i]);
+          if (i & 1) pw[nt][ce * 2 + (i >> 1)] = pack2(plo[nt], x);
           else plo[nt] = x;
         }
       } else {
@@ -337,6 +346,7 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
             lacc[n2] = mfma16x16x32(ones, u32x4{pw[n2][0], pw[n2][1], pw[n2][2], pw[n2][3]}, lacc[n2]);
         }
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
@@ -363,10 +373,13 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
       }
       __syncthreads();
       if (wave_active) {
+        u32x4 ring[RD];
+        prime(cb, 1, cb, 0, ring);
         prepare(t0, sa);
-        stream(cb, 1, cb, 0, sa, sb);
+        stream(cb, 1, cb, 0, sa, sb, ring);
+        prime(nb, 0, cb, 1, ring);
         prepare(t0 + 32, sb);
-        stream(nb, 0, cb, 1, sb, sa);
+        stream(nb, 0, cb, 1, sb, sa, ring);
       }
     };
     static_assert(NB == 3, "the tile loop is unrolled by the ring depth");
