@@ -388,25 +388,54 @@ int gemm_groups(int mode, int N) {
 }
 
 // Launch shapes (panels per wave, waves, weight steps in flight, X steps per
-// LDS stage), chosen by measurement at the decode shapes of an 8B-class layer:
-// split-K projections <1, 8, 4, 2>, SwiGLU <1, 4, 4, 4>, LM head <4, 8, 2, 1> (512 columns per
-// workgroup: the X rows every workgroup streams through LDS cost half as much per weight byte).
-// Above 64 rows (128-row tiles) each X fragment read from LDS must feed more than one MFMA, or
-// LDS reads, not HBM, set the pace: split-K and SwiGLU then run two panels per wave on four
-// waves (<2, 4, 4>; the same 128 columns per workgroup for split-K, twice the columns for
-// SwiGLU).  A row's arithmetic is the same under every shape (same k order, same split-K).
+// LDS stage), chosen by measurement at the shapes of an 8B-class layer (the
+// split-K factor comes with the call and depends on the shape only):
+// * up to 64 rows: split-K projections <1, 8, 4, 2>, SwiGLU <1, 4, 4, 4>;
+// * 65-128 rows (one 128-row tile): both <1, 8, 4> (128 columns per
+//   workgroup for split-K, 64 output features for SwiGLU);
+// * more rows: both <2, 8, 4> (256 columns / 128 features per workgroup: the
+//   two 128-row blocks of a column group then stream twice the weights per
+//   X stage they load);
+// * the LM head <4, 8, 2> at every height (512 columns per workgroup: the X
+//   rows every workgroup streams through LDS cost half as much per weight
+//   byte).
+// A row's arithmetic is the same under every shape (same k order, same
+// split-K).
+namespace {
+
+// a workgroup of `cols` columns never straddles segments
+bool segments_aligned(const GemmArgs& a, int cols) {
+  for (int i = 1; i < a.nseg; ++i)
+    if (a.seg[i].n0 % cols) return false;
+  return true;
+}
+template <int NT, int NW, int SW, int XS>
+hipError_t launch_store(const GemmArgs& a, hipStream_t s) {
+  constexpr int cols = 16 * NT * NW;
+  if (!segments_aligned(a, cols)) return hipErrorInvalidValue;
+  return launch_bf16<NT, NW, SW, GEMM_STORE, XS>(a, (a.N + cols - 1) / cols, s);
+}
+template <int NT, int NW, int SW, int XS>
+hipError_t launch_silu(const GemmArgs& a, hipStream_t s) {
+  constexpr int feats = 16 * NT * (NW / 2);
+  return launch_bf16<NT, NW, SW, GEMM_SILU, XS>(a, (a.N + feats - 1) / feats, s);
+}
+
+}  // namespace
+
 hipError_t gemm_bf16(const GemmArgs& a, hipStream_t s) {
   if (a.K % kStep != 0 || a.M < 1 || a.splits < 1 || a.splits > a.K / kStep) return hipErrorInvalidValue;
   const int g = gemm_groups(a.mode, a.N);
   switch (a.mode) {
     case GEMM_STORE:
-      for (int i = 1; i < a.nseg; ++i)
-        if (a.seg[i].n0 % 128) return hipErrorInvalidValue;  // a workgroup never straddles segments
-      return a.M > 64 ? launch_bf16<2, 4, 4, GEMM_STORE, 2>(a, g, s) : launch_bf16<1, 8, 4, GEMM_STORE, 2>(a, g, s);
+      // (segments that are not 256-column aligned keep 128-column workgroups)
+      if (a.M > 128 && segments_aligned(a, 256)) return launch_store<2, 8, 4, 2>(a, s);
+      return launch_store<1, 8, 4, 2>(a, s);
     case GEMM_SILU:
       if (a.splits != 1) return hipErrorInvalidValue;
-      return a.M > 64 ? launch_bf16<2, 4, 4, GEMM_SILU, 4>(a, (a.N + 63) / 64, s)
-                      : launch_bf16<1, 4, 4, GEMM_SILU, 4>(a, g, s);
+      if (a.M > 128) return launch_silu<2, 8, 4, 4>(a, s);
+      if (a.M > 64) return launch_silu<1, 8, 4, 4>(a, s);
+      return launch_silu<1, 4, 4, 4>(a, s);
     case GEMM_LOGITS:
       if (a.splits != 1 || a.ntiles != g) return hipErrorInvalidValue;
       return launch_bf16<4, 8, 2, GEMM_LOGITS, 1>(a, g, s);
