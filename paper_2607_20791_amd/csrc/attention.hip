@@ -384,7 +384,7 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
         stream(nb, 0, cb, 1, sb, sa, ring);
       }
     };
-    static_assert(NB == 3, "the tile loop is unrolled by the ring depth");
+    static_assert(NB == 3, "the tile loop is unrolled by the number of LDS tile buffers");
     for (int t = 0; t < ntile; t += NB) {
       tile(t, std::integral_constant<int, 0>{});
       if (t + 1 < ntile) tile(t + 1, std::integral_constant<int, 1>{});
