@@ -93,11 +93,14 @@ def test_64_row_steps_8192_prefix(rgd, p8192):
     print(f"8192-prefix layer, 64-row steps: logits rel err (worst) {worst:.3e}")
 
 
-@pytest.mark.parametrize("rows,check", [(128, (0, 77, 127)), (256, (0, 129, 255))])
+@pytest.mark.parametrize("rows,check", [(128, (0, 77, 127)), (256, (0, 129, 255)), (100, (0, 57, 99)),
+                                       (200, (0, 131, 199))])
 def test_wide_steps_512_prefix(rgd, p512_wide, rows, check):
     """128- and 256-row steps (the 8-layer workload's gated and ungated
     batches): 128-row GEMM blocks, two per weight panel at 256 rows, and four
-    or eight attention row blocks (more than the four passed by value)."""
+    or eight attention row blocks (more than the four passed by value); 100
+    and 200 rows: a partial 128-row block under each workgroup shape (one
+    panel per wave up to 128 rows, two above)."""
     w = p512_wide.w
     steps = 2
     forced = synth.forced_history(w, rows, steps, name=f"forced{rows}")
