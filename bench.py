@@ -365,10 +365,33 @@ def eight_layer(rgd, torch, reps):
     t_g, t_pg, dec, miss = runs[len(runs) // 2]
     t_u = sorted(ungated(range(B)) for _ in range(reps))[reps // 2]
     t_um = sorted(ungated(miss) for _ in range(reps))[reps // 2] if miss else 0.0
+    # one more ungated call with the library timers on: the LM head and the
+    # whole decode step at B x N rows
+    rgd.timing_enable(m, 1)
+    rgd.timing_enable(m, 0)
+    rgd.timing_read(m)
+    rgd.timing_enable(m, TIMING_PERIOD)
+    ungated(range(B))
+    rgd.timing_enable(m, 0)
+    tim = rgd.timing_read(m)
     rgd.check_status(m)
     pl = plen.cpu().numpy()
     hits = [b for b in range(B) if dec[b] == 1]
     returned = len(miss) * N * S + int(sum(int(pl[b]) for b in hits))
+    # Byte model of one ungated decode step (B x N rows): every layer's weights
+    # and the LM head once, each prompt's KV once per layer, each row's tail
+    # (on average (S + 1) / 2 positions) once per layer, the logits written and
+    # read once; bf16 weights and KV, fp32 logits.
+    R = B * N
+    qkv = (w.n_heads + 2 * w.n_kv_heads) * w.head_dim
+    layer_w = (qkv * w.d_model + w.n_heads * w.head_dim * w.d_model + 3 * w.ffn * w.d_model) * 2
+    kv_pos = w.n_kv_heads * w.head_dim * 2 * 2
+    step_bytes = (w.n_layers * layer_w + w.vocab * w.d_model * 2 + w.n_layers * B * n * kv_pos
+                  + w.n_layers * R * (S + 1) / 2 * kv_pos + R * w.vocab * 4 * 2)
+    ceiling = R / (step_bytes / (HBM_PEAK_GBS * 1e9))
+    lm_bytes = w.vocab * w.d_model * 2 + R * w.d_model * 2 + R * w.vocab * 4
+    lm_us = tim["lm_head"][0] / max(tim["lm_head"][1], 1) * 1e3
+    step_us = tim["step"][0] / max(tim["step"][1], 1) * 1e3
     return {"workload": w.name, "prompts": B, "prompt_len": n, "branches": N, "steps": S, "probe_k": k,
             "hits": len(hits), "misses": len(miss), "prefill_s": round(prefill_s, 4),
             "gated_s": round(t_g, 4), "gated_tokens_returned": returned,
@@ -378,7 +401,14 @@ def eight_layer(rgd, torch, reps):
             "miss_cost": {"check_tokens_per_miss": round(float(np.mean([pl[b] for b in miss])), 3) if miss else None,
                           "probe_gate_ms": round(t_pg * 1e3, 3),
                           "direct_sampling_of_misses_ms": round(t_um * 1e3, 3),
-                          "ratio": round((t_pg + t_um) / t_um, 4) if t_um > 0 else None}}
+                          "ratio": round((t_pg + t_um) / t_um, 4) if t_um > 0 else None},
+            "byte_model": {"ungated_bytes_per_step": int(step_bytes),
+                           "ungated_ceiling_tokens_per_s": round(ceiling, 1),
+                           "ungated_frac": round(B * N * S / t_u / ceiling, 4),
+                           "decode_step_us": round(step_us, 2),
+                           "decode_step_frac": round(step_bytes / (step_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                           "lm_head_us": round(lm_us, 2),
+                           "lm_head_frac": round(lm_bytes / (lm_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}}
 
 
 def cpu_baseline_units(reps=3):
