@@ -105,3 +105,52 @@ def test_first_token_brute_force(tiny):
     got = dec.prefill([7], KVCache(1))
     xf = x1 / math.sqrt(np.mean(x1 * x1) + TINY.rms_eps)
     assert np.allclose(got, om.widen(W.lm_head) @ xf, rtol=1e-11, atol=1e-11)
+
+
+def _segment_out(dec, positions, layer=0):
+    """One block over a two-token segment (tokens 5 and 9: different values, so
+    the attention weights matter) that sees only itself, causally."""
+    x = dec.embed([5, 9])
+    out, _, _ = dec._block(layer, x, positions, lambda t, k, v: (k[:t + 1], v[:t + 1]))
+    return out
+
+
+def test_block_rotary_positions_are_relative(tiny):
+    """RoPE on both queries and keys makes attention scores depend on the
+    offset between positions only: a segment shifted as a whole gives the same
+    block output, and a different gap between its two tokens does not."""
+    a = _segment_out(tiny, [0, 1])
+    b = _segment_out(tiny, [37, 38])
+    assert np.allclose(a, b, rtol=1e-10, atol=1e-12)
+    c = _segment_out(tiny, [0, 5])
+    assert not np.allclose(a[1], c[1], rtol=1e-6, atol=1e-9)
+
+
+def test_norm_gains_select_their_branch():
+    """Each RMSNorm gain scales only its own branch: a zero attention gain
+    zeroes q, k and v (so the attention branch adds exactly nothing), a zero
+    FFN gain zeroes the SwiGLU input (silu(0) * 0 = 0), and a zero final gain
+    zeroes the logits."""
+    import copy
+    W = synth.model_weights(TINY)
+    x = None
+
+    def out(attn_g, ffn_g):
+        w2 = copy.copy(W)
+        w2.layers = [dict(L) for L in W.layers]
+        w2.layers[0]["attn_norm"] = np.full_like(W.layers[0]["attn_norm"], attn_g)
+        w2.layers[0]["ffn_norm"] = np.full_like(W.layers[0]["ffn_norm"], ffn_g)
+        d = Decoder(w2)
+        x0 = d.embed([3])
+        o, _, _ = d._block(0, x0, [2], lambda t, k, v: (k[:t + 1], v[:t + 1]))
+        return x0, o
+
+    x, o = out(0.0, 0.0)
+    assert np.array_equal(o, x)
+    _, o = out(0.0, 1.0)
+    assert not np.allclose(o, x)
+    x, o = out(1.0, 0.0)
+    assert not np.allclose(o, x)
+    w3 = copy.copy(W)
+    w3.final_norm = np.zeros_like(W.final_norm)
+    assert np.array_equal(Decoder(w3).logits(np.ones(TINY.d_model)), np.zeros(TINY.vocab))

@@ -98,3 +98,18 @@ def test_many_matches_single():
         one = sampler.sample_minp(z, 1.3, 0.07, u)
         assert d.token == one.token
         assert np.isclose(d.cdf_margin, one.cdf_margin, rtol=0, atol=1e-15)
+
+
+def test_draw_on_an_exact_running_sum():
+    """The draw returns the smallest kept id whose running kept-weight sum
+    exceeds u * W (strictly): with two equal weights (W = 2) and u = 0.5 the
+    target 1.0 equals the first running sum, so token 1 is drawn, and u = 0
+    draws token 0.  The one-draw and many-draw forms agree on these edges."""
+    z = np.zeros(2)
+    for u, want in ((0.5, 1), (0.0, 0), (0.75, 1), (0.25, 0)):
+        assert sampler.sample_minp(z, 1.0, 0.1, u).token == want
+        assert sampler.sample_minp_many(z, 1.0, 0.1, [u])[0].token == want
+    z3 = np.zeros(4)                                   # W = 4, edges at 1, 2, 3
+    us = [0.25, 0.5, 0.75, 0.0]
+    assert [d.token for d in sampler.sample_minp_many(z3, 1.0, 0.1, us)] == [1, 2, 3, 0]
+    assert [sampler.sample_minp(z3, 1.0, 0.1, u).token for u in us] == [1, 2, 3, 0]
