@@ -62,6 +62,11 @@ def test_probe_events_and_early_exit():
     assert gate.probe(first, nxt, [], k=6) == ([7], gate.INCOMPAT)
 
 
+def test_gate_decision_per_event():
+    """Algorithm 1 returns the greedy probe on STOP and MAXLEN and samples on INCOMPAT."""
+    assert gate.is_hit(gate.STOP) and gate.is_hit(gate.MAXLEN) and not gate.is_hit(gate.INCOMPAT)
+
+
 @pytest.mark.parametrize("seed", range(20))
 def test_early_exit_decision_equals_full_probe(seed):
     """Prefix closure makes 'stop at the first incompatible token' and 'decode k

@@ -94,3 +94,5 @@ def test_matches_rocrand_engine_on_host():
     for (seed, ctr, stream), got in zip(cases, out):
         k0, k1 = seed & 0xFFFFFFFF, seed >> 32
         assert philox.philox4x32_10_int((ctr, stream, 0, 0), (k0, k1))[0] == int(got)
+        # the sampler's uniform is the top 24 bits of that word
+        assert float(philox.uniform(np.uint64(seed), ctr, stream)) == (int(got) >> 8) * 2.0 ** -24

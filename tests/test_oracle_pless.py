@@ -126,6 +126,19 @@ def test_inverse_cdf_matches_searchsorted_and_many_matches_single():
             assert d.token == int(np.searchsorted(cdf, float(u), side="right"))
 
 
+def test_draw_on_an_exact_running_sum():
+    """The draw takes the first kept token whose running sum is strictly above
+    u * W: with equal probabilities the running sums are exact multiples of
+    1/n, and u on such an edge selects the next token (both draw forms)."""
+    z2 = np.zeros(2)
+    for u, want in ((0.5, 1), (0.0, 0), (0.75, 1), (0.25, 0)):
+        assert pless.sample_pless(z2, 1.0, u).token == want
+        assert pless.sample_pless_many(z2, 1.0, [u])[0].token == want
+    us = [0.25, 0.5, 0.75, 0.0]
+    assert [pless.sample_pless(np.zeros(4), 1.0, u).token for u in us] == [1, 2, 3, 0]
+    assert [d.token for d in pless.sample_pless_many(np.zeros(4), 1.0, us)] == [1, 2, 3, 0]
+
+
 def test_draw_distribution_chi_square():
     from scipy import stats
     g = np.random.default_rng(19)

@@ -66,3 +66,18 @@ def test_adaptive_gate_limits(soft):
     # the decision is P <= theta, at the score itself
     r2 = precheck.adaptive_gated(dec, PROMPT, table, 6, seeds, 4, 2.0, 0.1, 2, w, 0.3, r0.score, soft=soft)
     assert r2.skipped
+
+
+def test_score_reads_the_residual_after_the_chosen_block():
+    """The pre-check scores the residual after block `layer` (0: the embedding):
+    each layer's score equals the readout of that tap, and the taps differ."""
+    dec = Decoder(synth.model_weights(TINY))
+    taps = {}
+    dec.prefill(PROMPT, KVCache(TINY.n_layers), taps=taps)
+    w = np.random.default_rng(8).normal(size=TINY.d_model)
+    scores = []
+    for layer in range(TINY.n_layers + 1):
+        r = precheck.adaptive_gated(dec, PROMPT, [[7, 8]], 4, [1], 2, 2.0, 0.1, layer, w, 0.1, 1.0)
+        assert r.score == precheck.residual_score(taps[layer], w, 0.1)
+        scores.append(r.score)
+    assert len(set(scores)) == len(scores)

@@ -53,6 +53,35 @@ def test_branch_first_token_uses_prompt_logits_and_counter_zero():
     assert br.tokens[0] == sampler.sample_minp(last, 1.5, 0.05, u0).token
 
 
+def test_branch_step_s_draws_with_counter_s_and_its_stream():
+    """Token s of a branch uses the uniform of Philox counter (s, stream, 0, 0)
+    under key (seed lo, seed hi), formed here from the scalar Philox that the
+    known-answer vectors pin; the whole draw (token and margins) must match."""
+    dec, prefix, last = _setup()
+    seed = (5 << 32) | 77
+    for stream in (0, 3):
+        br = rgd.sample_branch(dec, prefix, last, seed, 5, 1.5, 0.05, keep_logits=True, stream=stream)
+        for s in range(5):
+            w0 = philox.philox4x32_10_int((s, stream, 0, 0), (seed & 0xFFFFFFFF, seed >> 32))[0]
+            u = (w0 >> 8) * 2.0 ** -24
+            assert br.draws[s] == sampler.sample_minp(br.logits[s], 1.5, 0.05, u)
+
+
+def test_probe_ending_on_the_stop_token_is_a_hit():
+    """A compatible probe that emits the stop token ends the gate with STOP, and
+    Algorithm 1 returns the greedy probe (no branches)."""
+    dec, prefix, last = _setup()
+    full = [sampler.argmax(last)]
+    tail = KVCache(1)
+    for _ in range(3):
+        full.append(sampler.argmax(dec.decode(full[-1], prefix, tail)))
+    eos = full[1]
+    stop_at = full.index(eos) + 1
+    res = rgd.refusal_gated(dec, None, [full], 6, seeds=[1, 2], steps=4, T=2.0, p_min=0.1, eos=eos,
+                            prefix=prefix, last_logits=last)
+    assert res.event == gate.STOP and res.hit and res.probe == full[:stop_at] and res.branches == []
+
+
 def test_forced_history_changes_only_inputs():
     dec, prefix, last = _setup()
     forced = [4, 8, 15, 16]
