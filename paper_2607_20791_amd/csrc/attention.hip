@@ -660,8 +660,10 @@ __global__ __launch_bounds__(256) void attn_tail_combine_kernel(AttnArgs a, T* o
 // head form one 16-column tile, K and V^T fragments are loaded straight from
 // the pages (K rows in the gathered order of the prefix kernel, so every lane
 // ends up with eight consecutive positions).  The four waves' tail states are
-// merged through LDS, then wave h merges query head h's prefix-split partials
-// with its tail in log-sum-exp form (split order fixed) and writes the output.
+// merged through LDS, and wave h writes query head h's output.  The merge is
+// in log-sum-exp form with a fixed split order; for the wave's first head the
+// prefix-split partials are combined into one while the wave's first tile is
+// loading, which leaves a two-term merge with the tail after the exchange.
 constexpr int kMergeMaxSplits = 64;
 
 __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t* out) {
@@ -693,9 +695,9 @@ __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t
 
   // The prefix-split partials and log-sum-exps do not depend on the tail:
   // request those of this wave's first head now so their latency overlaps the
-  // tail attention (splits beyond kPrefetch are loaded in the merge).
+  // tail attention (splits beyond kPrefetch are loaded by the combine).
   const int S = a.splits;
-  constexpr int kPrefetch = 32;
+  constexpr int kPrefetch = 16;
   const long long pstep = R * a.Hq * D;
   // (Loads in this kernel are unconditional, from clamped addresses, and
   // masked afterwards: a predicated load makes the compiler wait for it where
@@ -726,6 +728,44 @@ __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t
   f32x4 o[8];
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // The prefix splits of this wave's first head combined into one partial
+  // (natural-log log-sum-exp s_lse, normalised output s_o0 / s_o1 for dims
+  // 2*lane, 2*lane+1), in fixed split order.  It needs no tail data, so it is
+  // formed while the first tile's loads are in flight.
+  float s_lse = -INFINITY, s_o0 = 0.f, s_o1 = 0.f;
+  auto combine_splits = [&]() {
+    const int head = g * G + min(wave, G - 1);
+    float mx = pre_lse;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+    const float w = pre_lse == -INFINITY ? 0.f : __expf(pre_lse - mx);
+    float den = w;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) den += __shfl_xor(den, off, 64);
+    const float inv = den > 0.f ? 1.f / den : 0.f;
+    const bf16_t* po = (const bf16_t*)a.part_o + ((long long)r * a.Hq + head) * D + 2 * lane;
+    float o0 = 0.f, o1 = 0.f;
+    // weight of split sp sits in lane sp
+#pragma unroll
+    for (int k = 0; k < kPrefetch; ++k) {
+      if (k < S) {
+        const float wk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), k)) * inv;
+        o0 += wk * __uint_as_float(pre[k] << 16);
+        o1 += wk * __uint_as_float(pre[k] & 0xFFFF0000u);
+      }
+    }
+#pragma unroll 1
+    for (int k = kPrefetch; k < S; ++k) {  // splits past the prefetched ones (long prompts)
+      const uint32_t v = *(const uint32_t*)(po + k * pstep);
+      const float wk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), k)) * inv;
+      o0 += wk * __uint_as_float(v << 16);
+      o1 += wk * __uint_as_float(v & 0xFFFF0000u);
+    }
+    s_lse = den > 0.f ? mx + __logf(den) : -INFINITY;
+    s_o0 = o0;
+    s_o1 = o1;
+  };
+  bool combined = false;
   // the row's own positions: first its prefix positions the split kernel left
   // (fewer than 64 past a split boundary, read in place from the shared
   // prefix), then its paged tail; 32-position tiles of either, dealt to the
@@ -771,6 +811,10 @@ __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t
       for (int ks = 0; ks < 4; ++ks) ka[e][ks] = *(const u32x4*)(kr[e] + ks * 32);  // past the end: masked scores
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) va[dt] = *(const u32x4*)(vr + dt * vstep);  // past the end: zeroed below
+    if (!combined) {  // uniform: the first tile of the wave
+      combine_splits();
+      combined = true;
+    }
     f32x4 sc[2];
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
@@ -817,6 +861,7 @@ __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) o[dt] = mfma16x16x32(va[dt], pb, o[dt]);
   }
+  if (!combined) combine_splits();
   // per-wave tail states -> LDS (query q = l16, dims dt*16 + grp*4 + i)
   lsum += __shfl_xor(lsum, 16, 64);
   lsum += __shfl_xor(lsum, 32, 64);
@@ -846,8 +891,20 @@ __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t
       }
     }
     const float tail_lse = tl > 0.f ? (tm + __log2f(tl)) * kLn2 : -INFINITY;
-    // split log-sum-exps: lane sp holds split sp's
-    const float ls = first ? pre_lse : (lane < S ? a.part_lse[((long long)lane * R + r) * a.Hq + head] : -INFINITY);
+    if (first) {  // the prefix splits are combined already: two partials left
+      const float mx = fmaxf(s_lse, tail_lse);
+      const float ws = s_lse == -INFINITY ? 0.f : __expf(s_lse - mx);
+      const float wt = tail_lse == -INFINITY ? 0.f : __expf(tail_lse - mx);
+      const float den = ws + wt;
+      const float inv = den > 0.f ? 1.f / den : 0.f;
+      const float ft = tl > 0.f ? wt * inv / tl : 0.f;  // applied to the unnormalised tail sum
+      const float fs = ws * inv;
+      *(uint32_t*)(out + ((long long)r * a.Hq + head) * D + 2 * lane) =
+          pack_bf16x2(fs * s_o0 + ft * to0, fs * s_o1 + ft * to1);
+      return;
+    }
+    // further heads (G > 4): split log-sum-exps, lane sp holds split sp's
+    const float ls = lane < S ? a.part_lse[((long long)lane * R + r) * a.Hq + head] : -INFINITY;
     float mx = fmaxf(ls, tail_lse);
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
@@ -863,16 +920,7 @@ __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t
     const bf16_t* po = (const bf16_t*)a.part_o + ((long long)r * a.Hq + head) * D + 2 * lane;
     // weight of split sp sits in lane sp; fixed split order
 #pragma unroll
-    for (int k = 0; k < kPrefetch; ++k) {
-      if (k < S) {
-        const uint32_t v = first ? pre[k] : *(const uint32_t*)(po + k * pstep);
-        const float wk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), k)) * inv;
-        o0 += wk * __uint_as_float(v << 16);
-        o1 += wk * __uint_as_float(v & 0xFFFF0000u);
-      }
-    }
-#pragma unroll
-    for (int k = kPrefetch; k < kMergeMaxSplits; ++k) {
+    for (int k = 0; k < kMergeMaxSplits; ++k) {
       if (k < S) {
         const uint32_t v = *(const uint32_t*)(po + k * pstep);
         const float wk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), k)) * inv;
@@ -882,7 +930,7 @@ __global__ __launch_bounds__(256) void attn_tail_merge_kernel(AttnArgs a, bf16_t
     }
     *(uint32_t*)(out + ((long long)r * a.Hq + head) * D + 2 * lane) = pack_bf16x2(o0, o1);
   };
-  // the first head of the wave uses the prefetched partials
+  // the first head of the wave uses the combined prefix partial
   if (wave < G) finish(wave, true);
   for (int h = wave + 4; h < G; h += 4) finish(h, false);
 }
