@@ -63,6 +63,14 @@ constexpr float kNoRef = -3.0e38f;
 // are free of bank conflicts.
 RGD_DEV int kswz(int r) { return (r & 3) | ((r >> 1) & 12); }
 
+// V^T tiles sit in LDS as unpadded 128-byte rows (64 positions of one head
+// dimension) whose 16-byte chunks are XOR-swizzled: chunk c of row r is stored
+// at chunk c ^ vswz(r).  A fragment read (16 consecutive rows, one chunk each)
+// and a tile store (8 lanes per row) are then free of bank conflicts by the
+// LDS conflict counter; a padded 144-byte pitch, conflict-free on paper, was
+// measured 2-way conflicted on the fragment reads.
+RGD_DEV int vswz(int r) { return (r >> 1) & 7; }
+
 // Row of a 64-position tile that lane l16 supplies as the A operand of score
 // block (h, e).  With this order the score MFMA leaves lane (q, grp) holding
 // positions h*32 + grp*8 + e*4 + {0..3}, i.e. eight consecutive positions per
@@ -129,7 +137,7 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
   const bool wave_active = (wave * NQ * 16) < nq;
 
   __shared__ __attribute__((aligned(16))) bf16_t k_lds[NB][TP * D];
-  __shared__ __attribute__((aligned(16))) bf16_t v_lds[NB][D][TP + 8];
+  __shared__ __attribute__((aligned(16))) bf16_t v_lds[NB][D][TP];
 
   // this (prompt, KV head): K rows [P][D]; V in 64-position blocks [VP/64][D][64]
   const long long bg = (long long)b * a.Hkv + g;
@@ -188,18 +196,18 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
     if (vt0 + TP <= hi) {
 #pragma unroll
       for (int i = 0; i < VSEG; ++i) {
-        const int seg = threadIdx.x + i * NT;
-        *(u32x4*)&v_lds[buf][seg >> 3][(seg & 7) * 8] = vreg[i];
+        const int seg = threadIdx.x + i * NT, row = seg >> 3;
+        *(u32x4*)&v_lds[buf][row][((seg & 7) ^ vswz(row)) * 8] = vreg[i];
       }
     } else {
 #pragma unroll
       for (int i = 0; i < VSEG; ++i) {
-        const int seg = threadIdx.x + i * NT;
+        const int seg = threadIdx.x + i * NT, row = seg >> 3;
         const int nv = hi - (vt0 + (seg & 7) * 8);  // valid positions of this segment
         u32x4 vv = vreg[i];
 #pragma unroll
         for (int w = 0; w < 4; ++w) vv[w] &= nv >= 2 * w + 2 ? 0xFFFFFFFFu : (nv == 2 * w + 1 ? 0xFFFFu : 0u);
-        *(u32x4*)&v_lds[buf][seg >> 3][(seg & 7) * 8] = vv;
+        *(u32x4*)&v_lds[buf][row][((seg & 7) ^ vswz(row)) * 8] = vv;
       }
     }
   };
@@ -212,7 +220,8 @@ __global__ __launch_bounds__(NW * 64) void attn_prefix_kernel(AttnArgs a) {
   };
   // V^T fragment: lane (l16, grp) reads row dt*16 + l16 at positions hh*32 + grp*8 + {0..7}
   auto v_frag = [&](int buf, int dt, int hh) -> u32x4 {
-    return *(const u32x4*)&v_lds[buf][dt * 16 + l16][hh * 32 + grp * 8];
+    const int row = dt * 16 + l16;
+    return *(const u32x4*)&v_lds[buf][row][((hh * 4 + grp) ^ vswz(row)) * 8];
   };
   auto scores = [&](int buf, int hh, f32x4 (&sc)[2][NQ]) {
 #pragma unroll
