@@ -39,6 +39,19 @@ RGD_DEV float silu(float g) { return g / (1.0f + __expf(-g)); }
 
 constexpr int kStep = 64;  // k values per pipeline step
 
+// X stage layouts.  Swizzled (the projections and SwiGLU): unpadded rows of
+// XS * 64 k values whose 16-byte chunks are XOR-swizzled, chunk c of row r at
+// chunk c ^ xswz<XS>(r); the A fragment reads (16 consecutive rows at one chunk
+// per 16 lanes, the next lane group two chunks on) and the stage stores
+// (consecutive lanes along a row) are then free of LDS bank conflicts, which
+// the conflict counter put at 37-44% of the LDS cycles with padded rows (the
+// functions were chosen by measuring each access pattern under that counter;
+// 128-row tiles 3-15% faster).  Padded (the LM head, whose A fragment feeds
+// four MFMAs): rows padded by 16 bytes, unswizzled; the swizzled layout made
+// it 2-7% slower.
+template <int XS>
+RGD_DEV int xswz(int r) { return XS == 1 ? ((r & 7) ^ ((r >> 3) & 1)) : (r & 15); }
+
 // panels of N rows, rounded up to whole groups
 __host__ __device__ inline long long packed_panels(int N, int group) {
   return (long long)((N + 15) / 16 + group - 1) / group * group;
@@ -68,6 +81,7 @@ template <int MT, int NT, int NW, int SW, int MODE, int XS>
 __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
   constexpr int NTH = NW * 64, XSEG = MT * 16 * 8 * XS, XPT = (XSEG + NTH - 1) / NTH;
   static_assert(XS % SW == 0 || SW % XS == 0, "ring slots must stay static within an X stage");
+  static_assert(XS == 1 || XS == 2 || XS == 4, "the X-stage swizzle covers stages of 1, 2 or 4 steps");
   // wave index as a scalar: the panel and weight segment it selects are then
   // scalar too (a per-lane index into the arguments becomes a vector load of
   // the argument segment and a full memory round trip before the first weight
@@ -123,7 +137,8 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
 
   // LDS: the two X stage slots; the SwiGLU hand-over of the up sums (after
   // the main loop, behind a barrier) reuses the same bytes
-  using XStage = bf16_t[2][MT * 16][XS * kStep + 8];
+  constexpr bool XSW = MODE != GEMM_LOGITS;  // swizzled X stage (else padded)
+  using XStage = bf16_t[2][MT * 16][XS * kStep + (XSW ? 0 : 8)];
   constexpr int kUpWaves = (MODE == GEMM_SILU) ? HALF : 1;  // sized for SwiGLU only
   using UpSums = float[kUpWaves][MT * NT * 4][64];
   constexpr int kLdsBytes = sizeof(XStage) > sizeof(UpSums) ? (int)sizeof(XStage) : (int)sizeof(UpSums);
@@ -173,7 +188,8 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
 #pragma unroll
     for (int i = 0; i < XPT; ++i) {
       const int seg = threadIdx.x + i * NTH;
-      if (seg < XSEG) *(u32x4*)&xs[slot][seg / (8 * XS)][(seg % (8 * XS)) * 8] = xr[i];
+      const int row = seg / (8 * XS), c = seg % (8 * XS);
+      if (seg < XSEG) *(u32x4*)&xs[slot][row][(XSW ? c ^ xswz<XS>(row) : c) * 8] = xr[i];
     }
   };
 
@@ -203,7 +219,10 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmArgs a) {
         for (int h = 0; h < 2; ++h)
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) {
-            const u32x4 av = XG ? xa[j % SW][h] : *(const u32x4*)&xs[xsl][mt * 16 + col16][kk + kq + h * 8];
+            const int xc = (kk + kq + h * 8) >> 3;  // 16-byte chunk of the fragment
+            const u32x4 av = XG ? xa[j % SW][h]
+                                : *(const u32x4*)&xs[xsl][mt * 16 + col16]
+                                                   [(XSW ? xc ^ xswz<XS>(mt * 16 + col16) : xc) * 8];
 #pragma unroll
             for (int jj = 0; jj < NT; ++jj) acc[mt][jj] = mfma16x16x32(av, wb[j % SW][jj][h], acc[mt][jj]);
           }
